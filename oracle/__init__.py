@@ -1,0 +1,6 @@
+"""CPU oracle (test infrastructure only; never on the product path)."""
+from .rosa_oracle import (OracleModel, attention, gelu_tanh, modulate, rms_norm, silu,
+                          softmax_rows, tau_grid, timestep_embedding)
+
+__all__ = ["OracleModel", "attention", "gelu_tanh", "modulate", "rms_norm", "silu",
+           "softmax_rows", "tau_grid", "timestep_embedding"]
