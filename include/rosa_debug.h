@@ -1,0 +1,66 @@
+/*
+ * rosa_debug.h - component entry points of the rosa library, for tests and
+ * for per-kernel timing.  Same conventions as rosa.h: pure C, noexcept, status
+ * returns, asynchronous on the handle's stream unless stated otherwise.
+ */
+#ifndef ROSA_DEBUG_H_
+#define ROSA_DEBUG_H_
+
+#include "rosa.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Host-only planning of a request set (no GPU needed, nothing enqueued): runs
+ * the same validation and batch plan as rosa_generate_actions.
+ *   order[n]      : plan position -> caller index (requests sorted by K
+ *                   descending, stable), so the requests active at step k are a
+ *                   prefix of the plan
+ *   tok_off[n]    : first stacked action-token row of each request, by caller index
+ *   m_k[cap->max_steps] : stacked action tokens active at step k (0 past the last step)
+ *   counts[4]     : distinct flow times, attention work items, attention query
+ *                   groups, query groups whose keys are split over several items
+ * Any output pointer may be NULL.  Returns the status rosa_generate_actions
+ * would return for this set (ROSA_E_DEVICE never). */
+rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *cap,
+                            const rosa_request *reqs, int32_t n, int32_t *order,
+                            int32_t *tok_off, int32_t *m_k, int32_t *counts);
+
+/* Time conditioning alone: for n flow times taus (HOST fp32), write the
+ * modulation table rows to out (DEVICE fp32 [n][L*6d + 2d]): per layer l the
+ * six d-wide vectors [shift_a|scale_a|gate_a|shift_m|scale_m|gate_m] at offset
+ * l*6d, then the final [shift|scale] at L*6d.  n <= 128. */
+rosa_status rosa_debug_time_conditioning(rosa_batch *b, const float *taus, int32_t n, float *out);
+
+/* Attention of one layer alone.  qkv: DEVICE [sum H][(n_q+2n_kv)*head_dim] in
+ * the model dtype, the fused projection of each request's action tokens, rows
+ * stacked in the caller's request order; o: DEVICE [sum H][n_q*head_dim] model
+ * dtype, written.  Keys and values are the requests' prefix (layer `layer`)
+ * followed by the k/v columns of qkv, exactly as inside rosa_generate_actions. */
+rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_t n, int32_t layer,
+                                 const void *qkv, void *o);
+
+/* One projection alone, on M stacked rows (M <= max_action_tokens).
+ *   which = 0: out[M][Q]      = a[M][d] W_qkv[layer]                      (model dtype)
+ *   which = 1: out[M][d]     += gate[M][d] * (a[M][n_q*hd] W_o[layer])     (fp32)
+ *   which = 2: out[M][d_mlp]  = gelu_tanh(a[M][d] W_up[layer])             (model dtype)
+ *   which = 3: out[M][d]     += gate[M][d] * (a[M][d_mlp] W_down[layer])   (fp32)
+ * a is DEVICE in the model dtype; gate is DEVICE fp32 (ignored for 0 and 2). */
+rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const void *a, int32_t M,
+                            void *out, const float *gate);
+
+/* Per-kernel timing.  While enabled, every launch of the handle is bracketed
+ * by HIP events on the handle's stream and its duration is added to its
+ * kernel class.  rosa_debug_get_profile synchronizes the stream, then fills up
+ * to max entries of names (static strings), launch counts and total
+ * milliseconds, and sets *n_out.  Enabling clears the totals. */
+rosa_status rosa_debug_set_profiling(rosa_batch *b, int32_t enable);
+rosa_status rosa_debug_get_profile(rosa_batch *b, const char **names, int64_t *launches,
+                                   double *total_ms, int32_t max, int32_t *n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROSA_DEBUG_H_ */

@@ -1,0 +1,786 @@
+// C ABI of the rosa library: handle lifetime, validation, the batch plan and
+// the step loop that enqueues the kernels on the handle's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/rosa.h"
+#include "../../include/rosa_debug.h"
+#include "rosa_internal.h"
+
+using namespace rosa;
+
+namespace {
+
+constexpr int kSplitTarget = 512;   // attention work items wanted per call before keys are split
+constexpr int kMinSplitKeys = 256;  // smallest key range worth a separate work item
+constexpr int kMaxSlots = 2 * kSplitTarget;
+
+enum KernelClass {
+  kcTime = 0, kcSetup, kcInProj, kcModNorm, kcGemmQKV, kcAttention, kcMerge, kcGemmO, kcGemmUp,
+  kcGemmDown, kcFinal, kcCount
+};
+const char *kClassNames[kcCount] = {"time_conditioning", "setup_rows", "in_proj", "modnorm", "gemm_qkv",
+                                    "attention", "attn_merge", "gemm_o", "gemm_up", "gemm_down",
+                                    "final_euler"};
+
+thread_local std::string g_create_error;
+
+uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+struct Plan {
+  std::vector<int32_t> order;        // plan position -> caller index
+  std::vector<int32_t> tok_off;      // by plan position
+  std::vector<int32_t> m_k;          // per step
+  std::vector<int32_t> n_active;     // per step
+  std::vector<float> taus;
+  std::vector<int32_t> tau_idx;      // [max_K][n]
+  std::vector<AttnItem> items;
+  std::vector<AttnGroup> groups;
+  std::vector<int32_t> items_upto;   // items of plan requests [0, r]
+  std::vector<int32_t> groups_upto;
+  int M0 = 0, Kmax = 0;
+};
+
+}  // namespace
+
+struct rosa_batch {
+  rosa_model_config cfg{};
+  rosa_capacity cap{};
+  Dims dims{};
+  bool bf16 = true;
+  size_t esz = 2;
+  int device = 0;
+  hipStream_t stream = nullptr;
+  bool poisoned = false;
+  std::string last_error;
+
+  // weights on the device
+  float *w_in = nullptr, *b_in = nullptr, *b_t1 = nullptr, *b_t2 = nullptr, *b_modall = nullptr;
+  float *w_out = nullptr, *b_out = nullptr;
+  void *w_t1 = nullptr, *w_t2 = nullptr, *w_modall = nullptr;       // [K][N], activation dtype
+  void *wt_qkv = nullptr, *wt_o = nullptr, *wt_up = nullptr, *wt_down = nullptr;  // [L][N][K]
+
+  // workspaces
+  float *x = nullptr, *h = nullptr;
+  void *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr;
+  int32_t *row_req = nullptr, *rowmod = nullptr, *ident = nullptr;
+  float *modtab = nullptr, *emb = nullptr, *tc1 = nullptr, *tc2 = nullptr;
+  float *part_o = nullptr, *part_ml = nullptr;
+  int max_items = 0;
+
+  // plan buffers: device region + two pinned host staging copies
+  void *d_plan = nullptr;
+  void *h_plan[2] = {nullptr, nullptr};
+  hipEvent_t plan_copied[2] = {nullptr, nullptr};
+  bool plan_pending[2] = {false, false};
+  int plan_flip = 0;
+  size_t plan_bytes = 0;
+  size_t off_reqs = 0, off_tau_idx = 0, off_taus = 0, off_items = 0, off_groups = 0;
+
+  std::vector<void *> allocations;
+
+  // profiling
+  bool prof = false;
+  struct Pending { int cls; hipEvent_t a, b; };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> free_events;
+  int64_t prof_launches[kcCount] = {};
+  double prof_ms[kcCount] = {};
+};
+
+namespace {
+
+rosa_status fail(rosa_batch *b, rosa_status st, const std::string &msg) {
+  if (b) b->last_error = msg;
+  else g_create_error = msg;
+  return st;
+}
+
+rosa_status device_fail(rosa_batch *b, hipError_t e, const char *what) {
+  std::string msg = std::string(what) + ": " + hipGetErrorString(e);
+  if (b) {
+    b->poisoned = true;
+    b->last_error = msg;
+  } else {
+    g_create_error = msg;
+  }
+  return ROSA_E_DEVICE;
+}
+
+rosa_status check_config(const rosa_model_config *c) {
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 1 ||
+      c->d_mlp < 1 || c->action_dim < 1 || c->time_emb_dim < 2 || !(c->rms_eps >= 0.f))
+    return ROSA_E_INVALID;
+  if (c->dtype != ROSA_BF16 && c->dtype != ROSA_FP32) return ROSA_E_INVALID;
+  if (c->n_q_heads % c->n_kv_heads != 0) return ROSA_E_UNSUPPORTED;
+  if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
+    return ROSA_E_UNSUPPORTED;
+  if (c->d_model % 64 || c->d_mlp % 64 || (c->n_q_heads * c->head_dim) % 64) return ROSA_E_UNSUPPORTED;
+  if (c->d_model > 4096 || c->action_dim > 64 || c->time_emb_dim % 2 || c->time_emb_dim > 8192)
+    return ROSA_E_UNSUPPORTED;
+  return ROSA_OK;
+}
+
+rosa_status check_capacity(const rosa_capacity *c) {
+  if (c->max_requests < 1 || c->max_horizon < 1 || c->max_action_tokens < 1 || c->max_steps < 1 ||
+      c->max_prefix_tokens < 0)
+    return ROSA_E_INVALID;
+  if (c->max_steps > kMaxSteps) return ROSA_E_UNSUPPORTED;
+  return ROSA_OK;
+}
+
+Dims make_dims(const rosa_model_config *c) {
+  Dims d{};
+  d.L = c->n_layers; d.d = c->d_model; d.nq = c->n_q_heads; d.nkv = c->n_kv_heads; d.hd = c->head_dim;
+  d.dff = c->d_mlp; d.A = c->action_dim; d.dt = c->time_emb_dim;
+  d.qkv_dim = (d.nq + 2 * d.nkv) * d.hd;
+  d.o_dim = d.nq * d.hd;
+  d.mod_stride = d.L * 6 * d.d + 2 * d.d;
+  d.eps = c->rms_eps;
+  return d;
+}
+
+// Validation of a request set (all-or-nothing) and the batch plan.
+rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
+                       int n, bool sort_by_steps, bool allow_split, Plan &p, std::string &err) {
+  if (n < 0) { err = "n_reqs < 0"; return ROSA_E_INVALID; }
+  if (n > 0 && !reqs) { err = "reqs is NULL"; return ROSA_E_INVALID; }
+  if (n > cap->max_requests) { err = "more requests than max_requests"; return ROSA_E_CAPACITY; }
+  int64_t sumH = 0, sumP = 0;
+  for (int i = 0; i < n; ++i) {
+    const rosa_request &r = reqs[i];
+    char buf[160];
+    if (r.reserved != 0) { snprintf(buf, sizeof buf, "request %d: reserved != 0", i); err = buf; return ROSA_E_INVALID; }
+    if (r.prefix_len < 0 || r.horizon < 1 || r.num_steps < 1) {
+      snprintf(buf, sizeof buf, "request %d: P=%d H=%d K=%d out of range", i, r.prefix_len, r.horizon, r.num_steps);
+      err = buf; return ROSA_E_INVALID;
+    }
+    if (r.horizon > cap->max_horizon || r.num_steps > cap->max_steps) {
+      snprintf(buf, sizeof buf, "request %d: H=%d or K=%d above max_horizon=%d / max_steps=%d", i, r.horizon,
+               r.num_steps, cap->max_horizon, cap->max_steps);
+      err = buf; return ROSA_E_INVALID;
+    }
+    if (!r.noise || !r.actions || (r.prefix_len > 0 && (!r.prefix_k || !r.prefix_v))) {
+      snprintf(buf, sizeof buf, "request %d: NULL pointer", i); err = buf; return ROSA_E_INVALID;
+    }
+    sumH += r.horizon;
+    sumP += r.prefix_len;
+  }
+  if (sumH > cap->max_action_tokens) { err = "sum of horizons above max_action_tokens"; return ROSA_E_CAPACITY; }
+  if (sumP > cap->max_prefix_tokens) { err = "sum of prefix lengths above max_prefix_tokens"; return ROSA_E_CAPACITY; }
+
+  p = Plan();
+  p.order.resize(n);
+  for (int i = 0; i < n; ++i) p.order[i] = i;
+  if (sort_by_steps)
+    std::stable_sort(p.order.begin(), p.order.end(),
+                     [&](int a, int b) { return reqs[a].num_steps > reqs[b].num_steps; });
+  p.tok_off.resize(n);
+  int M = 0;
+  for (int i = 0; i < n; ++i) { p.tok_off[i] = M; M += reqs[p.order[i]].horizon; p.Kmax = std::max(p.Kmax, reqs[p.order[i]].num_steps); }
+  p.M0 = M;
+  p.m_k.assign(p.Kmax, 0);
+  p.n_active.assign(p.Kmax, 0);
+  for (int i = 0; i < n; ++i)
+    for (int k = 0; k < reqs[p.order[i]].num_steps; ++k) { p.m_k[k] += reqs[p.order[i]].horizon; p.n_active[k] += 1; }
+
+  // Distinct flow times tau = k / K (fp32 division) and each (step, request)'s index.
+  p.tau_idx.assign((size_t)p.Kmax * n, 0);
+  for (int i = 0; i < n; ++i) {
+    const int K = reqs[p.order[i]].num_steps;
+    for (int k = 0; k < K; ++k) {
+      const float tau = (float)k / (float)K;
+      int idx = -1;
+      for (size_t j = 0; j < p.taus.size(); ++j)
+        if (p.taus[j] == tau) { idx = (int)j; break; }
+      if (idx < 0) {
+        if ((int)p.taus.size() >= kMaxTau) { err = "more than 128 distinct flow times in one call"; return ROSA_E_CAPACITY; }
+        idx = (int)p.taus.size();
+        p.taus.push_back(tau);
+      }
+      p.tau_idx[(size_t)k * n + i] = idx;
+    }
+  }
+
+  // Attention work items: per request, KV head and block of kAttnQB query rows;
+  // keys split over several items only when the batch is too small to fill the GPU.
+  const int G = cfg->n_q_heads / cfg->n_kv_heads;
+  int64_t total_qb = 0;
+  for (int i = 0; i < n; ++i)
+    total_qb += (int64_t)cfg->n_kv_heads * ((reqs[i].horizon * G + kAttnQB - 1) / kAttnQB);
+  const bool split = allow_split && total_qb > 0 && total_qb < kSplitTarget;
+  int slots = 0;
+  p.items_upto.resize(n);
+  p.groups_upto.resize(n);
+  for (int i = 0; i < n; ++i) {
+    const rosa_request &r = reqs[p.order[i]];
+    const int nk = r.prefix_len + r.horizon;
+    const int nqb = (r.horizon * G + kAttnQB - 1) / kAttnQB;
+    int nsplit = 1, chunk = nk;
+    if (split) {
+      const int want = (int)((kSplitTarget + total_qb - 1) / total_qb);
+      const int most = std::max(1, (nk + kMinSplitKeys - 1) / kMinSplitKeys);
+      nsplit = std::min(want, most);
+      chunk = (nk + nsplit - 1) / nsplit;
+      chunk = (chunk + 63) / 64 * 64;          // whole 64-key tiles per item
+      nsplit = (nk + chunk - 1) / chunk;
+    }
+    for (int kvh = 0; kvh < cfg->n_kv_heads; ++kvh)
+      for (int qb = 0; qb < nqb; ++qb) {
+        if (nsplit > 1) {
+          AttnGroup gr{i, kvh, qb, slots, nsplit, 0, 0, 0};
+          p.groups.push_back(gr);
+        }
+        for (int c = 0; c < nsplit; ++c) {
+          AttnItem it{};
+          it.req = i; it.kvh = kvh; it.qb = qb;
+          it.kbeg = c * chunk;
+          it.kend = std::min(nk, (c + 1) * chunk);
+          it.slot = nsplit > 1 ? slots++ : -1;
+          p.items.push_back(it);
+        }
+      }
+    p.items_upto[i] = (int)p.items.size();
+    p.groups_upto[i] = (int)p.groups.size();
+  }
+  if (slots > kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
+  return ROSA_OK;
+}
+
+template <typename T>
+T *dalloc(rosa_batch *b, size_t count, hipError_t &e) {
+  void *ptr = nullptr;
+  if (e != hipSuccess) return nullptr;
+  e = hipMalloc(&ptr, std::max<size_t>(count * sizeof(T), 256));
+  if (e == hipSuccess) b->allocations.push_back(ptr);
+  return (T *)ptr;
+}
+
+// Upload a host fp32 tensor, converted to the activation dtype.
+hipError_t upload_act(rosa_batch *b, void *dst, const float *src, size_t n) {
+  if (!b->bf16) return hipMemcpy(dst, src, n * 4, hipMemcpyHostToDevice);
+  std::vector<uint16_t> tmp(n);
+  for (size_t i = 0; i < n; ++i) tmp[i] = f32_to_bf16_rne(src[i]);
+  return hipMemcpy(dst, tmp.data(), n * 2, hipMemcpyHostToDevice);
+}
+
+// Upload L stacked [K][N] matrices as [L][N][K] (transposed), activation dtype.
+hipError_t upload_transposed(rosa_batch *b, void *dst, const float *src, int L, int K, int N) {
+  const size_t per = (size_t)K * N;
+  std::vector<uint8_t> tmp(per * L * b->esz);
+  auto work = [&](int l) {
+    const float *s = src + per * l;
+    for (int k0 = 0; k0 < K; k0 += 64)
+      for (int n0 = 0; n0 < N; n0 += 64)
+        for (int n = n0; n < std::min(N, n0 + 64); ++n)
+          for (int k = k0; k < std::min(K, k0 + 64); ++k) {
+            const float v = s[(size_t)k * N + n];
+            const size_t di = per * l + (size_t)n * K + k;
+            if (b->bf16) reinterpret_cast<uint16_t *>(tmp.data())[di] = f32_to_bf16_rne(v);
+            else reinterpret_cast<float *>(tmp.data())[di] = v;
+          }
+  };
+  std::vector<std::thread> th;
+  const int nt = std::max(1, std::min(L, 8));
+  for (int t = 0; t < nt; ++t)
+    th.emplace_back([&, t] { for (int l = t; l < L; l += nt) work(l); });
+  for (auto &x : th) x.join();
+  return hipMemcpy(dst, tmp.data(), tmp.size(), hipMemcpyHostToDevice);
+}
+
+// Profiling helpers.
+hipEvent_t get_event(rosa_batch *b) {
+  if (!b->free_events.empty()) { hipEvent_t e = b->free_events.back(); b->free_events.pop_back(); return e; }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+hipError_t timed(rosa_batch *b, int cls, F &&launch) {
+  if (!b->prof) return launch();
+  hipEvent_t e0 = get_event(b), e1 = get_event(b);
+  if (!e0 || !e1) return launch();
+  hipEventRecord(e0, b->stream);
+  const hipError_t err = launch();
+  hipEventRecord(e1, b->stream);
+  b->pending.push_back({cls, e0, e1});
+  return err;
+}
+
+hipError_t harvest_profile(rosa_batch *b) {
+  hipError_t e = hipStreamSynchronize(b->stream);
+  if (e != hipSuccess) return e;
+  for (auto &p : b->pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      b->prof_ms[p.cls] += ms;
+      b->prof_launches[p.cls] += 1;
+    }
+    b->free_events.push_back(p.a);
+    b->free_events.push_back(p.b);
+  }
+  b->pending.clear();
+  return hipSuccess;
+}
+
+// Copy the plan through a pinned staging buffer into the device plan region.
+hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, int n) {
+  if ((int64_t)p.items.size() > b->max_items || (int64_t)p.groups.size() > kMaxSlots) return hipErrorInvalidValue;
+  const int slot = b->plan_flip;
+  b->plan_flip ^= 1;
+  if (b->plan_pending[slot]) {
+    hipError_t e = hipEventSynchronize(b->plan_copied[slot]);
+    if (e != hipSuccess) return e;
+  }
+  uint8_t *hp = (uint8_t *)b->h_plan[slot];
+  ReqDesc *rd = (ReqDesc *)(hp + b->off_reqs);
+  for (int i = 0; i < n; ++i) {
+    const rosa_request &r = reqs[p.order[i]];
+    ReqDesc d{};
+    d.pk = r.prefix_k; d.pv = r.prefix_v; d.noise = r.noise; d.actions = r.actions;
+    d.P = r.prefix_len; d.H = r.horizon; d.K = r.num_steps; d.tok_off = p.tok_off[i]; d.orig = p.order[i];
+    rd[i] = d;
+  }
+  std::memcpy(hp + b->off_tau_idx, p.tau_idx.data(), p.tau_idx.size() * 4);
+  std::memcpy(hp + b->off_taus, p.taus.data(), p.taus.size() * 4);
+  std::memcpy(hp + b->off_items, p.items.data(), p.items.size() * sizeof(AttnItem));
+  std::memcpy(hp + b->off_groups, p.groups.data(), p.groups.size() * sizeof(AttnGroup));
+  const size_t used = b->off_groups + p.groups.size() * sizeof(AttnGroup);
+  hipError_t e = hipMemcpyAsync(b->d_plan, hp, used, hipMemcpyHostToDevice, b->stream);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b->plan_copied[slot], b->stream);
+  b->plan_pending[slot] = true;
+  return e;
+}
+
+// Modulation table for the plan's distinct flow times.
+hipError_t run_time_conditioning(rosa_batch *b, const float *d_taus, int n_tau, float *out) {
+  const Dims &D = b->dims;
+  hipError_t e = timed(b, kcTime, [&] { return launch_time_embedding(d_taus, n_tau, D.dt, b->emb, b->stream); });
+  if (e == hipSuccess)
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->emb, n_tau, D.dt, b->w_t1, b->bf16, b->b_t1, D.d, 1, b->tc1, b->stream); });
+  if (e == hipSuccess)
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc1, n_tau, D.d, b->w_t2, b->bf16, b->b_t2, D.d, 1, b->tc2, b->stream); });
+  if (e == hipSuccess)
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc2, n_tau, D.d, b->w_modall, b->bf16, b->b_modall, D.mod_stride, 0, out, b->stream); });
+  return e;
+}
+
+hipError_t run_attention(rosa_batch *b, const Plan &p, int n_act, int layer, const void *qkv, void *o) {
+  const Dims &D = b->dims;
+  const ReqDesc *reqs = (const ReqDesc *)((uint8_t *)b->d_plan + b->off_reqs);
+  const AttnItem *items = (const AttnItem *)((uint8_t *)b->d_plan + b->off_items);
+  const AttnGroup *groups = (const AttnGroup *)((uint8_t *)b->d_plan + b->off_groups);
+  if (n_act <= 0) return hipSuccess;
+  AttnArgs a{};
+  a.items = items; a.n_items = p.items_upto[n_act - 1];
+  a.reqs = reqs; a.layer = layer;
+  a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
+  a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
+  a.part_o = b->part_o; a.part_ml = b->part_ml;
+  hipError_t e = timed(b, kcAttention, [&] { return launch_attention(a, b->bf16, b->stream); });
+  const int ng = p.groups_upto[n_act - 1];
+  if (e == hipSuccess && ng > 0)
+    e = timed(b, kcMerge, [&] {
+      return launch_attn_merge(groups, ng, reqs, b->part_o, b->part_ml, o, D.o_dim, D.nq, D.nkv, D.hd, b->bf16, b->stream);
+    });
+  return e;
+}
+
+void free_all(rosa_batch *b) {
+  for (void *ptr : b->allocations) hipFree(ptr);
+  b->allocations.clear();
+  for (int i = 0; i < 2; ++i) {
+    if (b->h_plan[i]) hipHostFree(b->h_plan[i]);
+    if (b->plan_copied[i]) hipEventDestroy(b->plan_copied[i]);
+  }
+  for (auto &p : b->pending) { hipEventDestroy(p.a); hipEventDestroy(p.b); }
+  for (auto e : b->free_events) hipEventDestroy(e);
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+
+extern "C" {
+
+const char *rosa_status_string(rosa_status s) {
+  switch (s) {
+    case ROSA_OK: return "ok";
+    case ROSA_E_INVALID: return "invalid argument";
+    case ROSA_E_CAPACITY: return "capacity exceeded";
+    case ROSA_E_NOMEM: return "out of memory";
+    case ROSA_E_DEVICE: return "device error";
+    case ROSA_E_UNSUPPORTED: return "unsupported shape";
+  }
+  return "unknown status";
+}
+
+const char *rosa_last_error(const rosa_batch *b) {
+  return b ? b->last_error.c_str() : g_create_error.c_str();
+}
+
+rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *w, const rosa_capacity *cap,
+                              void *hip_stream, rosa_batch **out) {
+  try {
+    g_create_error.clear();
+    if (!out) return fail(nullptr, ROSA_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (!cfg || !w || !cap) return fail(nullptr, ROSA_E_INVALID, "NULL config, weights or capacity");
+    rosa_status st = check_config(cfg);
+    if (st != ROSA_OK) return fail(nullptr, st, "model configuration not supported");
+    st = check_capacity(cap);
+    if (st != ROSA_OK) return fail(nullptr, st, "bad capacity");
+    const float *need[] = {w->w_in, w->b_in, w->w_t1, w->b_t1, w->w_t2, w->b_t2, w->w_mod, w->b_mod, w->w_qkv,
+                           w->w_o, w->w_up, w->w_down, w->w_fmod, w->b_fmod, w->w_out, w->b_out};
+    for (const float *p : need)
+      if (!p) return fail(nullptr, ROSA_E_INVALID, "NULL weight pointer");
+
+    rosa_batch *b = new rosa_batch();
+    b->cfg = *cfg;
+    b->cap = *cap;
+    b->dims = make_dims(cfg);
+    b->bf16 = cfg->dtype == ROSA_BF16;
+    b->esz = b->bf16 ? 2 : 4;
+    b->stream = (hipStream_t)hip_stream;
+    const Dims &D = b->dims;
+    hipError_t e = hipGetDevice(&b->device);
+    if (e != hipSuccess) { rosa_status s2 = device_fail(nullptr, e, "hipGetDevice"); delete b; return s2; }
+
+    const size_t L = D.L, d = D.d, maxM = cap->max_action_tokens;
+    // weights
+    b->w_in = dalloc<float>(b, (size_t)D.A * d, e);
+    b->b_in = dalloc<float>(b, d, e);
+    b->w_t1 = dalloc<uint8_t>(b, (size_t)D.dt * d * b->esz, e);
+    b->b_t1 = dalloc<float>(b, d, e);
+    b->w_t2 = dalloc<uint8_t>(b, d * d * b->esz, e);
+    b->b_t2 = dalloc<float>(b, d, e);
+    b->w_modall = dalloc<uint8_t>(b, d * D.mod_stride * b->esz, e);
+    b->b_modall = dalloc<float>(b, D.mod_stride, e);
+    b->wt_qkv = dalloc<uint8_t>(b, L * D.qkv_dim * d * b->esz, e);
+    b->wt_o = dalloc<uint8_t>(b, L * d * D.o_dim * b->esz, e);
+    b->wt_up = dalloc<uint8_t>(b, L * D.dff * d * b->esz, e);
+    b->wt_down = dalloc<uint8_t>(b, L * d * D.dff * b->esz, e);
+    b->w_out = dalloc<float>(b, d * D.A, e);
+    b->b_out = dalloc<float>(b, D.A, e);
+    // workspaces
+    b->x = dalloc<float>(b, maxM * D.A, e);
+    b->h = dalloc<float>(b, maxM * d, e);
+    b->u = dalloc<uint8_t>(b, maxM * d * b->esz, e);
+    b->qkv = dalloc<uint8_t>(b, maxM * D.qkv_dim * b->esz, e);
+    b->o = dalloc<uint8_t>(b, maxM * D.o_dim * b->esz, e);
+    b->g = dalloc<uint8_t>(b, maxM * D.dff * b->esz, e);
+    b->row_req = dalloc<int32_t>(b, maxM, e);
+    b->rowmod = dalloc<int32_t>(b, maxM * cap->max_steps, e);
+    b->ident = dalloc<int32_t>(b, maxM, e);
+    b->modtab = dalloc<float>(b, (size_t)kMaxTau * D.mod_stride, e);
+    b->emb = dalloc<float>(b, (size_t)kMaxTau * D.dt, e);
+    b->tc1 = dalloc<float>(b, (size_t)kMaxTau * d, e);
+    b->tc2 = dalloc<float>(b, (size_t)kMaxTau * d, e);
+    b->part_o = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * D.hd, e);
+    b->part_ml = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * 2, e);
+    // plan region
+    const int G = D.nq / D.nkv;
+    const int64_t qb_bound = (int64_t)D.nkv * (((int64_t)maxM * G + kAttnQB - 1) / kAttnQB + cap->max_requests);
+    b->max_items = (int)std::max<int64_t>(kMaxSlots + qb_bound, qb_bound);
+    auto align = [](size_t v) { return (v + 255) / 256 * 256; };
+    b->off_reqs = 0;
+    b->off_tau_idx = align(b->off_reqs + (size_t)cap->max_requests * sizeof(ReqDesc));
+    b->off_taus = align(b->off_tau_idx + (size_t)cap->max_requests * cap->max_steps * 4);
+    b->off_items = align(b->off_taus + kMaxTau * 4);
+    b->off_groups = align(b->off_items + (size_t)b->max_items * sizeof(AttnItem));
+    b->plan_bytes = align(b->off_groups + (size_t)kMaxSlots * sizeof(AttnGroup));
+    b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
+    if (e != hipSuccess) {
+      rosa_status s2 = e == hipErrorOutOfMemory ? fail(nullptr, ROSA_E_NOMEM, "device allocation failed")
+                                                 : device_fail(nullptr, e, "hipMalloc");
+      free_all(b); delete b; return s2;
+    }
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+      e = hipHostMalloc(&b->h_plan[i], b->plan_bytes, hipHostMallocDefault);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&b->plan_copied[i], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) { rosa_status s2 = fail(nullptr, ROSA_E_NOMEM, "pinned host allocation failed"); free_all(b); delete b; return s2; }
+
+    // upload weights
+    std::vector<float> modall(d * D.mod_stride), bmodall(D.mod_stride);
+    for (size_t l = 0; l < L; ++l)
+      for (size_t i = 0; i < d; ++i)
+        std::memcpy(&modall[i * D.mod_stride + l * 6 * d], w->w_mod + (l * d + i) * 6 * d, 6 * d * 4);
+    for (size_t i = 0; i < d; ++i)
+      std::memcpy(&modall[i * D.mod_stride + L * 6 * d], w->w_fmod + i * 2 * d, 2 * d * 4);
+    std::memcpy(bmodall.data(), w->b_mod, L * 6 * d * 4);
+    std::memcpy(bmodall.data() + L * 6 * d, w->b_fmod, 2 * d * 4);
+    if (e == hipSuccess) e = hipMemcpy(b->w_in, w->w_in, (size_t)D.A * d * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(b->b_in, w->b_in, d * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = upload_act(b, b->w_t1, w->w_t1, (size_t)D.dt * d);
+    if (e == hipSuccess) e = hipMemcpy(b->b_t1, w->b_t1, d * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = upload_act(b, b->w_t2, w->w_t2, d * d);
+    if (e == hipSuccess) e = hipMemcpy(b->b_t2, w->b_t2, d * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = upload_act(b, b->w_modall, modall.data(), modall.size());
+    if (e == hipSuccess) e = hipMemcpy(b->b_modall, bmodall.data(), bmodall.size() * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = upload_transposed(b, b->wt_qkv, w->w_qkv, D.L, D.d, D.qkv_dim);
+    if (e == hipSuccess) e = upload_transposed(b, b->wt_o, w->w_o, D.L, D.o_dim, D.d);
+    if (e == hipSuccess) e = upload_transposed(b, b->wt_up, w->w_up, D.L, D.d, D.dff);
+    if (e == hipSuccess) e = upload_transposed(b, b->wt_down, w->w_down, D.L, D.dff, D.d);
+    if (e == hipSuccess) e = hipMemcpy(b->w_out, w->w_out, d * D.A * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(b->b_out, w->b_out, D.A * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) {
+      std::vector<int32_t> id(maxM);
+      for (size_t i = 0; i < maxM; ++i) id[i] = (int32_t)i;
+      e = hipMemcpy(b->ident, id.data(), maxM * 4, hipMemcpyHostToDevice);
+    }
+    if (e != hipSuccess) { rosa_status s2 = device_fail(nullptr, e, "weight upload"); free_all(b); delete b; return s2; }
+    *out = b;
+    return ROSA_OK;
+  } catch (const std::bad_alloc &) {
+    return fail(nullptr, ROSA_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(nullptr, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32_t n) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    b->last_error.clear();
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned by an earlier device error");
+    Plan p;
+    std::string err;
+    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, true, b->bf16, p, err);
+    if (st != ROSA_OK) return fail(b, st, err);
+    if (n == 0) return ROSA_OK;
+    hipError_t e = hipSetDevice(b->device);
+    if (e == hipSuccess) e = upload_plan(b, p, reqs, n);
+    if (e != hipSuccess) return device_fail(b, e, "plan upload");
+    const Dims &D = b->dims;
+    uint8_t *dp = (uint8_t *)b->d_plan;
+    const ReqDesc *d_reqs = (const ReqDesc *)(dp + b->off_reqs);
+    const int32_t *d_tau_idx = (const int32_t *)(dp + b->off_tau_idx);
+    const float *d_taus = (const float *)(dp + b->off_taus);
+
+    e = run_time_conditioning(b, d_taus, (int)p.taus.size(), b->modtab);
+    if (e == hipSuccess)
+      e = timed(b, kcSetup, [&] {
+        return launch_setup_rows(d_reqs, n, d_tau_idx, p.Kmax, D.A, b->row_req, b->rowmod, p.M0, b->x, b->stream);
+      });
+    const size_t d6 = (size_t)6 * D.d;
+    for (int k = 0; k < p.Kmax && e == hipSuccess; ++k) {
+      const int M = p.m_k[k];
+      const int n_act = p.n_active[k];
+      const int32_t *rowmod = b->rowmod + (size_t)k * p.M0;
+      e = timed(b, kcInProj, [&] { return launch_in_proj(b->x, M, D.A, b->w_in, b->b_in, D.d, b->h, b->stream); });
+      for (int l = 0; l < D.L && e == hipSuccess; ++l) {
+        const int base = (int)(l * d6);
+        e = timed(b, kcModNorm, [&] {
+          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, b->u, b->bf16, b->stream);
+        });
+        if (e != hipSuccess) break;
+        GemmArgs g{};
+        g.a = b->u; g.lda = D.d; g.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * b->esz;
+        g.M = M; g.N = D.qkv_dim; g.K = D.d; g.epi = kEpiStore; g.out = b->qkv; g.ldo = D.qkv_dim;
+        e = timed(b, kcGemmQKV, [&] { return launch_gemm(g, b->bf16, b->stream); });
+        if (e != hipSuccess) break;
+        e = run_attention(b, p, n_act, l, b->qkv, b->o);
+        if (e != hipSuccess) break;
+        GemmArgs go{};
+        go.a = b->o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * b->esz;
+        go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = b->h; go.ldo = D.d;
+        go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
+        e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, b->stream); });
+        if (e != hipSuccess) break;
+        e = timed(b, kcModNorm, [&] {
+          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, b->u, b->bf16, b->stream);
+        });
+        if (e != hipSuccess) break;
+        GemmArgs gu{};
+        gu.a = b->u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * b->esz;
+        gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = b->g; gu.ldo = D.dff;
+        e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, b->stream); });
+        if (e != hipSuccess) break;
+        GemmArgs gd{};
+        gd.a = b->g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * b->esz;
+        gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = b->h; gd.ldo = D.d;
+        gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
+        e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, b->stream); });
+      }
+      if (e == hipSuccess)
+        e = timed(b, kcFinal, [&] {
+          return launch_final_euler(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, D.L * (int)d6, D.L * (int)d6 + D.d,
+                                    rowmod, b->w_out, b->b_out, D.A, b->row_req, d_reqs, k, b->x, b->stream);
+        });
+    }
+    if (e != hipSuccess) return device_fail(b, e, "kernel launch");
+    return ROSA_OK;
+  } catch (const std::bad_alloc &) {
+    return fail(b, ROSA_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+void rosa_destroy(rosa_batch *b) {
+  if (!b) return;
+  try {
+    hipSetDevice(b->device);
+    hipStreamSynchronize(b->stream);
+    free_all(b);
+  } catch (...) {
+  }
+  delete b;
+}
+
+// ---------------------------------------------------------------------- debug ABI
+
+rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
+                            int32_t n, int32_t *order, int32_t *tok_off, int32_t *m_k, int32_t *counts) {
+  try {
+    if (!cfg || !cap) return ROSA_E_INVALID;
+    rosa_status st = check_config(cfg);
+    if (st != ROSA_OK) return st;
+    st = check_capacity(cap);
+    if (st != ROSA_OK) return st;
+    Plan p;
+    std::string err;
+    st = build_plan(cfg, cap, reqs, n, true, cfg->dtype == ROSA_BF16, p, err);
+    if (st != ROSA_OK) return st;
+    for (int i = 0; i < n; ++i) {
+      if (order) order[i] = p.order[i];
+      if (tok_off) tok_off[p.order[i]] = p.tok_off[i];
+    }
+    if (m_k)
+      for (int k = 0; k < cap->max_steps; ++k) m_k[k] = k < p.Kmax ? p.m_k[k] : 0;
+    if (counts) {
+      counts[0] = (int32_t)p.taus.size();
+      counts[1] = (int32_t)p.items.size();
+      counts[2] = 0;
+      for (int i = 0; i < n; ++i) {
+        const int G = cfg->n_q_heads / cfg->n_kv_heads;
+        counts[2] += cfg->n_kv_heads * ((reqs[i].horizon * G + kAttnQB - 1) / kAttnQB);
+      }
+      counts[3] = (int32_t)p.groups.size();
+    }
+    return ROSA_OK;
+  } catch (...) {
+    return ROSA_E_NOMEM;
+  }
+}
+
+rosa_status rosa_debug_time_conditioning(rosa_batch *b, const float *taus, int32_t n, float *out) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned");
+    if (!taus || !out || n < 1 || n > kMaxTau) return fail(b, ROSA_E_INVALID, "bad taus/out/n");
+    hipError_t e = hipSetDevice(b->device);
+    float *d_taus = (float *)((uint8_t *)b->d_plan + b->off_taus);
+    if (e == hipSuccess) e = hipStreamSynchronize(b->stream);
+    if (e == hipSuccess) e = hipMemcpy(d_taus, taus, n * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = run_time_conditioning(b, d_taus, n, out);
+    if (e != hipSuccess) return device_fail(b, e, "time conditioning");
+    return ROSA_OK;
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_t n, int32_t layer,
+                                 const void *qkv, void *o) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned");
+    if (!qkv || !o || layer < 0 || layer >= b->dims.L) return fail(b, ROSA_E_INVALID, "bad qkv/o/layer");
+    Plan p;
+    std::string err;
+    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, false, b->bf16, p, err);
+    if (st != ROSA_OK) return fail(b, st, err);
+    if (n == 0) return ROSA_OK;
+    hipError_t e = hipSetDevice(b->device);
+    if (e == hipSuccess) e = upload_plan(b, p, reqs, n);
+    if (e == hipSuccess) e = run_attention(b, p, n, layer, qkv, o);
+    if (e != hipSuccess) return device_fail(b, e, "attention");
+    return ROSA_OK;
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const void *a, int32_t M, void *out,
+                            const float *gate) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned");
+    const Dims &D = b->dims;
+    if (which < 0 || which > 3 || layer < 0 || layer >= D.L || !a || !out || M < 0 ||
+        M > b->cap.max_action_tokens || ((which == 1 || which == 3) && !gate))
+      return fail(b, ROSA_E_INVALID, "bad gemm arguments");
+    GemmArgs g{};
+    g.a = a; g.M = M; g.out = out; g.gate = gate; g.rowmod = b->ident;
+    switch (which) {
+      case 0: g.lda = D.d; g.K = D.d; g.N = D.qkv_dim; g.epi = kEpiStore; g.ldo = D.qkv_dim;
+              g.wt = (uint8_t *)b->wt_qkv + (size_t)layer * D.qkv_dim * D.d * b->esz; break;
+      case 1: g.lda = D.o_dim; g.K = D.o_dim; g.N = D.d; g.epi = kEpiGatedResidual; g.ldo = D.d; g.gate_stride = D.d;
+              g.wt = (uint8_t *)b->wt_o + (size_t)layer * D.d * D.o_dim * b->esz; break;
+      case 2: g.lda = D.d; g.K = D.d; g.N = D.dff; g.epi = kEpiGelu; g.ldo = D.dff;
+              g.wt = (uint8_t *)b->wt_up + (size_t)layer * D.dff * D.d * b->esz; break;
+      default: g.lda = D.dff; g.K = D.dff; g.N = D.d; g.epi = kEpiGatedResidual; g.ldo = D.d; g.gate_stride = D.d;
+               g.wt = (uint8_t *)b->wt_down + (size_t)layer * D.d * D.dff * b->esz; break;
+    }
+    const int cls = which == 0 ? kcGemmQKV : which == 1 ? kcGemmO : which == 2 ? kcGemmUp : kcGemmDown;
+    hipError_t e = hipSetDevice(b->device);
+    if (e == hipSuccess) e = timed(b, cls, [&] { return launch_gemm(g, b->bf16, b->stream); });
+    if (e != hipSuccess) return device_fail(b, e, "gemm");
+    return ROSA_OK;
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_debug_set_profiling(rosa_batch *b, int32_t enable) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned");
+    hipError_t e = harvest_profile(b);
+    if (e != hipSuccess) return device_fail(b, e, "profile sync");
+    for (int i = 0; i < kcCount; ++i) { b->prof_ms[i] = 0.0; b->prof_launches[i] = 0; }
+    b->prof = enable != 0;
+    return ROSA_OK;
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_debug_get_profile(rosa_batch *b, const char **names, int64_t *launches, double *total_ms,
+                                   int32_t max, int32_t *n_out) {
+  if (!b) return ROSA_E_INVALID;
+  try {
+    if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned");
+    hipError_t e = harvest_profile(b);
+    if (e != hipSuccess) return device_fail(b, e, "profile sync");
+    const int n = std::min<int>(max, kcCount);
+    for (int i = 0; i < n; ++i) {
+      if (names) names[i] = kClassNames[i];
+      if (launches) launches[i] = b->prof_launches[i];
+      if (total_ms) total_ms[i] = b->prof_ms[i];
+    }
+    if (n_out) *n_out = n;
+    return ROSA_OK;
+  } catch (...) {
+    return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// Internal structures shared by the host planner and the kernels' launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rosa {
+
+// Per-request descriptor on the device (64 bytes), in plan order (K descending).
+struct ReqDesc {
+  const void *pk;        // prefix K, [L][P][n_kv][hd]
+  const void *pv;        // prefix V, same layout
+  const float *noise;    // [H][A]
+  float *actions;        // [H][A]
+  int32_t P, H, K, tok_off;
+  int32_t orig, pad0, pad1, pad2;
+};
+static_assert(sizeof(ReqDesc) == 64, "ReqDesc is 64 bytes");
+
+// One attention work item: query block `qb` (kAttnQB query rows) of KV head
+// `kvh` of request `req`, over keys [kbeg, kend) of the request's key sequence
+// (prefix keys first, then its action keys).  slot >= 0: write unnormalized
+// partial results to partial slot `slot`; slot < 0: write o directly.
+struct AttnItem {
+  int32_t req, kvh, qb, kbeg, kend, slot, pad0, pad1;
+};
+static_assert(sizeof(AttnItem) == 32, "AttnItem is 32 bytes");
+
+// A query block whose keys were split over n items starting at `first`
+// (partial slots first_slot .. first_slot + n - 1).
+struct AttnGroup {
+  int32_t req, kvh, qb, first_slot, n, pad0, pad1, pad2;
+};
+static_assert(sizeof(AttnGroup) == 32, "AttnGroup is 32 bytes");
+
+constexpr int kAttnQB = 128;       // query rows per attention work item (4 waves x 32)
+constexpr int kMaxTau = 128;       // distinct flow times per call
+constexpr int kMaxSteps = 64;
+
+// Dimensions a launch needs.
+struct Dims {
+  int L, d, nq, nkv, hd, dff, A, dt, qkv_dim, o_dim, mod_stride;
+  float eps;
+};
+
+enum Epilogue : int {
+  kEpiStore = 0,          // out = acc                      (activation dtype)
+  kEpiGelu = 1,           // out = gelu_tanh(acc)           (activation dtype)
+  kEpiGatedResidual = 2,  // h += gate[rowmod[m]][n] * acc  (fp32)
+};
+
+// ---------------------------------------------------------------- launchers
+// All return hipGetLastError() of the launch.  `bf16` selects the activation
+// and weight dtype (true: bf16, false: fp32).
+
+// Time conditioning.
+hipError_t launch_time_embedding(const float *taus, int n_tau, int dt, float *emb, hipStream_t s);
+// Y[n][N] = act(X[n][K] W[K][N] + b); act: 0 none, 1 SiLU.  W row-major [K][N].
+hipError_t launch_small_gemv(const float *X, int n, int K, const void *W, bool w_bf16, const float *b,
+                             int N, int act, float *Y, hipStream_t s);
+
+// Row kernels.
+hipError_t launch_setup_rows(const ReqDesc *reqs, int n_req, const int32_t *tau_idx, int max_steps,
+                             int A, int32_t *row_req, int32_t *rowmod, int M0, float *x, hipStream_t s);
+hipError_t launch_in_proj(const float *x, int M, int A, const float *w_in, const float *b_in, int d,
+                          float *h, hipStream_t s);
+hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *modtab, int mod_stride,
+                          int shift_off, int scale_off, const int32_t *rowmod, void *u, bool bf16,
+                          hipStream_t s);
+hipError_t launch_final_euler(const float *h, int M, int d, float eps, const float *modtab,
+                              int mod_stride, int shift_off, int scale_off, const int32_t *rowmod,
+                              const float *w_out, const float *b_out, int A, const int32_t *row_req,
+                              const ReqDesc *reqs, int step, float *x, hipStream_t s);
+
+// GEMM: C[M][N] = A[M][K] * W^T where Wt is [N][K] (K contiguous).
+struct GemmArgs {
+  const void *a; int lda;
+  const void *wt;            // [N][K]
+  int M, N, K;
+  int epi;
+  void *out; int ldo;        // kEpiStore / kEpiGelu: activation dtype; kEpiGatedResidual: fp32 h
+  const float *gate; int gate_stride; const int32_t *rowmod;  // gate = gate[rowmod[m]*gate_stride + n]
+};
+hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s);
+
+// Attention of one layer.
+struct AttnArgs {
+  const AttnItem *items; int n_items;
+  const ReqDesc *reqs;
+  int layer;
+  const void *qkv; int ldqkv;      // q at column g*hd, k_a at (nq+j)*hd, v_a at (nq+nkv+j)*hd
+  void *o; int ldo;                // o at column g*hd
+  int nq, nkv, hd;
+  float *part_o;                   // [slot][kAttnQB][hd] fp32
+  float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
+};
+hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
+hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
+                             const float *part_o, const float *part_ml, void *o, int ldo, int nq,
+                             int nkv, int hd, bool bf16, hipStream_t s);
+
+}  // namespace rosa

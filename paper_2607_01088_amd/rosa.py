@@ -1,0 +1,246 @@
+"""Python binding of the rosa C ABI (include/rosa.h, include/rosa_debug.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+library.  PyTorch supplies device memory and the stream.  The library must be
+built (``python -m paper_2607_01088_amd.build``); loading fails loudly if it
+is not.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librosa.so")
+
+ROSA_OK, ROSA_E_INVALID, ROSA_E_CAPACITY, ROSA_E_NOMEM, ROSA_E_DEVICE, ROSA_E_UNSUPPORTED = range(6)
+ROSA_BF16, ROSA_FP32 = 0, 1
+
+
+class ModelConfig(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_mlp", C.c_int32),
+                ("action_dim", C.c_int32), ("time_emb_dim", C.c_int32), ("rms_eps", C.c_float),
+                ("dtype", C.c_int32)]
+
+
+_WEIGHT_FIELDS = ["w_in", "b_in", "w_t1", "b_t1", "w_t2", "b_t2", "w_mod", "b_mod", "w_qkv", "w_o",
+                  "w_up", "w_down", "w_fmod", "b_fmod", "w_out", "b_out"]
+
+
+class Weights(C.Structure):
+    _fields_ = [(n, C.POINTER(C.c_float)) for n in _WEIGHT_FIELDS]
+
+
+class Capacity(C.Structure):
+    _fields_ = [("max_requests", C.c_int32), ("max_horizon", C.c_int32),
+                ("max_action_tokens", C.c_int32), ("max_steps", C.c_int32),
+                ("max_prefix_tokens", C.c_int64)]
+
+
+class Request(C.Structure):
+    _fields_ = [("prefix_k", C.c_void_p), ("prefix_v", C.c_void_p), ("noise", C.c_void_p),
+                ("actions", C.c_void_p), ("prefix_len", C.c_int32), ("horizon", C.c_int32),
+                ("num_steps", C.c_int32), ("reserved", C.c_int32)]
+
+
+class RosaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"rosa status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None) -> C.CDLL:
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    p = path or _LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"rosa HIP library not built: {p} is missing "
+                           "(run python -m paper_2607_01088_amd.build)")
+    lib = C.CDLL(p)
+    vp, i32, i64 = C.c_void_p, C.c_int32, C.c_int64
+    lib.rosa_batch_create.argtypes = [C.POINTER(ModelConfig), C.POINTER(Weights), C.POINTER(Capacity), vp,
+                                      C.POINTER(vp)]
+    lib.rosa_batch_create.restype = C.c_int
+    lib.rosa_generate_actions.argtypes = [vp, C.POINTER(Request), i32]
+    lib.rosa_generate_actions.restype = C.c_int
+    lib.rosa_destroy.argtypes = [vp]
+    lib.rosa_destroy.restype = None
+    lib.rosa_status_string.argtypes = [C.c_int]
+    lib.rosa_status_string.restype = C.c_char_p
+    lib.rosa_last_error.argtypes = [vp]
+    lib.rosa_last_error.restype = C.c_char_p
+    lib.rosa_debug_plan.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32,
+                                    C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)]
+    lib.rosa_debug_plan.restype = C.c_int
+    lib.rosa_debug_time_conditioning.argtypes = [vp, C.POINTER(C.c_float), i32, vp]
+    lib.rosa_debug_time_conditioning.restype = C.c_int
+    lib.rosa_debug_attention.argtypes = [vp, C.POINTER(Request), i32, i32, vp, vp]
+    lib.rosa_debug_attention.restype = C.c_int
+    lib.rosa_debug_gemm.argtypes = [vp, i32, i32, vp, i32, vp, vp]
+    lib.rosa_debug_gemm.restype = C.c_int
+    lib.rosa_debug_set_profiling.argtypes = [vp, i32]
+    lib.rosa_debug_set_profiling.restype = C.c_int
+    lib.rosa_debug_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64), C.POINTER(C.c_double),
+                                           i32, C.POINTER(i32)]
+    lib.rosa_debug_get_profile.restype = C.c_int
+    _lib = lib
+    return lib
+
+
+def model_config(shape, dtype: str) -> ModelConfig:
+    return ModelConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                       shape.d_mlp, shape.action_dim, shape.time_emb_dim, shape.rms_eps,
+                       ROSA_BF16 if dtype == "bf16" else ROSA_FP32)
+
+
+def capacity(max_requests: int, max_horizon: int, max_action_tokens: int, max_steps: int,
+             max_prefix_tokens: int) -> Capacity:
+    return Capacity(max_requests, max_horizon, max_action_tokens, max_steps, max_prefix_tokens)
+
+
+def _f32_ptr(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_float))
+
+
+def request_struct(prefix_k, prefix_v, noise, actions, P: int, H: int, K: int, reserved: int = 0) -> Request:
+    """Build a request from torch device tensors (or raw integer device pointers)."""
+    def ptr(t):
+        if t is None:
+            return None
+        return t if isinstance(t, int) else t.data_ptr()
+    return Request(ptr(prefix_k), ptr(prefix_v), ptr(noise), ptr(actions), P, H, K, reserved)
+
+
+def request_array(reqs: Sequence[Request]):
+    arr = (Request * max(1, len(reqs)))()
+    for i, r in enumerate(reqs):
+        arr[i] = r
+    return arr
+
+
+def plan(shape, dtype: str, cap: Capacity, reqs: Sequence[Request]):
+    """Host-only planning (rosa_debug_plan): (status, order, tok_off, m_k, counts)."""
+    lib = load()
+    cfg = model_config(shape, dtype)
+    n = len(reqs)
+    arr = request_array(reqs)
+    order = (C.c_int32 * max(1, n))()
+    tok = (C.c_int32 * max(1, n))()
+    mk = (C.c_int32 * max(1, cap.max_steps))()
+    counts = (C.c_int32 * 4)()
+    st = lib.rosa_debug_plan(C.byref(cfg), C.byref(cap), arr, n, order, tok, mk, counts)
+    return st, list(order)[:n], list(tok)[:n], list(mk)[:cap.max_steps], list(counts)
+
+
+class ActionExpert:
+    """A rosa_batch handle: the action expert's weights on the GPU plus workspaces."""
+
+    def __init__(self, shape, dtype: str, weights: Dict[str, np.ndarray], cap: Capacity,
+                 stream: Optional[int] = None):
+        import torch
+        self.lib = load()
+        self.shape, self.dtype, self.cap = shape, dtype, cap
+        self._cfg = model_config(shape, dtype)
+        self._host = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in _WEIGHT_FIELDS}
+        w = Weights(*[_f32_ptr(self._host[k]) for k in _WEIGHT_FIELDS])
+        if stream is None:
+            stream = torch.cuda.current_stream().cuda_stream
+        self.stream = stream
+        h = C.c_void_p()
+        st = self.lib.rosa_batch_create(C.byref(self._cfg), C.byref(w), C.byref(cap), C.c_void_p(stream),
+                                        C.byref(h))
+        self._host = None   # the library copied what it needs
+        if st != ROSA_OK:
+            raise RosaError(st, self.lib.rosa_last_error(None).decode())
+        self.handle = h
+
+    def _check(self, st: int):
+        if st != ROSA_OK:
+            raise RosaError(st, self.lib.rosa_last_error(self.handle).decode())
+
+    def generate(self, reqs: Sequence[Request]) -> int:
+        """Enqueue rosa_generate_actions; returns the status (raises on error)."""
+        arr = request_array(reqs)
+        st = self.lib.rosa_generate_actions(self.handle, arr, len(reqs))
+        self._check(st)
+        return st
+
+    def generate_status(self, reqs: Sequence[Request]) -> int:
+        """Like generate but returns the status instead of raising."""
+        arr = request_array(reqs)
+        return self.lib.rosa_generate_actions(self.handle, arr, len(reqs))
+
+    def time_conditioning(self, taus: Sequence[float], out) -> None:
+        t = (C.c_float * len(taus))(*taus)
+        self._check(self.lib.rosa_debug_time_conditioning(self.handle, t, len(taus), out.data_ptr()))
+
+    def attention(self, reqs: Sequence[Request], layer: int, qkv, o) -> None:
+        arr = request_array(reqs)
+        self._check(self.lib.rosa_debug_attention(self.handle, arr, len(reqs), layer, qkv.data_ptr(),
+                                                  o.data_ptr()))
+
+    def gemm(self, which: int, layer: int, a, M: int, out, gate=None) -> None:
+        self._check(self.lib.rosa_debug_gemm(self.handle, which, layer, a.data_ptr(), M, out.data_ptr(),
+                                             None if gate is None else gate.data_ptr()))
+
+    def set_profiling(self, enable: bool) -> None:
+        self._check(self.lib.rosa_debug_set_profiling(self.handle, 1 if enable else 0))
+
+    def profile(self) -> Dict[str, tuple]:
+        n = 32
+        names = (C.c_char_p * n)()
+        launches = (C.c_int64 * n)()
+        ms = (C.c_double * n)()
+        cnt = C.c_int32()
+        self._check(self.lib.rosa_debug_get_profile(self.handle, names, launches, ms, n, C.byref(cnt)))
+        return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(cnt.value)}
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self.lib.rosa_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- device upload helpers
+
+def to_device_kv(arr: np.ndarray, dtype: str, device="cuda"):
+    """Prefix KV array (uint16 bf16 bits or float32) -> torch device tensor."""
+    import torch
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32))
+    return t.to(device)
+
+
+class DeviceBatch:
+    """A list of requests uploaded to the GPU (prefix KV resident), with output
+    buffers, and the request structs that point at them."""
+
+    def __init__(self, requests, dtype: str, device="cuda"):
+        import torch
+        self.k, self.v, self.noise, self.actions, self.structs = [], [], [], [], []
+        for r in requests:
+            k = to_device_kv(r.prefix_k, dtype, device) if r.prefix_len > 0 else None
+            v = to_device_kv(r.prefix_v, dtype, device) if r.prefix_len > 0 else None
+            nz = torch.from_numpy(np.ascontiguousarray(r.noise, dtype=np.float32)).to(device)
+            out = torch.full_like(nz, float("nan"))
+            self.k.append(k); self.v.append(v); self.noise.append(nz); self.actions.append(out)
+            self.structs.append(request_struct(k, v, nz, out, r.prefix_len, r.horizon, r.steps))
+
+    def results(self) -> List[np.ndarray]:
+        return [a.cpu().numpy() for a in self.actions]

@@ -1,0 +1,125 @@
+"""Host-side checks of the C ABI: the library loads and exports every declared
+function, validation is all-or-nothing with the documented status codes, and
+the batch plan (K-descending order, token offsets, active tokens per step,
+distinct flow times) is right.  No GPU needed."""
+import ctypes as C
+
+import pytest
+
+from paper_2607_01088_amd import rosa
+from synthetic import PI0_SHAPE, TINY_SHAPE
+from tests.helpers import declared_functions
+
+FAKE = 0x1000   # non-NULL device address; host planning never dereferences it
+
+
+def req(P, H, K, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, reserved=0):
+    return rosa.request_struct(k, v, noise, out, P, H, K, reserved)
+
+
+def test_library_exports_every_declared_function():
+    lib = rosa.load()
+    names = declared_functions()
+    assert "rosa_batch_create" in names and "rosa_generate_actions" in names and "rosa_destroy" in names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    lib = rosa.load()
+    for s in range(6):
+        assert lib.rosa_status_string(s)
+    assert lib.rosa_status_string(99) == b"unknown status"
+
+
+def test_create_rejects_null_and_bad_shapes_before_touching_the_gpu():
+    lib = rosa.load()
+    h = C.c_void_p()
+    assert lib.rosa_batch_create(None, None, None, None, C.byref(h)) == rosa.ROSA_E_INVALID
+    assert not h.value
+    cfg = rosa.model_config(TINY_SHAPE, "fp32")
+    cap = rosa.capacity(2, 8, 16, 4, 200)
+    w = rosa.Weights()
+    assert lib.rosa_batch_create(C.byref(cfg), C.byref(w), C.byref(cap), None, C.byref(h)) == rosa.ROSA_E_INVALID
+    cfg.head_dim = 48
+    assert lib.rosa_batch_create(C.byref(cfg), C.byref(w), C.byref(cap), None, C.byref(h)) \
+        == rosa.ROSA_E_UNSUPPORTED
+    assert lib.rosa_last_error(None)
+    assert lib.rosa_generate_actions(None, None, 0) == rosa.ROSA_E_INVALID
+    lib.rosa_destroy(None)   # NULL-safe
+
+
+def _plan(reqs, cap=None, shape=PI0_SHAPE, dtype="bf16"):
+    cap = cap or rosa.capacity(16, 50, 400, 10, 100000)
+    return rosa.plan(shape, dtype, cap, reqs)
+
+
+def test_plan_sorts_by_steps_and_prefixes_active_tokens():
+    reqs = [req(1000, 16, 5), req(2000, 50, 10), req(0, 16, 10), req(700, 50, 5)]
+    st, order, tok, mk, counts = _plan(reqs)
+    assert st == rosa.ROSA_OK
+    assert order == [1, 2, 0, 3]                         # K descending, stable
+    assert tok == [66, 0, 50, 82]                        # offsets follow the plan order
+    assert mk == [132] * 5 + [66] * 5
+    n_tau, n_items, n_qb, n_split = counts
+    assert n_tau == 10                                   # {k/5} is a subset of {k/10}
+    assert n_qb == 1 + 4 + 1 + 4                         # ceil(8H/128) per request
+    # a small batch splits long key ranges (>= 256 keys per item); short ones stay whole
+    assert n_items > n_qb and n_split > 0
+
+
+def test_plan_distinct_taus_counts_fp32_division():
+    reqs = [req(1, 2, 3), req(1, 2, 4), req(1, 2, 6)]
+    st, _, _, _, counts = _plan(reqs)
+    assert st == rosa.ROSA_OK
+    taus = {k / K for K in (3, 4, 6) for k in range(K)}
+    import numpy as np
+    taus32 = {float(np.float32(k) / np.float32(K)) for K in (3, 4, 6) for k in range(K)}
+    assert counts[0] == len(taus32) == len(taus)
+
+
+def test_plan_no_split_for_a_full_batch():
+    reqs = [req(600, 50, 10) for _ in range(160)]       # 640 query blocks >= split target
+    cap = rosa.capacity(256, 50, 256 * 50, 10, 256 * 2048)
+    st, _, _, _, counts = _plan(reqs, cap)
+    assert st == rosa.ROSA_OK
+    assert counts[1] == counts[2] == 640 and counts[3] == 0
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(P=-1), rosa.ROSA_E_INVALID),
+    (dict(H=0), rosa.ROSA_E_INVALID),
+    (dict(H=51), rosa.ROSA_E_INVALID),
+    (dict(K=0), rosa.ROSA_E_INVALID),
+    (dict(K=11), rosa.ROSA_E_INVALID),
+    (dict(noise=None), rosa.ROSA_E_INVALID),
+    (dict(out=None), rosa.ROSA_E_INVALID),
+    (dict(k=None), rosa.ROSA_E_INVALID),
+    (dict(reserved=1), rosa.ROSA_E_INVALID),
+])
+def test_plan_validation_all_or_nothing(bad, status):
+    args = dict(P=10, H=16, K=5, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, reserved=0)
+    args.update(bad)
+    good = req(5, 8, 5)
+    bad_req = req(args["P"], args["H"], args["K"], args["k"], args["v"], args["noise"], args["out"], args["reserved"])
+    st, *_ = _plan([good, bad_req, good])
+    assert st == status
+
+
+def test_plan_null_prefix_allowed_when_empty():
+    st, *_ = _plan([req(0, 8, 2, k=None, v=None)])
+    assert st == rosa.ROSA_OK
+
+
+def test_plan_capacity_limits():
+    cap = rosa.capacity(2, 50, 60, 10, 1000)
+    assert _plan([req(10, 8, 2)] * 3, cap)[0] == rosa.ROSA_E_CAPACITY          # too many requests
+    assert _plan([req(10, 50, 2), req(10, 16, 2)], cap)[0] == rosa.ROSA_E_CAPACITY  # sum H
+    assert _plan([req(600, 8, 2), req(600, 8, 2)], cap)[0] == rosa.ROSA_E_CAPACITY  # sum P
+    assert _plan([], cap)[0] == rosa.ROSA_OK
+
+
+def test_plan_too_many_distinct_taus():
+    cap = rosa.capacity(64, 8, 512, 64, 1000)
+    reqs = [req(1, 1, K) for K in range(40, 64)]
+    assert _plan(reqs, cap, shape=TINY_SHAPE)[0] == rosa.ROSA_E_CAPACITY
