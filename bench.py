@@ -1,0 +1,245 @@
+"""Benchmark: batched action-chunk generation on one MI355X.
+
+One step = one rosa_generate_actions call over the whole factory-fleet batch
+(256 ragged robot requests, pi0-shaped action expert, bf16): every request runs
+its own 5 or 10 Euler steps over 18 layers with attention over its own cached
+prefix.  Prefix KV, noise and weights are resident in HBM before timing.
+
+Prints one JSON line (rank 0): throughput in action chunks/s, p50/p99 batch
+latency, the roofline of the dominant kernel (timed live with HIP events on
+the library's stream), and the CPU oracle timed on this host's cores on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFS = 2500.0    # MI355X dense bf16 MFMA
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def algorithmic_work(shape, reqs):
+    """Per-call algorithmic work by kernel class, from the request shapes.
+
+    GEMM flops: 2 * rows * (in * out) for the four projections of every layer
+    at every step.  Attention: prefix K and V bytes streamed once per
+    layer-step (L * 2 * n_kv * hd * 2 bytes per prefix token), and
+    4 * n_q * hd * H * (P + H) flops per layer-step."""
+    L, d, nq, nkv, hd, dff = (shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
+                              shape.head_dim, shape.d_mlp)
+    qkv = (nq + 2 * nkv) * hd
+    tok_steps = sum(r.horizon * r.steps for r in reqs)
+    w = {
+        "gemm_qkv": 2.0 * tok_steps * d * qkv * L,
+        "gemm_o": 2.0 * tok_steps * nq * hd * d * L,
+        "gemm_up": 2.0 * tok_steps * d * dff * L,
+        "gemm_down": 2.0 * tok_steps * dff * d * L,
+    }
+    attn_bytes = sum(r.prefix_len * r.steps for r in reqs) * L * 2 * nkv * hd * 2
+    attn_flops = sum(4.0 * nq * hd * r.horizon * (r.prefix_len + r.horizon) * r.steps for r in reqs) * L
+    return w, float(attn_bytes), float(attn_flops), tok_steps
+
+
+def kernel_source_hash(name: str) -> str:
+    src = {"attention": "k_attn.hip"}.get(name, "k_gemm.hip")
+    with open(os.path.join(ROOT, "paper_2607_01088_amd", "csrc", src), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(name: str, launches_per_call: float):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel source."""
+    path = os.path.join(PROFILES, f"traffic_{name}_factory_b256.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha") != kernel_source_hash(name):
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(preset, weights, reqs_meta, budget_s: float):
+    """The oracle on a stratified sample of the workload's requests; its
+    throughput is extrapolated to the whole batch by algorithmic GEMM +
+    attention flops (the oracle's cost is additive over requests)."""
+    from oracle import OracleModel
+    from synthetic import make_requests
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    cores = len(os.sched_getaffinity(0))
+    om = OracleModel(weights, preset.shape)
+    classes = {}
+    for i, m in enumerate(reqs_meta):
+        classes.setdefault((m.horizon, m.steps), []).append(i)
+    order = []
+    pools = [sorted(v) for _, v in sorted(classes.items())]
+    for j in range(max(len(p) for p in pools)):
+        for p in pools:
+            if j < len(p):
+                order.append(p[j])
+
+    def flops(m):
+        sh = preset.shape
+        per_tok = 2.0 * sh.n_layers * (sh.d_model * sh.qkv_dim + sh.n_q_heads * sh.head_dim * sh.d_model
+                                       + 2 * sh.d_model * sh.d_mlp)
+        att = 4.0 * sh.n_layers * sh.n_q_heads * sh.head_dim * m.horizon * (m.prefix_len + m.horizon)
+        return (per_tok * m.horizon + att) * m.steps
+
+    done, t_used = [], 0.0
+    for i in order:
+        r = make_requests(preset, indices=[i], threads=1)[0]
+        t0 = time.perf_counter()
+        om.generate([r])
+        t_used += time.perf_counter() - t0
+        done.append(i)
+        if t_used >= budget_s and len(done) >= len(pools):
+            break
+    f_sample = sum(flops(reqs_meta[i]) for i in done)
+    f_total = sum(flops(m) for m in reqs_meta)
+    batch_s = t_used * f_total / f_sample
+    return {
+        "value": len(reqs_meta) / batch_s,
+        "unit": "chunks/s",
+        "cores": int(max(1, min(cores, blas_threads))) if blas_threads > 1 else 1,
+        "host_cores_available": cores,
+        "blas_threads": int(blas_threads),
+        "kind": "oracle",
+        "sample": (f"{len(done)} of {len(reqs_meta)} requests (stratified over horizon x steps), "
+                   f"{t_used:.1f} s measured, scaled to the whole batch by algorithmic flops "
+                   f"(extrapolated batch time {batch_s:.1f} s); NumPy float64"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="factory_b256")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported in this build "
+              "(requests shard across GPUs with no exchange; see DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_01088_amd import rosa
+    from synthetic import PRESETS, make_metadata, make_requests, make_weights
+
+    preset = PRESETS[args.workload]
+    t0 = time.time()
+    weights = make_weights(preset.shape, preset.dtype)
+    meta = make_metadata(preset)
+    reqs = make_requests(preset, threads=16)
+    print(f"[bench] generated inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    cap = rosa.capacity(len(reqs), max(r.horizon for r in reqs), sum(r.horizon for r in reqs),
+                        max(r.steps for r in reqs), sum(r.prefix_len for r in reqs))
+    expert = rosa.ActionExpert(preset.shape, preset.dtype, weights, cap)
+    db = rosa.DeviceBatch(reqs, preset.dtype)
+    kv_bytes = sum(k.numel() * k.element_size() * 2 for k in db.k if k is not None)
+    torch.cuda.synchronize()
+    print(f"[bench] uploaded (prefix KV {kv_bytes / 1e9:.2f} GB resident)", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        expert.generate(db.structs)
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for a, b in evs:
+        a.record(stream)
+        expert.generate(db.structs)
+        b.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    lat = np.array([a.elapsed_time(b) for a, b in evs])
+    print(f"[bench] timed {args.steps} calls: {elapsed:.3f} s", file=sys.stderr, flush=True)
+
+    # Per-kernel durations, live, with HIP events on the library's stream.
+    expert.set_profiling(True)
+    n_prof = 2
+    for _ in range(n_prof):
+        expert.generate(db.structs)
+    prof = expert.profile()
+    expert.set_profiling(False)
+
+    gemm_flops, attn_bytes, attn_flops, tok_steps = algorithmic_work(preset.shape, reqs)
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        if launches == 0:
+            continue
+        per_call_launches = launches / n_prof
+        avg_ms = ms / launches
+        entry = {"launches_per_call": per_call_launches, "avg_launch_ms": avg_ms, "ms_per_call": ms / n_prof}
+        if name in gemm_flops:
+            per_launch = gemm_flops[name] / per_call_launches
+            ach = per_launch / (avg_ms * 1e-3) / 1e12
+            entry.update({"bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                          "frac": ach / MFMA_BF16_PEAK_TFS})
+        elif name == "attention":
+            per_launch = attn_bytes / per_call_launches
+            ach = per_launch / (avg_ms * 1e-3) / 1e9
+            entry.update({"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": ach / HBM_PEAK_GBS,
+                          "mfma_tflops": attn_flops / per_call_launches / (avg_ms * 1e-3) / 1e12})
+        kernels[name] = entry
+    dom = max((k for k in kernels if "bound" in kernels[k]), key=lambda k: kernels[k]["ms_per_call"])
+    d = kernels[dom]
+    roofline = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 2), "peak": d["peak"],
+                "unit": d["unit"], "frac": round(d["frac"], 4),
+                "traffic": load_traffic(dom, d["launches_per_call"])}
+    gemm_total_ms = sum(kernels[k]["ms_per_call"] for k in gemm_flops if k in kernels)
+    gemm_all = sum(gemm_flops.values()) / (gemm_total_ms * 1e-3) / 1e12
+
+    B = len(reqs)
+    ms_per_step = elapsed / args.steps * 1e3
+    value = B * args.steps / elapsed
+    out = {
+        "metric": "action chunks/sec + p50/p99 batch latency at B=256; % HBM and MFMA peak",
+        "value": round(value, 2),
+        "unit": "chunks/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": preset.name, "requests": B,
+                   "action_tokens": int(sum(r.horizon for r in reqs)),
+                   "prefix_tokens": int(sum(r.prefix_len for r in reqs)),
+                   "token_steps": int(tok_steps)},
+        "actions_per_s": round(sum(r.horizon for r in reqs) * args.steps / elapsed, 1),
+        "p50_ms": round(float(np.percentile(lat, 50)), 3),
+        "p99_ms": round(float(np.percentile(lat, 99)), 3),
+        "roofline": roofline,
+        "gemm_all": {"achieved": round(gemm_all, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                     "frac": round(gemm_all / MFMA_BF16_PEAK_TFS, 4)},
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kernels.items()},
+        "prefix_kv_gb": round(kv_bytes / 1e9, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(preset, weights, meta, args.cpu_budget)
+    expert.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

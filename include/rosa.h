@@ -61,7 +61,7 @@ typedef enum rosa_dtype {
 
 /* Model shape.  Constraints (else ROSA_E_UNSUPPORTED): n_q_heads % n_kv_heads == 0;
  * head_dim in {32, 64, 128, 256}; d_model, d_mlp and n_q_heads*head_dim multiples
- * of 64; d_model <= 8192; 1 <= action_dim <= 64; time_emb_dim even and <= 8192. */
+ * of 128; d_model <= 4096; 1 <= action_dim <= 64; time_emb_dim even and <= 8192. */
 typedef struct rosa_model_config {
   int32_t n_layers;
   int32_t d_model;

@@ -27,10 +27,19 @@
 namespace rosa {
 
 namespace at {
-constexpr int TK = 64;   // keys per LDS tile
-}
+constexpr int TK = 32;   // keys per LDS stage
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// Chunk swizzle of LDS rows: 16-byte chunk c of row r is stored at c ^ swz(r),
+// swz(r) = the two 2-bit halves of r % 16 swapped.  The 16 consecutive rows
+// that one 16-lane group reads at one chunk (K operand), and the 4 rows x 4
+// chunks that the transpose reads of a 32-lane half touch (V operand), then
+// fall in distinct bank groups.
+__device__ __forceinline__ int swz(int r, int cpr) { return (((r & 3) << 2) | ((r >> 2) & 3)) & (cpr - 1); }
+}  // namespace at
 
-__device__ __forceinline__ bf16x8 lds_tr_pair(const bf16 *p0, const bf16 *p1) {
+#define ROSA_LDS_A(p) ((__attribute__((address_space(3))) void *)(p))
+
+__device__ __forceinline__ bf16x8 lds_tr_pair(const uint8_t *p0, const uint8_t *p1) {
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
   const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p0));
   const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p1));
@@ -40,21 +49,53 @@ __device__ __forceinline__ bf16x8 lds_tr_pair(const bf16 *p0, const bf16 *p1) {
 }
 
 template <int HD>
-__global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
+struct AttnTile {
+  static constexpr int ROWB = HD * 2;             // bytes per K or V row
+  static constexpr int CPR = ROWB / 16;           // 16-byte chunks per row
+  static constexpr int TILEB = 32 * ROWB;         // bytes of one 32-key K (or V) tile
+  static constexpr int UNITS = 2 * TILEB / 1024;  // 1 KB copies per stage (K then V)
+  static constexpr int CPW = 2 * ((UNITS / 2 + 3) / 4);   // copies per copying wave per stage
+  static constexpr int RPU = 1024 / ROWB;         // rows per 1 KB copy
+  // A wave copies CPW units of a stage or none, so waiting until at most
+  // 2 CPW copies are outstanding leaves exactly the two next stages in flight.
+  static constexpr int WAIT = at::waitcnt_vm(2 * CPW);
+  static constexpr int WAIT0 = at::waitcnt_vm(0);
+  static_assert((UNITS / 2) % 4 == 0 || UNITS / 2 < 4, "copy split");
+};
+
+// Maps block b to a work item so that the items of one request (consecutive
+// in the list) run on the same XCD at about the same time and share its L2:
+// blocks are handed to the 8 XCDs round-robin, and XCD x takes the x-th
+// eighth of the list in order.
+__device__ __forceinline__ int xcd_item(int b, int n_items) {
+  const int x = b & 7, q = b >> 3;
+  const int per = n_items >> 3, extra = n_items & 7;
+  const int start = x * per + min(x, extra);
+  const int len = per + (x < extra ? 1 : 0);
+  return q < len ? start + q : -1;
+}
+
+template <int HD>
+__global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   using at::TK;
-  constexpr int KW = HD + 8;    // K tile row stride (bf16): 16-byte pad
-  constexpr int VW = HD + 32;   // V tile row stride (bf16): 64-byte pad
+  using T = AttnTile<HD>;
   constexpr int NS = HD / 16;   // MFMA k-steps over head_dim for S
   constexpr int NT = HD / 32;   // 32-row output tiles over head_dim
-  constexpr int CPR = HD / 8;   // 16-byte chunks per K/V row
-  constexpr int CPT = TK * CPR / 256;
-  static_assert(CPT >= 1, "head_dim too small");
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][TK * KW];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][TK * VW];
+  constexpr int CPR = T::CPR, ROWB = T::ROWB, TILEB = T::TILEB;
+  // Four LDS stages (K tile, then V tile): three tiles are in flight while
+  // one is used.  Each stage is its own LDS object, so the compiler's own
+  // waits never cover the copies of later stages.
+  __shared__ __attribute__((aligned(1024))) uint8_t S0[2 * TILEB];
+  __shared__ __attribute__((aligned(1024))) uint8_t S1[2 * TILEB];
+  __shared__ __attribute__((aligned(1024))) uint8_t S2[2 * TILEB];
+  __shared__ __attribute__((aligned(1024))) uint8_t S3[2 * TILEB];
 
-  const AttnItem it = a.items[blockIdx.x];
+  const int item = xcd_item(blockIdx.x, a.n_items);
+  if (item < 0) return;
+  const AttnItem it = a.items[item];
   const ReqDesc rq = a.reqs[it.req];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
   const int half = lane >> 5;
   const int G = a.nq / a.nkv;
   const int nrows = rq.H * G;
@@ -65,15 +106,14 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   const int qg = it.kvh * G + (qvalid ? qrow % G : 0);
   const bf16 *qkv = reinterpret_cast<const bf16 *>(a.qkv);
 
-  // Q^T operand: lane holds Q[qrow][16 s + 8 half .. + 7] for k-step s.
+  // Q^T operand, held for the whole item: lane holds Q[qrow][16 s + 8 half .. + 7].
+  // Rows past the request's queries read its first row instead: their results
+  // are never stored.
   bf16x8 qf[NS];
   {
     const bf16 *qp = qkv + (size_t)(rq.tok_off + qt) * a.ldqkv + (size_t)qg * HD + half * 8;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const uint4 v = qvalid ? *reinterpret_cast<const uint4 *>(qp + 16 * s) : make_uint4(0, 0, 0, 0);
-      qf[s] = __builtin_bit_cast(bf16x8, v);
-    }
+    for (int s = 0; s < NS; ++s) qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
 
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
@@ -81,30 +121,50 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   const bf16 *pv = reinterpret_cast<const bf16 *>(rq.pv) + (size_t)a.layer * rq.P * prow + (size_t)it.kvh * HD;
   const bf16 *ak = qkv + (size_t)rq.tok_off * a.ldqkv + (size_t)(a.nq + it.kvh) * HD;
   const bf16 *av = qkv + (size_t)rq.tok_off * a.ldqkv + (size_t)(a.nq + a.nkv + it.kvh) * HD;
+  const long ldq = a.ldqkv;
 
-  uint4 rk[CPT], rv[CPT];
-  auto load_tile = [&](int kt0) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, row = c / CPR, c8 = (c % CPR) * 8;
-      const int key = kt0 + row;
-      if (key < it.kend) {
-        const bf16 *sk = key < rq.P ? pk + (size_t)key * prow : ak + (size_t)(key - rq.P) * a.ldqkv;
-        const bf16 *sv = key < rq.P ? pv + (size_t)key * prow : av + (size_t)(key - rq.P) * a.ldqkv;
-        rk[i] = *reinterpret_cast<const uint4 *>(sk + c8);
-        rv[i] = *reinterpret_cast<const uint4 *>(sv + c8);
-      } else {
-        rk[i] = make_uint4(0, 0, 0, 0);
-        rv[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
+  // Copies: 1 KB units, unit u of the K tile (then of the V tile) by wave
+  // u % 4; lane i fills physical chunk i % CPR of row u * RPU + i / CPR, which
+  // holds logical chunk (i % CPR) ^ swz(row).  Keys past the range load the
+  // last valid key (finite values; their scores are masked).
+  auto copy_unit = [&](uint8_t *dst, const bf16 *pre_base, const bf16 *act_base, int kt0, int u) {
+    const int row = u * T::RPU + lane / CPR;
+    const int c = (lane % CPR) ^ at::swz(row, CPR);
+    const int key = min(kt0 + row, it.kend - 1);
+    const bool pre = key < rq.P;
+    const bf16 *base = pre ? pre_base : act_base;
+    const long roff = pre ? (long)key * (long)prow : (long)(key - rq.P) * ldq;
+    __builtin_amdgcn_global_load_lds((const void *)(base + roff + c * 8), ROSA_LDS_A(dst + u * 1024), 16, 0, 0);
   };
-  auto store_tile = [&](int buf) {
+  // Tiles that lie wholly in the prefix (all but at most two per item) copy
+  // from a uniform base plus per-lane offsets fixed for the whole item.
+  constexpr int UPW = (T::UNITS / 2 + 3) / 4;    // K (or V) units per copying wave
+  int poff[UPW];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, row = c / CPR, c8 = (c % CPR) * 8;
-      *reinterpret_cast<uint4 *>(&Ks[buf][row * KW + c8]) = rk[i];
-      *reinterpret_cast<uint4 *>(&Vs[buf][row * VW + c8]) = rv[i];
+  for (int j = 0; j < UPW; ++j) {
+    const int row = (4 * j + wave) * T::RPU + lane / CPR;
+    poff[j] = row * (int)prow + (((lane % CPR) ^ at::swz(row, CPR)) << 3);
+  }
+  auto issue = [&](uint8_t *st, int kt0) {
+    if (kt0 + TK <= rq.P && kt0 + TK <= it.kend) {
+      const bf16 *kb = pk + (size_t)kt0 * prow;
+      const bf16 *vb = pv + (size_t)kt0 * prow;
+#pragma unroll
+      for (int j = 0; j < UPW; ++j)
+        if (4 * j + wave < T::UNITS / 2)
+          __builtin_amdgcn_global_load_lds((const void *)(kb + poff[j]), ROSA_LDS_A(st + (4 * j + wave) * 1024), 16, 0, 0);
+#pragma unroll
+      for (int j = 0; j < UPW; ++j)
+        if (4 * j + wave < T::UNITS / 2)
+          __builtin_amdgcn_global_load_lds((const void *)(vb + poff[j]), ROSA_LDS_A(st + TILEB + (4 * j + wave) * 1024),
+                                           16, 0, 0);
+    } else {
+#pragma unroll
+      for (int u0 = 0; u0 < T::UNITS / 2; u0 += 4)
+        if (u0 + wave < T::UNITS / 2) copy_unit(st, pk, ak, kt0, u0 + wave);
+#pragma unroll
+      for (int u0 = 0; u0 < T::UNITS / 2; u0 += 4)
+        if (u0 + wave < T::UNITS / 2) copy_unit(st + TILEB, pv, av, kt0, u0 + wave);
     }
   };
 
@@ -113,93 +173,122 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
   for (int n = 0; n < NT; ++n)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[n][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;     // running max (raw score units) and sum
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
+  const float lazy = 8.0f / sl2;            // rescale only when the max grows by > 2^8
 
-  const int nkt = (it.kend - it.kbeg + TK - 1) / TK;
-  load_tile(it.kbeg);
-  store_tile(0);
-  __syncthreads();
-  for (int t = 0; t < nkt; ++t) {
-    const int cur = t & 1;
-    const int kt0 = it.kbeg + t * TK;
-    if (t + 1 < nkt) load_tile(kt0 + TK);
+  // K operand: row lane%32, logical chunk 2 ks + half.
+  const int krow = lane & 31;
+  const int kbase = krow * ROWB;
+  const int ksw = at::swz(krow, CPR);
+  // V transpose reads: source lane s of 16-lane group G16 reads 8 bytes at
+  // row 16 ks + 4 half + s/4 (and 8 rows further), head-dim column
+  // 32 n + 16 G16 + 4 (s%4).
+  const int src16 = lane & 15, g16 = (lane >> 4) & 1;
+  const int vcol = 16 * g16 + 4 * (src16 & 3);
 
-    // S^T (keys x queries) for two 32-key sub-tiles.
-    f32x16 s[2];
+  auto tile = [&](const uint8_t *st, int kt0) {
+    // S^T (32 keys x 32 queries): lane holds query lane%32; register r holds
+    // key kt0 + (r/4)*8 + 4 half + r%4.
+    // Two independent accumulation chains (even and odd k-steps) so that
+    // consecutive MFMAs do not wait on each other's results.
+    f32x16 s, s2;
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
+    for (int r = 0; r < 16; ++r) { s[r] = 0.f; s2[r] = 0.f; }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[sub][r] = 0.f;
-      const bf16 *kb = &Ks[cur][(sub * 32 + (lane & 31)) * KW + half * 8];
+    for (int ks = 0; ks < NS; ks += 2) {
+      const bf16x8 kf0 = *reinterpret_cast<const bf16x8 *>(st + kbase + (((2 * ks + half) ^ ksw) << 4));
+      const bf16x8 kf1 = *reinterpret_cast<const bf16x8 *>(st + kbase + (((2 * ks + 2 + half) ^ ksw) << 4));
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[ks], s, 0, 0, 0);
+      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[ks + 1], s2, 0, 0, 0);
+    }
 #pragma unroll
-      for (int ks = 0; ks < NS; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kb + ks * 16);
-        s[sub] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[sub], 0, 0, 0);
+    for (int r = 0; r < 16; ++r) s[r] += s2[r];
+    // Keep at most a couple of K fragments in flight (register budget of two
+    // blocks per CU): one LDS read, then one MFMA.
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    }
+    if (kt0 + TK > it.kend) {               // last, partial tile
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt0 + (r >> 2) * 8 + half * 4 + (r & 3);
+        if (key >= it.kend) s[r] = -INFINITY;
       }
     }
-    // Lane holds query (lane & 31); register r of sub-tile `sub` holds key
-    // kt0 + 32 sub + (r/4)*8 + 4 half + r%4.
-    float tmax = -INFINITY;
+    float tmax = s[0];
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt0 + sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-        const float v = key < it.kend ? s[sub][r] * sl2 : -INFINITY;
-        s[sub][r] = v;
-        tmax = fmaxf(tmax, v);
-      }
+    for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, s[r]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);     // finite: every tile has a valid key
-    const float alpha = exp2f(m_run - m_new);
+    if (__builtin_amdgcn_ballot_w64(tmax > m_run + lazy) != 0) {   // wave-uniform rescale
+      const float m_new = fmaxf(m_run, tmax);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
+      l_run *= alpha;
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[n][r] *= alpha;
+      m_run = m_new;
+    }
+    const float mb = -m_run * sl2;
     float psum = 0.f;
+    bf16x8 pf[2];
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[sub][r] - m_new);
-        s[sub][r] = p;
-        psum += p;
-      }
+    for (int r = 0; r < 16; ++r) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, mb));
+      psum += p;
+      pf[r >> 3][r & 7] = (bf16)p;
+    }
     psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    l_run += psum;
+    // O^T (head_dim x queries) += V^T P^T; k-step ks uses P^T registers
+    // 8 ks .. 8 ks + 7, i.e. keys 16 ks + 8 (i/4) + 4 half + i%4.
 #pragma unroll
-    for (int n = 0; n < NT; ++n)
+    for (int ks = 0; ks < 2; ++ks) {
+      const int r0 = ks * 16 + half * 4 + (src16 >> 2);
+      const uint8_t *v0 = st + TILEB + r0 * ROWB;
+      const uint8_t *v1 = st + TILEB + (r0 + 8) * ROWB;
+      const int sw0 = at::swz(r0, CPR), sw1 = at::swz(r0 + 8, CPR);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[n][r] *= alpha;
-
-    // P^T operands: k-step ks of sub-tile sub uses registers 8 ks .. 8 ks + 7,
-    // i.e. keys 16 ks + 8 (i/4) + 4 half + i%4 for element i.
-    bf16x8 pf[2][2];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pf[sub][ks][i] = (bf16)s[sub][8 * ks + i];
-
-    // O^T (head_dim x queries) += V^T P^T.  The V^T operand of lane l needs
-    // V[key(i)][32 n + l%32]; each transpose read delivers four consecutive keys.
-    const int src = lane & 15;
-    const int mcol = 16 * ((lane >> 4) & 1) + 4 * (src & 3);
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
-        const int krow = sub * 32 + ks * 16 + half * 4 + (src >> 2);
-        const bf16 *vb = &Vs[cur][krow * VW + mcol];
-#pragma unroll
-        for (int n = 0; n < NT; ++n) {
-          const bf16x8 vf = lds_tr_pair(vb + n * 32, vb + 8 * VW + n * 32);
-          o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[sub][ks], o[n], 0, 0, 0);
-        }
+      for (int n = 0; n < NT; ++n) {
+        const int x = n * 32 + vcol;   // head-dim column (bf16 index)
+        const int off0 = (((x >> 3) ^ sw0) << 4) + ((x & 7) << 1);
+        const int off1 = (((x >> 3) ^ sw1) << 4) + ((x & 7) << 1);
+        const bf16x8 vf = lds_tr_pair(v0 + off0, v1 + off1);
+        o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[n], 0, 0, 0);
       }
+    }
+#pragma unroll
+    for (int n = 0; n < 2 * NT; ++n) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+    }
+  };
 
-    if (t + 1 < nkt) store_tile(cur ^ 1);
-    __syncthreads();
+  // Ring of four stages; tile t lives in stage t % 4.  Copies past the last
+  // tile repeat it (harmless), so every step issues exactly one stage and the
+  // wait count stays uniform.
+  const int nkt = (it.kend - it.kbeg + TK - 1) / TK;
+  auto issue_t = [&](uint8_t *st, int t) { issue(st, it.kbeg + min(t, nkt - 1) * TK); };
+  auto step = [&](uint8_t *cur, uint8_t *refill, int t) {
+    __builtin_amdgcn_s_waitcnt(T::WAIT);    // this wave's copies of tile t have landed
+    __builtin_amdgcn_s_barrier();           // ... and every wave's; tile t-1's stage is free
+    __builtin_amdgcn_sched_barrier(0);
+    issue_t(refill, t + 3);
+    tile(cur, it.kbeg + t * TK);
+  };
+  issue_t(S0, 0);
+  issue_t(S1, 1);
+  issue_t(S2, 2);
+  for (int t = 0; t < nkt; t += 4) {
+    step(S0, S3, t);
+    if (t + 1 < nkt) step(S1, S0, t + 1);
+    if (t + 2 < nkt) step(S2, S1, t + 2);
+    if (t + 3 < nkt) step(S3, S2, t + 3);
   }
+  __builtin_amdgcn_s_waitcnt(T::WAIT0);     // no copy may outlive the block's LDS
 
   // Accumulator layout: lane holds query (lane & 31); register r of tile n holds
   // head-dim index 32 n + (r/4)*8 + 4 half + r%4.
@@ -227,7 +316,7 @@ __global__ void __launch_bounds__(256) attention_bf16_kernel(AttnArgs a) {
       }
     if (half == 0) {
       float *pm = a.part_ml + ((size_t)it.slot * kAttnQB + qloc) * 2;
-      pm[0] = m_run;
+      pm[0] = m_run * sl2;     // log2 units, as the merge expects
       pm[1] = l_run;
     }
   }
@@ -330,7 +419,7 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
 hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
   if (bf16_mode) {
-    dim3 grid(a.n_items);
+    dim3 grid((a.n_items + 7) / 8 * 8);
     switch (a.hd) {
       case 32: hipLaunchKernelGGL(attention_bf16_kernel<32>, grid, dim3(256), 0, s, a); break;
       case 64: hipLaunchKernelGGL(attention_bf16_kernel<64>, grid, dim3(256), 0, s, a); break;

@@ -81,6 +81,7 @@ struct rosa_batch {
   float *part_o = nullptr, *part_ml = nullptr;
   int max_items = 0;
 
+
   // plan buffers: device region + two pinned host staging copies
   void *d_plan = nullptr;
   void *h_plan[2] = {nullptr, nullptr};
@@ -128,7 +129,7 @@ rosa_status check_config(const rosa_model_config *c) {
   if (c->n_q_heads % c->n_kv_heads != 0) return ROSA_E_UNSUPPORTED;
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
     return ROSA_E_UNSUPPORTED;
-  if (c->d_model % 64 || c->d_mlp % 64 || (c->n_q_heads * c->head_dim) % 64) return ROSA_E_UNSUPPORTED;
+  if (c->d_model % 128 || c->d_mlp % 128 || (c->n_q_heads * c->head_dim) % 128) return ROSA_E_UNSUPPORTED;
   if (c->d_model > 4096 || c->action_dim > 64 || c->time_emb_dim % 2 || c->time_emb_dim > 8192)
     return ROSA_E_UNSUPPORTED;
   return ROSA_OK;
@@ -493,6 +494,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->tc2 = dalloc<float>(b, (size_t)kMaxTau * d, e);
     b->part_o = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * D.hd, e);
     b->part_ml = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * 2, e);
+
     // plan region
     const int G = D.nq / D.nkv;
     const int64_t qb_bound = (int64_t)D.nkv * (((int64_t)maxM * G + kAttnQB - 1) / kAttnQB + cap->max_requests);

@@ -34,10 +34,14 @@ __device__ __forceinline__ float wave_max(float v) {
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
 
-// tanh-approximate GELU: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))).
+// tanh-approximate GELU: 0.5 x (1 + tanh(z)), z = sqrt(2/pi) (x + 0.044715 x^3),
+// evaluated through the identity 0.5 (1 + tanh(z)) = 1 / (1 + e^(-2z)): one
+// exponential and one reciprocal instead of a tanh.  For large |x| the
+// exponential saturates to 0 or +inf, giving x or -0 exactly.
 __device__ __forceinline__ float gelu_tanh_f(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  return 0.5f * x * (1.0f + tanhf(k0 * (x + 0.044715f * x * x * x)));
+  const float k2 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float e = exp2f(k2 * (x + 0.044715f * x * x * x));
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 }  // namespace rosa

@@ -82,6 +82,9 @@ struct GemmArgs {
   const float *gate; int gate_stride; const int32_t *rowmod;  // gate = gate[rowmod[m]*gate_stride + n]
 };
 hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s);
+// bf16 GEMM with a given block configuration (0: 256x256/4 waves, 1: 256x256/8 waves,
+// 2: 256x256/16 waves, 3: 128x128/4 waves, 4: 256x128/4 waves).
+hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s);
 
 // Attention of one layer.
 struct AttnArgs {
