@@ -249,8 +249,25 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs g) {
 hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   if (bf16_mode) {
-    // 256 x 256 blocks of 16 waves (four per SIMD hide LDS and barrier latency).
-    return launch_gemm_cfg(g, 2, s);
+    // 256 x 256 blocks of 16 waves (one block per CU) or 128 x 128 blocks of 4
+    // waves (two per CU), whichever needs less time: full rounds of blocks over
+    // the CUs times the measured time of one round (per 1024 of K: 33 us for
+    // 256 x 256 blocks, 19 us for 128 x 128 blocks on MI355X).  Small M with
+    // N = d leaves most CUs idle with the large blocks.
+    static int n_cu = 0;
+    if (n_cu == 0) {
+      int dev = 0, v = 0;
+      if (hipGetDevice(&dev) == hipSuccess &&
+          hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+        n_cu = v;
+      else
+        n_cu = 256;
+    }
+    const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
+    const long t128 = (long)((g.M + 127) / 128) * ((g.N + 127) / 128);
+    const long cost256 = (t256 + n_cu - 1) / n_cu * 33;
+    const long cost128 = (t128 + 2 * n_cu - 1) / (2 * n_cu) * 19;
+    return launch_gemm_cfg(g, cost128 < cost256 ? 3 : 2, s);
   }
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   switch (g.epi) {

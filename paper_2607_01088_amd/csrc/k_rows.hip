@@ -5,6 +5,8 @@
 // All are HBM/L2-bound streaming kernels over the stacked action-token rows;
 // one 64-lane wavefront owns one row so that the RMS reduction is a single
 // wave reduction with no block barrier.
+#include <algorithm>
+
 #include "rosa_device.h"
 #include "rosa_internal.h"
 
@@ -34,23 +36,41 @@ hipError_t launch_setup_rows(const ReqDesc *reqs, int n_req, const int32_t *tau_
   return hipGetLastError();
 }
 
-// h[m][n] = sum_a x[m][a] w_in[a][n] + b_in[n]   (fp32; A is small)
-__global__ void in_proj_kernel(const float *__restrict__ x, int A, const float *__restrict__ w_in,
-                               const float *__restrict__ b_in, int d, float *__restrict__ h) {
-  const int m = blockIdx.y;
+// h[m][n] = sum_a x[m][a] w_in[a][n] + b_in[n]   (fp32; A <= 64 is small).
+// A block covers 16 rows x 256 columns: the rows of x are staged in LDS
+// (broadcast reads) and each thread keeps its column of W_in in registers.
+constexpr int kInProjRows = 16;
+__global__ void __launch_bounds__(256) in_proj_kernel(const float *__restrict__ x, int M, int A,
+                                                      const float *__restrict__ w_in,
+                                                      const float *__restrict__ b_in, int d,
+                                                      float *__restrict__ h) {
+  __shared__ float xs[kInProjRows][64];
+  const int m0 = blockIdx.y * kInProjRows;
+  const int rows = min(kInProjRows, M - m0);
+  for (int i = threadIdx.x; i < kInProjRows * 64; i += 256) {
+    const int r = i / 64, a = i % 64;
+    xs[r][a] = (r < rows && a < A) ? x[(size_t)(m0 + r) * A + a] : 0.f;
+  }
+  __syncthreads();
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= d) return;
-  const float *xr = x + (size_t)m * A;
-  float acc = b_in[n];
-  for (int a = 0; a < A; ++a) acc = fmaf(xr[a], w_in[(size_t)a * d + n], acc);
-  h[(size_t)m * d + n] = acc;
+  float w[64];
+#pragma unroll
+  for (int a = 0; a < 64; ++a) w[a] = a < A ? w_in[(size_t)a * d + n] : 0.f;
+  const float bias = b_in[n];
+  for (int r = 0; r < rows; ++r) {
+    float acc = bias;
+#pragma unroll
+    for (int a = 0; a < 64; ++a) acc = fmaf(xs[r][a], w[a], acc);
+    h[(size_t)(m0 + r) * d + n] = acc;
+  }
 }
 
 hipError_t launch_in_proj(const float *x, int M, int A, const float *w_in, const float *b_in, int d,
                           float *h, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  dim3 grid((d + 255) / 256, M);
-  hipLaunchKernelGGL(in_proj_kernel, grid, dim3(256), 0, s, x, A, w_in, b_in, d, h);
+  dim3 grid((d + 255) / 256, (M + kInProjRows - 1) / kInProjRows);
+  hipLaunchKernelGGL(in_proj_kernel, grid, dim3(256), 0, s, x, M, A, w_in, b_in, d, h);
   return hipGetLastError();
 }
 
@@ -104,44 +124,74 @@ hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *
 
 // Final modulated RMSNorm, velocity v = norm W_out + b_out, Euler step
 // x += (1/K_r) v, and on the request's last step the store of x into the
-// caller's action chunk.  One wave per row; the normalized row is staged in
-// LDS so that the A output dot products read it as a broadcast.
+// caller's action chunk.
+//
+// A block takes groups of R rows (R = 256 / A_pad, A_pad = 32 or 64): its
+// waves normalize the group's rows into LDS, then each thread owns one
+// (row, output) pair and walks d against W_out in LDS.  When W_out fits next
+// to the rows (d * A_pad + R * d floats <= 160 KB; 128 KB + 32 KB at the pi0
+// shape) it is loaded once per block and the blocks walk the row groups
+// persistently; otherwise it is staged in chunks of kFinalChunk rows.
+constexpr int kFinalChunk = 128;
+constexpr size_t kLdsMax = 160 * 1024;
 __global__ void __launch_bounds__(256) final_euler_kernel(
     const float *__restrict__ h, int M, int d, float eps, const float *__restrict__ modtab,
     int mod_stride, int shift_off, int scale_off, const int32_t *__restrict__ rowmod,
     const float *__restrict__ w_out, const float *__restrict__ b_out, int A,
     const int32_t *__restrict__ row_req, const ReqDesc *__restrict__ reqs, int step,
-    float *__restrict__ x) {
-  extern __shared__ float lds_rows[];  // [4][d]
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + w;
-  const bool active = row < M;
-  float *hf = lds_rows + (size_t)w * d;
-  if (active) {
-    const float *hr = h + (size_t)row * d;
-    float ss = 0.f;
-    for (int i = lane; i < d; i += 64) ss += hr[i] * hr[i];
-    ss = wave_sum(ss);
-    const float r = 1.0f / sqrtf(ss / (float)d + eps);
-    const float *mrow = modtab + (size_t)rowmod[row] * mod_stride;
-    for (int i = lane; i < d; i += 64) hf[i] = hr[i] * r * (1.0f + mrow[scale_off + i]) + mrow[shift_off + i];
-  }
-  __syncthreads();
-  if (!active) return;
-  const ReqDesc q = reqs[row_req[row]];
-  const float dt = 1.0f / (float)q.K;
-  const int half = lane >> 5;
-  for (int a0 = 0; a0 < A; a0 += 32) {
-    const int a = a0 + (lane & 31);
+    float *__restrict__ x, int resident) {
+  extern __shared__ float lds_final[];
+  const int a_pad = A <= 32 ? 32 : 64;
+  const int R = 256 / a_pad;                       // rows per group
+  const int wrows = resident ? d : kFinalChunk;    // rows of W_out held in LDS
+  float *wc = lds_final;                           // [wrows][a_pad]
+  float *hf = lds_final + (size_t)wrows * a_pad;   // [R][d]
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int my_r = tid / a_pad, my_a = tid % a_pad;
+  auto load_w = [&](int c0, int cn) {
+    for (int i = tid; i < cn * a_pad; i += 256) {
+      const int ri = i / a_pad, ai = i % a_pad;
+      wc[i] = ai < A ? w_out[(size_t)(c0 + ri) * A + ai] : 0.f;
+    }
+  };
+  if (resident) load_w(0, d);
+  const int n_groups = (M + R - 1) / R;
+  for (int grp = blockIdx.x; grp < n_groups; grp += gridDim.x) {
+    const int row0 = grp * R;
+    __syncthreads();                               // previous group's reads of hf are done
+    for (int r = wave; r < R; r += 4) {
+      const int row = row0 + r;
+      if (row >= M) continue;
+      const float *hr = h + (size_t)row * d;
+      float ss = 0.f;
+      for (int i = lane; i < d; i += 64) ss += hr[i] * hr[i];
+      ss = wave_sum(ss);
+      const float rn = 1.0f / sqrtf(ss / (float)d + eps);
+      const float *mrow = modtab + (size_t)rowmod[row] * mod_stride;
+      for (int i = lane; i < d; i += 64)
+        hf[(size_t)r * d + i] = hr[i] * rn * (1.0f + mrow[scale_off + i]) + mrow[shift_off + i];
+    }
     float acc = 0.f;
-    if (a < A)
-      for (int i = half; i < d; i += 2) acc = fmaf(hf[i], w_out[(size_t)i * A + a], acc);
-    acc += __shfl_xor(acc, 32, 64);
-    if (half == 0 && a < A) {
-      const float v = acc + b_out[a];
-      const float xn = x[(size_t)row * A + a] + dt * v;
-      x[(size_t)row * A + a] = xn;
-      if (step == q.K - 1) q.actions[(size_t)(row - q.tok_off) * A + a] = xn;
+    const float *hrow = hf + (size_t)my_r * d;
+    if (resident) {
+      __syncthreads();
+      for (int i = 0; i < d; ++i) acc = fmaf(hrow[i], wc[i * a_pad + my_a], acc);
+    } else {
+      for (int c0 = 0; c0 < d; c0 += kFinalChunk) {
+        const int cn = min(kFinalChunk, d - c0);
+        __syncthreads();                           // hf written / previous chunk consumed
+        load_w(c0, cn);
+        __syncthreads();
+        for (int i = 0; i < cn; ++i) acc = fmaf(hrow[c0 + i], wc[i * a_pad + my_a], acc);
+      }
+    }
+    const int row = row0 + my_r;
+    if (row < M && my_a < A) {
+      const ReqDesc q = reqs[row_req[row]];
+      const float v = acc + b_out[my_a];
+      const float xn = x[(size_t)row * A + my_a] + (1.0f / (float)q.K) * v;
+      x[(size_t)row * A + my_a] = xn;
+      if (step == q.K - 1) q.actions[(size_t)(row - q.tok_off) * A + my_a] = xn;
     }
   }
 }
@@ -151,9 +201,24 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
                               const float *w_out, const float *b_out, int A, const int32_t *row_req,
                               const ReqDesc *reqs, int step, float *x, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  const size_t lds = (size_t)4 * d * sizeof(float);
-  hipLaunchKernelGGL(final_euler_kernel, dim3((M + 3) / 4), dim3(256), lds, s, h, M, d, eps, modtab,
-                     mod_stride, shift_off, scale_off, rowmod, w_out, b_out, A, row_req, reqs, step, x);
+  const int a_pad = A <= 32 ? 32 : 64;
+  const int R = 256 / a_pad;
+  const int groups = (M + R - 1) / R;
+  const size_t lds_res = ((size_t)d * a_pad + (size_t)R * d) * sizeof(float);
+  const int resident = lds_res <= kLdsMax ? 1 : 0;
+  const size_t lds = resident ? lds_res : ((size_t)kFinalChunk * a_pad + (size_t)R * d) * sizeof(float);
+  if (lds > kLdsMax) return hipErrorInvalidValue;
+  static bool lds_raised = false;   // the attribute is per function: raise it to the maximum once
+  if (!lds_raised) {
+    const hipError_t e = hipFuncSetAttribute((const void *)final_euler_kernel,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+    if (e != hipSuccess) return e;
+    lds_raised = true;
+  }
+  // Resident: one block per CU walks the groups (W_out is loaded once per block).
+  const int blocks = resident ? std::min(groups, 256) : std::min(groups, 1024);
+  hipLaunchKernelGGL(final_euler_kernel, dim3(blocks), dim3(256), lds, s, h, M, d, eps, modtab, mod_stride,
+                     shift_off, scale_off, rowmod, w_out, b_out, A, row_req, reqs, step, x, resident);
   return hipGetLastError();
 }
 

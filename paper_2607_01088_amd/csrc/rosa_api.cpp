@@ -77,7 +77,7 @@ struct rosa_batch {
   float *x = nullptr, *h = nullptr;
   void *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr;
   int32_t *row_req = nullptr, *rowmod = nullptr, *ident = nullptr;
-  float *modtab = nullptr, *emb = nullptr, *tc1 = nullptr, *tc2 = nullptr;
+  float *modtab = nullptr, *emb = nullptr, *tc1 = nullptr, *tc2 = nullptr, *gemv_ws = nullptr;
   float *part_o = nullptr, *part_ml = nullptr;
   int max_items = 0;
 
@@ -373,11 +373,11 @@ hipError_t run_time_conditioning(rosa_batch *b, const float *d_taus, int n_tau, 
   const Dims &D = b->dims;
   hipError_t e = timed(b, kcTime, [&] { return launch_time_embedding(d_taus, n_tau, D.dt, b->emb, b->stream); });
   if (e == hipSuccess)
-    e = timed(b, kcTime, [&] { return launch_small_gemv(b->emb, n_tau, D.dt, b->w_t1, b->bf16, b->b_t1, D.d, 1, b->tc1, b->stream); });
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->emb, n_tau, D.dt, b->w_t1, b->bf16, b->b_t1, D.d, 1, b->tc1, b->gemv_ws, b->stream); });
   if (e == hipSuccess)
-    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc1, n_tau, D.d, b->w_t2, b->bf16, b->b_t2, D.d, 1, b->tc2, b->stream); });
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc1, n_tau, D.d, b->w_t2, b->bf16, b->b_t2, D.d, 1, b->tc2, b->gemv_ws, b->stream); });
   if (e == hipSuccess)
-    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc2, n_tau, D.d, b->w_modall, b->bf16, b->b_modall, D.mod_stride, 0, out, b->stream); });
+    e = timed(b, kcTime, [&] { return launch_small_gemv(b->tc2, n_tau, D.d, b->w_modall, b->bf16, b->b_modall, D.mod_stride, 0, out, b->gemv_ws, b->stream); });
   return e;
 }
 
@@ -492,6 +492,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->emb = dalloc<float>(b, (size_t)kMaxTau * D.dt, e);
     b->tc1 = dalloc<float>(b, (size_t)kMaxTau * d, e);
     b->tc2 = dalloc<float>(b, (size_t)kMaxTau * d, e);
+    b->gemv_ws = dalloc<float>(b, small_gemv_workspace_floats(std::max(D.mod_stride, D.d)), e);
     b->part_o = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * D.hd, e);
     b->part_ml = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * 2, e);
 

@@ -56,8 +56,11 @@ enum Epilogue : int {
 // Time conditioning.
 hipError_t launch_time_embedding(const float *taus, int n_tau, int dt, float *emb, hipStream_t s);
 // Y[n][N] = act(X[n][K] W[K][N] + b); act: 0 none, 1 SiLU.  W row-major [K][N].
+// ws: workspace of small_gemv_workspace_floats(N) floats (K-slice partials).
+constexpr int kGemvMaxSlices = 8;
+size_t small_gemv_workspace_floats(int N);
 hipError_t launch_small_gemv(const float *X, int n, int K, const void *W, bool w_bf16, const float *b,
-                             int N, int act, float *Y, hipStream_t s);
+                             int N, int act, float *Y, float *ws, hipStream_t s);
 
 // Row kernels.
 hipError_t launch_setup_rows(const ReqDesc *reqs, int n_req, const int32_t *tau_idx, int max_steps,
