@@ -115,9 +115,8 @@ def cpu_baseline(preset, weights, reqs_meta, budget_s: float):
     return {
         "value": len(reqs_meta) / batch_s,
         "unit": "chunks/s",
-        "cores": int(max(1, min(cores, blas_threads))) if blas_threads > 1 else 1,
+        "cores": int(blas_threads),          # threads the oracle's matrix products ran on
         "host_cores_available": cores,
-        "blas_threads": int(blas_threads),
         "kind": "oracle",
         "sample": (f"{len(done)} of {len(reqs_meta)} requests (stratified over horizon x steps), "
                    f"{t_used:.1f} s measured, scaled to the whole batch by algorithmic flops "

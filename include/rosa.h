@@ -3,12 +3,13 @@
  *
  * One call serves a batch of robot requests with a shared action expert, the
  * System-1 model of the paper's serving system: many robots' action-model
- * requests are batched into one call on one GPU worker (Sec. 3.2 "better
- * hardware utilization", Sec. 3.4.1 "batching", Sec. 4 "System 1 batching").
+ * requests are batched into one call on one GPU worker (Sec. 3.2, inter-robot
+ * batching on a shared pool; Sec. 3.4.1, batching decisions; Sec. 4.3, System-1
+ * batching).
  * Each request brings its own cached vision-language prefix (keys and values
  * of every layer), an initial noise action chunk and a number of denoising
- * steps (Sec. 2.1.1: a VLM backbone feeds a diffusion-transformer action head;
- * Sec. 2.2: diffusion action experts run a few denoising steps), and gets back
+ * steps (Sec. 2.2.1: a VLM backbone feeds a diffusion-transformer action head;
+ * Sec. 2.3: diffusion action experts run a few denoising steps), and gets back
  * its action chunk.
  *
  * The action expert computes, for every request independently:

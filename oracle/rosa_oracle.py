@@ -6,12 +6,12 @@ time, one layer at a time, with matrix products as the only library steps.
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 it; the product path never calls it.
 
-What is computed.  The paper (Sec. 2.1.1) describes System-1 action models as a
+What is computed.  The paper (Sec. 2.2.1) describes System-1 action models as a
 vision-language backbone whose cached prefix feeds an action-generation head
-such as a diffusion transformer, and (Sec. 2.2) diffusion-style action experts
+such as a diffusion transformer, and (Sec. 2.3) diffusion-style action experts
 that run a small number of denoising steps.  Its serving system batches
-System-1 requests from many robots into one call on a GPU worker (Sec. 3.2,
-Sec. 3.4.1 "batching", Sec. 4 "System 1 batching").  The paper does not write
+System-1 requests from many robots into one call on a GPU worker (Sec. 3.2;
+Sec. 3.4.1, batching decisions; Sec. 4.3, System-1 batching).  The paper does not write
 out the action expert's layers, so the forward pass below follows these
 readings (each is restated where it is used):
 

@@ -7,7 +7,7 @@ and the GPU library can consume the same inputs without sharing any code.
 
 The workloads stand in for the paper's System-1 action model serving a fleet of
 robots (Sec. 3.2 and 3.4.1: requests from many robots are batched into one
-action-model call; Sec. 4, System-1 batching).  The paper evaluates GR00T N1.6
+action-model call; Sec. 4.3, the System-1 batching ablation).  The paper evaluates GR00T N1.6
 and pi0.5 on real observations; those weights and observations are not
 available, so every tensor here is synthetic with the shapes of a pi0-style
 action expert (18 layers, width 1024, 8 query heads sharing one 256-wide KV
