@@ -124,6 +124,21 @@ def cpu_baseline(preset, weights, reqs_meta, budget_s: float):
     }
 
 
+def copy_probe(torch):
+    """A plain copy of known size: each launch reads and writes exactly 1 GiB.
+    Its FETCH_SIZE / WRITE_SIZE readings give the factor that turns those
+    counters into bytes for the other kernels."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read_per_launch": n, "copy_probe_bytes_written_per_launch": n,
+                      "launches": 5}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +147,8 @@ def main():
     ap.add_argument("--workload", default="factory_b256")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported in this build "
@@ -139,6 +156,9 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        copy_probe(torch)
+        return
     from paper_2607_01088_amd import rosa
     from synthetic import PRESETS, make_metadata, make_requests, make_weights
 
