@@ -46,9 +46,18 @@ rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_
  *   which = 1: out[M][d]     += gate[M][d] * (a[M][n_q*hd] W_o[layer])     (fp32)
  *   which = 2: out[M][d_mlp]  = gelu_tanh(a[M][d] W_up[layer])             (model dtype)
  *   which = 3: out[M][d]     += gate[M][d] * (a[M][d_mlp] W_down[layer])   (fp32)
- * a is DEVICE in the model dtype; gate is DEVICE fp32 (ignored for 0 and 2). */
+ * a is DEVICE in the model dtype; gate is DEVICE fp32 (ignored for 0 and 2).
+ * a, out and gate must be 16-byte aligned (ROSA_E_INVALID otherwise). */
 rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const void *a, int32_t M,
                             void *out, const float *gate);
+
+/* Force the block configuration of every bf16 projection launched on this
+ * handle (rosa_generate_actions and rosa_debug_gemm): cfg in [0, n) where n is
+ * returned in *n_configs, or -1 for the built-in cost model (the default).
+ * Every configuration computes each output with the same instruction sequence,
+ * so results are bitwise identical whichever is used; only speed differs.
+ * n_configs may be NULL. */
+rosa_status rosa_debug_gemm_config(rosa_batch *b, int32_t cfg, int32_t *n_configs);
 
 /* Per-kernel timing.  While enabled, every launch of the handle is bracketed
  * by HIP events on the handle's stream and its duration is added to its

@@ -10,35 +10,31 @@
 
 namespace rosa {
 
-template <int EPI, typename OutT>
-__device__ __forceinline__ void epilogue_one(const GemmArgs &g, int row, int col, float v) {
-  if constexpr (EPI == kEpiStore) {
-    reinterpret_cast<OutT *>(g.out)[(size_t)row * g.ldo + col] = from_f32<OutT>(v);
-  } else if constexpr (EPI == kEpiGelu) {
-    reinterpret_cast<OutT *>(g.out)[(size_t)row * g.ldo + col] = from_f32<OutT>(gelu_tanh_f(v));
-  } else {
-    const float gate = g.gate[(size_t)g.rowmod[row] * g.gate_stride + col];
-    float *h = reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo + col;
-    *h = *h + gate * v;
-  }
-}
-
 // ------------------------------------------------------------------ bf16 MFMA GEMM
-// Block tile BM x BN, WM x WN waves, each wave a (BM/WM) x (BN/WN) tile made of
-// 32 x 32 v_mfma_f32_32x32x16_bf16 accumulators.
+// Block tile BM x BN = (32 MB) x (32 TN WN), WM x WN waves, each wave
+// (32 MB / WM) x (32 TN) made of 32 x 32 v_mfma_f32_32x32x16_bf16 tiles.
 //
-// K is consumed 32 at a time through a ring of four LDS stages filled by
-// global_load_lds_dwordx4 (global -> LDS without staging registers): while the
-// waves multiply stage s, stages s+1 and s+2 are landing and stage s+3 is
-// being requested.  One barrier per stage.  Each stage buffer is its own LDS
-// object and the barrier is a bare s_barrier, so the only wait on the
-// asynchronous copies is the explicit vmcnt before it.
+// Main loop: K is consumed 32 at a time through a ring of four LDS stages
+// filled by global_load_lds_dwordx4 (global -> LDS without staging
+// registers): while the waves multiply stage s, stages s+1 and s+2 are landing
+// and stage s+3 is being requested.  One barrier per stage.  Each stage buffer
+// is its own LDS object and the barrier is a bare s_barrier, so the only wait
+// on the asynchronous copies is the explicit vmcnt before it.
 //
 // LDS rows are 64 bytes (32 bf16 of K); the four 16-byte chunks of row r are
 // stored XOR-swizzled by (r / 4) % 4, so the 16 rows a 16-lane group reads at
-// one logical chunk land in 16 distinct bank groups.  The copy writes lane i
-// of a wave's instruction to byte 16 i of a 1 KB block (16 rows), so each
-// lane fetches the logical chunk that belongs at its physical position.
+// one logical chunk land in 16 distinct bank groups.  A copy instruction
+// writes lane i to byte 16 i of a 1 KB block (16 rows), so each lane fetches
+// the logical chunk that belongs at its physical position.
+//
+// The MFMA takes the weight fragment as its first operand, so a lane's
+// accumulator registers hold four consecutive output columns of one output row.
+// The epilogue stages each 32 x 32 accumulator tile through LDS and writes
+// whole 64- or 128-byte row segments with 16-byte accesses.
+//
+// Blocks are mapped to tiles so that each of the 8 XCDs (which receive blocks
+// round-robin) works on a contiguous range of the row-major tile list: the
+// column tiles of one row panel share an XCD's L2.
 namespace gb {
 constexpr int BK = 32;
 constexpr int NST = 4;
@@ -47,96 +43,107 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) 
 
 #define ROSA_LDS(p) ((__attribute__((address_space(3))) void *)(p))
 
-template <int BM_, int BN_, int WM_, int WN_>
+template <int MB_, int TN_, int WM_, int WN_>
 struct GemmTile {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
-  static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;     // MFMA tiles per wave
+  static constexpr int MB = MB_, TN = TN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
+  static constexpr int MBW = MB / WM;                                   // 32-row blocks per wave
+  static constexpr int BM = 32 * MB, BN = 32 * TN * WN;
   static constexpr int ABYTES = BM * gb::BK * 2, SBYTES = ABYTES + BN * gb::BK * 2;
-  static constexpr int DA = BM / 16 / NW, DB = BN / 16 / NW;      // 1 KB copies per wave per stage
-  static_assert(DA * 16 * NW == BM && DB * 16 * NW == BN, "copy split");
-  static_assert(TM * 32 * WM == BM && TN * 32 * WN == BN, "wave split");
-  static constexpr int WAIT = gb::waitcnt_vm((DA + DB) * (gb::NST - 2));
-  static constexpr int WAIT0 = gb::waitcnt_vm(0);
+  static constexpr int U = (BM + BN) / 16;                              // 1 KB copies per stage
+  static constexpr int CHI = (U + NW - 1) / NW, CLO = U / NW;           // copies per wave
+  static constexpr int NHI = U % NW == 0 ? NW : U % NW;                 // waves with CHI copies
+  static constexpr int PERB = SBYTES / 4096;                            // 4 KB epilogue slots per stage
+  static_assert(MBW * WM == MB, "row split");
+  static_assert(gb::NST * PERB >= NW, "epilogue staging space");
 };
 
 template <typename T, int EPI>
-__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g) {
+__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct) {
   using namespace gb;
-  constexpr int ABYTES = T::ABYTES, SBYTES = T::SBYTES, DA = T::DA, DB = T::DB, TM = T::TM, TN = T::TN;
-  constexpr int NW = T::NW;
+  constexpr int NW = T::NW, MBW = T::MBW, TN = T::TN, CHI = T::CHI, CLO = T::CLO;
+  constexpr int ABYTES = T::ABYTES, SBYTES = T::SBYTES;
   __shared__ __attribute__((aligned(1024))) uint8_t L0[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L1[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L2[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L3[SBYTES];
 
+  // Tile of this block: XCD x = b % 8 takes the x-th eighth of the tile list.
+  const int n_tiles = nrt * nct;
+  const int b = blockIdx.x, x = b & 7, q = b >> 3;
+  const int per = n_tiles >> 3, extra = n_tiles & 7;
+  if (q >= per + (x < extra ? 1 : 0)) return;
+  const int tile = x * per + min(x, extra) + q;
+  const int m0 = (tile / nct) * T::BM, n0 = (tile % nct) * T::BN;
+
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (T::NW - 1);   // wave-uniform, in an SGPR
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % NW;   // wave-uniform, in an SGPR
   const int wm = wave / T::WN, wn = wave % T::WN;
-  const int m0 = blockIdx.y * T::BM, n0 = blockIdx.x * T::BN;
   const bf16 *A = reinterpret_cast<const bf16 *>(g.a);
   const bf16 *W = reinterpret_cast<const bf16 *>(g.wt);
 
-  // Copy sources: instruction j of this wave fills rows 16 (NW j + wave) .. +15;
-  // lane i writes physical chunk i % 4 of row i / 4 there, which holds logical
-  // chunk (i % 4) ^ ((row / 4) % 4) = (i % 4) ^ ((i / 16) % 4).
+  // Copy sources: 1 KB unit u (A rows first, then W rows) is copied by wave
+  // u % NW; lane i writes physical chunk i % 4 of row i / 4 of the unit, which
+  // holds logical chunk (i % 4) ^ ((i / 16) % 4).  Rows past M (or N) re-read
+  // the last row; their results are never stored.
   const int csrc = (lane & 3) ^ ((lane >> 4) & 3);
-  const bf16 *asrc[DA];
-  const bf16 *bsrc[DB];
+  const bf16 *src[CHI];
 #pragma unroll
-  for (int j = 0; j < DA; ++j) {
-    const int row = min(m0 + (NW * j + wave) * 16 + (lane >> 2), g.M - 1);
-    asrc[j] = A + (size_t)row * g.lda + csrc * 8;
+  for (int j = 0; j < CHI; ++j) {
+    const int u = min(j * NW + wave, T::U - 1);
+    if (u < T::BM / 16) {
+      const int row = min(m0 + u * 16 + (lane >> 2), g.M - 1);
+      src[j] = A + (size_t)row * g.lda + csrc * 8;
+    } else {
+      const int row = min(n0 + (u - T::BM / 16) * 16 + (lane >> 2), g.N - 1);
+      src[j] = W + (size_t)row * g.K + csrc * 8;
+    }
   }
-#pragma unroll
-  for (int j = 0; j < DB; ++j) {
-    const int row = min(n0 + (NW * j + wave) * 16 + (lane >> 2), g.N - 1);
-    bsrc[j] = W + (size_t)row * g.K + csrc * 8;
-  }
+  const bool hi = wave < T::NHI;
   const int nk = g.K / BK;
   auto issue = [&](uint8_t *st, int kt) {
-    const int k0 = min(kt, nk - 1) * BK;
+    const int k0 = min(kt, nk - 1) * BK;    // past the end: repeat the last stage (never read)
 #pragma unroll
-    for (int j = 0; j < DA; ++j)
-      __builtin_amdgcn_global_load_lds((const void *)(asrc[j] + k0), ROSA_LDS(st + (NW * j + wave) * 1024), 16, 0, 0);
-#pragma unroll
-    for (int j = 0; j < DB; ++j)
-      __builtin_amdgcn_global_load_lds((const void *)(bsrc[j] + k0), ROSA_LDS(st + ABYTES + (NW * j + wave) * 1024),
-                                       16, 0, 0);
+    for (int j = 0; j < CHI; ++j)
+      if (j < CLO || hi)
+        __builtin_amdgcn_global_load_lds((const void *)(src[j] + k0), ROSA_LDS(st + (j * NW + wave) * 1024), 16, 0, 0);
   };
 
-  f32x16 acc[TM][TN];
+  f32x16 acc[MBW][TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < MBW; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Operand reads: lane reads row (lane & 31) of a 32-row tile, logical chunk
+  // Operand reads: lane reads row (lane & 31) of a 32-row block, logical chunk
   // 2 ks + lane / 32, at physical chunk (logical) ^ ((lane / 4) % 4).
   const int swz = (lane >> 2) & 3;
-  const int ph0 = (lane >> 5) ^ swz, ph1 = (2 + (lane >> 5)) ^ swz;
-  const int arow = (wm * TM * 32 + (lane & 31)) * 64;
+  const int ph0 = ((lane >> 5) ^ swz) * 16, ph1 = ((2 + (lane >> 5)) ^ swz) * 16;
+  const int arow = (wm * MBW * 32 + (lane & 31)) * 64;
   const int brow = ABYTES + (wn * TN * 32 + (lane & 31)) * 64;
   auto compute = [&](const uint8_t *st) {
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const int ph = (ks == 0 ? ph0 : ph1) * 16;
-      bf16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * 64 + ph);
+      const int ph = ks == 0 ? ph0 : ph1;
+      bf16x8 af[MBW], bfr[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * 64 + ph);
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < MBW; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * 64 + ph);
+#pragma unroll
+      for (int i = 0; i < MBW; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
     }
   };
+  // A wave copies CHI or CLO units per stage, so waiting until at most two
+  // stages of its copies are outstanding means stage kt has landed.
   auto step = [&](uint8_t *cur, uint8_t *refill, int kt) {
-    __builtin_amdgcn_s_waitcnt(T::WAIT);    // this wave's copies of stage kt have landed
-    __builtin_amdgcn_s_barrier();           // ... and every wave's; stage kt-1 is no longer read
+    if (hi) __builtin_amdgcn_s_waitcnt(waitcnt_vm(CHI * (NST - 2)));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(CLO * (NST - 2)));
+    __builtin_amdgcn_s_barrier();           // ... every wave's too; stage kt-1 is no longer read
     __builtin_amdgcn_sched_barrier(0);
     issue(refill, kt + NST - 1);
     compute(cur);
@@ -151,51 +158,144 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g) {
     step(L2, L1, kt + 2);
     step(L3, L2, kt + 3);
   }
-  __builtin_amdgcn_s_waitcnt(T::WAIT0);     // no copy may outlive the block's LDS
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  __syncthreads();                          // every wave is past its last stage read: LDS is free
 
-  // 32x32 accumulator layout: lane l, register r -> row (r/4)*8 + (l/32)*4 + r%4, column l%32.
+  // Epilogue.  Register r of tile (i, j) holds row m0 + 32 (wm MBW + i) + lane % 32,
+  // columns n0 + 32 (wn TN + j) + 8 (r / 4) + 4 (lane / 32) + r % 4: four
+  // consecutive columns per 4 registers.  Each wave stages one 32 x 32 tile at a
+  // time in its own 4 KB slot, then reads it back row-contiguous.
+  const int sb = wave / T::PERB;
+  uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+  const int r32 = lane & 31, half = lane >> 5;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < MBW; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * TN * 32 + j * 32 + (lane & 31);
-      if (col >= g.N) continue;
+      const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
+      if constexpr (EPI == kEpiGatedResidual) {
+        // fp32 slot: 32 rows x 8 chunks of 16 B, chunk c of row r at c ^ ((r / 2) % 8).
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * TM * 32 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (row < g.M) epilogue_one<EPI, bf16>(g, row, col, acc[i][j][r]);
+        for (int gq = 0; gq < 4; ++gq) {
+          const int c = (2 * gq + half) ^ ((r32 >> 1) & 7);
+          *reinterpret_cast<float4 *>(stg + r32 * 128 + c * 16) =
+              make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+        }
+        // Pass p: rows 8 p + lane / 8, columns 4 (lane % 8) .. + 3.  All loads first.
+        float4 v[4], hv[4], gt[4];
+        const int col = cb + (lane & 7) * 4;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int rr = 8 * p + (lane >> 3), c = lane & 7;
+          v[p] = *reinterpret_cast<const float4 *>(stg + rr * 128 + ((c ^ ((rr >> 1) & 7)) * 16));
+          const int row = rb + rr;
+          if (row < g.M && col < g.N) {
+            hv[p] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(g.out) + (size_t)row * g.ldo + col);
+            gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
+          }
+        }
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int row = rb + 8 * p + (lane >> 3);
+          if (row < g.M && col < g.N) {
+            float4 h = hv[p];
+            h.x = h.x + gt[p].x * v[p].x;
+            h.y = h.y + gt[p].y * v[p].y;
+            h.z = h.z + gt[p].z * v[p].z;
+            h.w = h.w + gt[p].w * v[p].w;
+            *reinterpret_cast<float4 *>(reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo + col) = h;
+          }
+        }
+      } else {
+        // bf16 slot: 32 rows x 4 chunks of 16 B (8 bf16), chunk c of row r at
+        // c ^ ((r / 4) % 4); this lane's 4 values are half `half` of chunk gq.
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          float a0 = acc[i][j][4 * gq], a1 = acc[i][j][4 * gq + 1], a2 = acc[i][j][4 * gq + 2], a3 = acc[i][j][4 * gq + 3];
+          if constexpr (EPI == kEpiGelu) {
+            a0 = gelu_tanh_f(a0); a1 = gelu_tanh_f(a1); a2 = gelu_tanh_f(a2); a3 = gelu_tanh_f(a3);
+          }
+          bf16x4 o;
+          o[0] = (bf16)a0; o[1] = (bf16)a1; o[2] = (bf16)a2; o[3] = (bf16)a3;
+          const int c = gq ^ ((r32 >> 2) & 3);
+          *reinterpret_cast<bf16x4 *>(stg + r32 * 64 + c * 16 + half * 8) = o;
+        }
+        // Pass p: rows 16 p + lane / 4, columns 8 (lane % 4) .. + 7.
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int rr = 16 * p + (lane >> 2), c = lane & 3;
+          const bf16x8 v = *reinterpret_cast<const bf16x8 *>(stg + rr * 64 + ((c ^ ((rr >> 2) & 3)) * 16));
+          const int row = rb + rr, col = cb + c * 8;
+          if (row < g.M && col < g.N)
+            *reinterpret_cast<bf16x8 *>(reinterpret_cast<bf16 *>(g.out) + (size_t)row * g.ldo + col) = v;
+        }
       }
     }
 }
 
-using Tile256x4 = GemmTile<256, 256, 2, 2>;    // 4 waves, 128 x 128 each
-using Tile256x8 = GemmTile<256, 256, 2, 4>;    // 8 waves, 128 x 64 each
-using Tile256x16 = GemmTile<256, 256, 4, 4>;   // 16 waves, 64 x 64 each
-using Tile128x4 = GemmTile<128, 128, 2, 2>;    // 4 waves, 64 x 64 each
-using Tile256x128 = GemmTile<256, 128, 2, 2>;  // 4 waves, 128 x 64 each
+// Block configurations and their measured cost on MI355X (one round of
+// blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
+// (store, GELU, gated residual).
+struct GemmCfg { int bm, bn; float a, b[3]; };
+static constexpr GemmCfg kCfgs[kGemmConfigs] = {
+    {384, 128, 17.4f, {11.0f, 14.9f, 18.7f}},   // 0: 8 waves, 96 x 64 each
+    {256, 256, 21.2f, {9.7f, 17.3f, 15.9f}},    // 1: 16 waves, 64 x 64 each
+    {128, 256, 12.9f, {5.9f, 11.6f, 13.3f}},    // 2: 8 waves, 64 x 64 each
+    {192, 128, 13.7f, {2.2f, 5.1f, 7.8f}},      // 3: 8 waves, 96 x 32 each
+    {288, 128, 20.4f, {2.6f, 9.4f, 10.7f}},     // 4: 12 waves, 96 x 32 each
+};
+using Cfg0 = GemmTile<12, 2, 4, 2>;
+using Cfg1 = GemmTile<8, 2, 4, 4>;
+using Cfg2 = GemmTile<4, 2, 2, 4>;
+using Cfg3 = GemmTile<6, 1, 2, 4>;
+using Cfg4 = GemmTile<9, 1, 3, 4>;
+static_assert(Cfg0::BM == 384 && Cfg0::BN == 128 && Cfg1::BM == 256 && Cfg1::BN == 256 && Cfg2::BM == 128 &&
+              Cfg2::BN == 256 && Cfg3::BM == 192 && Cfg3::BN == 128 && Cfg4::BM == 288 && Cfg4::BN == 128,
+              "cost table matches the tiles");
 
 template <typename T>
 static hipError_t launch_tile(const GemmArgs &g, hipStream_t s) {
-  dim3 grid((g.N + T::BN - 1) / T::BN, (g.M + T::BM - 1) / T::BM);
+  const int nrt = (g.M + T::BM - 1) / T::BM, nct = (g.N + T::BN - 1) / T::BN;
+  dim3 grid((nrt * nct + 7) / 8 * 8);
   switch (g.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore>), grid, dim3(T::NT), 0, s, g); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu>), grid, dim3(T::NT), 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGatedResidual>), grid, dim3(T::NT), 0, s, g); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
+    default: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGatedResidual>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
-  if (g.K % 128 != 0) return hipErrorInvalidValue;
+  if (g.K % 128 != 0 || g.N % 8 != 0) return hipErrorInvalidValue;
   switch (cfg) {
-    case 0: return launch_tile<Tile256x4>(g, s);
-    case 1: return launch_tile<Tile256x8>(g, s);
-    case 2: return launch_tile<Tile256x16>(g, s);
-    case 3: return launch_tile<Tile128x4>(g, s);
-    case 4: return launch_tile<Tile256x128>(g, s);
+    case 0: return launch_tile<Cfg0>(g, s);
+    case 1: return launch_tile<Cfg1>(g, s);
+    case 2: return launch_tile<Cfg2>(g, s);
+    case 3: return launch_tile<Cfg3>(g, s);
+    case 4: return launch_tile<Cfg4>(g, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+int gemm_pick_config(int M, int N, int K, int epi, int n_cu) {
+  int best = 0;
+  float best_t = 0.f;
+  for (int c = 0; c < kGemmConfigs; ++c) {
+    const long tiles = (long)((M + kCfgs[c].bm - 1) / kCfgs[c].bm) * ((N + kCfgs[c].bn - 1) / kCfgs[c].bn);
+    const long rounds = (tiles + n_cu - 1) / n_cu;
+    const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].b[epi < 0 || epi > 2 ? 2 : epi]);
+    if (c == 0 || t < best_t) { best = c; best_t = t; }
+  }
+  return best;
+}
+
+template <int EPI>
+__device__ __forceinline__ void epilogue_f32(const GemmArgs &g, int row, int col, float v) {
+  float *out = reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo + col;
+  if constexpr (EPI == kEpiStore) *out = v;
+  else if constexpr (EPI == kEpiGelu) *out = gelu_tanh_f(v);
+  else *out = *out + g.gate[(size_t)g.rowmod[row] * g.gate_stride + col] * v;
 }
 
 // ------------------------------------------------------------------ fp32 VALU GEMM (debug mode)
@@ -241,19 +341,14 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int col = n0 + tx * 4 + j;
-      if (col < g.N) epilogue_one<EPI, float>(g, row, col, acc[i][j]);
+      if (col < g.N) epilogue_f32<EPI>(g, row, col, acc[i][j]);
     }
   }
 }
 
-hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int force_cfg) {
   if (g.M <= 0) return hipSuccess;
   if (bf16_mode) {
-    // 256 x 256 blocks of 16 waves (one block per CU) or 128 x 128 blocks of 4
-    // waves (two per CU), whichever needs less time: full rounds of blocks over
-    // the CUs times the measured time of one round (per 1024 of K: 33 us for
-    // 256 x 256 blocks, 19 us for 128 x 128 blocks on MI355X).  Small M with
-    // N = d leaves most CUs idle with the large blocks.
     static int n_cu = 0;
     if (n_cu == 0) {
       int dev = 0, v = 0;
@@ -263,11 +358,8 @@ hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s) {
       else
         n_cu = 256;
     }
-    const long t256 = (long)((g.M + 255) / 256) * ((g.N + 255) / 256);
-    const long t128 = (long)((g.M + 127) / 128) * ((g.N + 127) / 128);
-    const long cost256 = (t256 + n_cu - 1) / n_cu * 33;
-    const long cost128 = (t128 + 2 * n_cu - 1) / (2 * n_cu) * 19;
-    return launch_gemm_cfg(g, cost128 < cost256 ? 3 : 2, s);
+    const int cfg = force_cfg >= 0 ? force_cfg : gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu);
+    return launch_gemm_cfg(g, cfg, s);
   }
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   switch (g.epi) {

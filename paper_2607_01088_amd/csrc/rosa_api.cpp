@@ -65,6 +65,7 @@ struct rosa_batch {
   int device = 0;
   hipStream_t stream = nullptr;
   bool poisoned = false;
+  int gemm_cfg = -1;                 // forced projection block configuration, -1: cost model
   std::string last_error;
 
   // weights on the device
@@ -596,7 +597,7 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
         GemmArgs g{};
         g.a = b->u; g.lda = D.d; g.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * b->esz;
         g.M = M; g.N = D.qkv_dim; g.K = D.d; g.epi = kEpiStore; g.out = b->qkv; g.ldo = D.qkv_dim;
-        e = timed(b, kcGemmQKV, [&] { return launch_gemm(g, b->bf16, b->stream); });
+        e = timed(b, kcGemmQKV, [&] { return launch_gemm(g, b->bf16, b->stream, b->gemm_cfg); });
         if (e != hipSuccess) break;
         e = run_attention(b, p, n_act, l, b->qkv, b->o);
         if (e != hipSuccess) break;
@@ -604,7 +605,7 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
         go.a = b->o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * b->esz;
         go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = b->h; go.ldo = D.d;
         go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
-        e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, b->stream); });
+        e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, b->stream, b->gemm_cfg); });
         if (e != hipSuccess) break;
         e = timed(b, kcModNorm, [&] {
           return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, b->u, b->bf16, b->stream);
@@ -613,13 +614,13 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
         GemmArgs gu{};
         gu.a = b->u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * b->esz;
         gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = b->g; gu.ldo = D.dff;
-        e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, b->stream); });
+        e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, b->stream, b->gemm_cfg); });
         if (e != hipSuccess) break;
         GemmArgs gd{};
         gd.a = b->g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * b->esz;
         gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = b->h; gd.ldo = D.d;
         gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
-        e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, b->stream); });
+        e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, b->stream, b->gemm_cfg); });
       }
       if (e == hipSuccess)
         e = timed(b, kcFinal, [&] {
@@ -730,6 +731,8 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
     if (which < 0 || which > 3 || layer < 0 || layer >= D.L || !a || !out || M < 0 ||
         M > b->cap.max_action_tokens || ((which == 1 || which == 3) && !gate))
       return fail(b, ROSA_E_INVALID, "bad gemm arguments");
+    if (((uintptr_t)a | (uintptr_t)out | (uintptr_t)gate) & 15)
+      return fail(b, ROSA_E_INVALID, "gemm operands must be 16-byte aligned");
     GemmArgs g{};
     g.a = a; g.M = M; g.out = out; g.gate = gate; g.rowmod = b->ident;
     switch (which) {
@@ -744,12 +747,20 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
     }
     const int cls = which == 0 ? kcGemmQKV : which == 1 ? kcGemmO : which == 2 ? kcGemmUp : kcGemmDown;
     hipError_t e = hipSetDevice(b->device);
-    if (e == hipSuccess) e = timed(b, cls, [&] { return launch_gemm(g, b->bf16, b->stream); });
+    if (e == hipSuccess) e = timed(b, cls, [&] { return launch_gemm(g, b->bf16, b->stream, b->gemm_cfg); });
     if (e != hipSuccess) return device_fail(b, e, "gemm");
     return ROSA_OK;
   } catch (...) {
     return fail(b, ROSA_E_DEVICE, "unexpected exception");
   }
+}
+
+rosa_status rosa_debug_gemm_config(rosa_batch *b, int32_t cfg, int32_t *n_configs) {
+  if (!b) return ROSA_E_INVALID;
+  if (n_configs) *n_configs = kGemmConfigs;
+  if (cfg < -1 || cfg >= kGemmConfigs) return fail(b, ROSA_E_INVALID, "gemm configuration out of range");
+  b->gemm_cfg = cfg;
+  return ROSA_OK;
 }
 
 rosa_status rosa_debug_set_profiling(rosa_batch *b, int32_t enable) {

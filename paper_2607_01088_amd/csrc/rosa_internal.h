@@ -84,10 +84,13 @@ struct GemmArgs {
   void *out; int ldo;        // kEpiStore / kEpiGelu: activation dtype; kEpiGatedResidual: fp32 h
   const float *gate; int gate_stride; const int32_t *rowmod;  // gate = gate[rowmod[m]*gate_stride + n]
 };
-hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s);
-// bf16 GEMM with a given block configuration (0: 256x256/4 waves, 1: 256x256/8 waves,
-// 2: 256x256/16 waves, 3: 128x128/4 waves, 4: 256x128/4 waves).
+// force_cfg < 0: block configuration chosen by the cost model.
+hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1);
+// bf16 GEMM with a given block configuration (0: 384x128, 1: 256x256, 2: 128x256,
+// 3: 192x128, 4: 288x128).
+constexpr int kGemmConfigs = 5;
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s);
+int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 
 // Attention of one layer.
 struct AttnArgs {

@@ -86,6 +86,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_attention.restype = C.c_int
     lib.rosa_debug_gemm.argtypes = [vp, i32, i32, vp, i32, vp, vp]
     lib.rosa_debug_gemm.restype = C.c_int
+    lib.rosa_debug_gemm_config.argtypes = [vp, i32, C.POINTER(i32)]
+    lib.rosa_debug_gemm_config.restype = C.c_int
     lib.rosa_debug_set_profiling.argtypes = [vp, i32]
     lib.rosa_debug_set_profiling.restype = C.c_int
     lib.rosa_debug_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64), C.POINTER(C.c_double),
@@ -190,6 +192,13 @@ class ActionExpert:
     def gemm(self, which: int, layer: int, a, M: int, out, gate=None) -> None:
         self._check(self.lib.rosa_debug_gemm(self.handle, which, layer, a.data_ptr(), M, out.data_ptr(),
                                              None if gate is None else gate.data_ptr()))
+
+    def gemm_config(self, cfg: int) -> int:
+        """Force the projection block configuration (-1: cost model); returns
+        the number of configurations."""
+        n = C.c_int32()
+        self._check(self.lib.rosa_debug_gemm_config(self.handle, cfg, C.byref(n)))
+        return n.value
 
     def set_profiling(self, enable: bool) -> None:
         self._check(self.lib.rosa_debug_set_profiling(self.handle, 1 if enable else 0))

@@ -109,6 +109,49 @@ def test_projection_matches_float64(which, proj, M, request):
         assert rel_l2(got, gate * acc) < (1e-5 if dtype == "fp32" else 1e-5), tol
 
 
+@pytest.mark.parametrize("which,M", [("tiny_bf16", 129), ("pi0_bf16", 50), ("pi0_bf16", 1600)])
+@pytest.mark.parametrize("proj", [0, 1, 2, 3])
+def test_projection_each_block_config(which, M, proj, request):
+    """Every bf16 block configuration against float64, and bitwise equal to
+    the others (the same MFMA sequence computes each output)."""
+    e, w = request.getfixturevalue(which)
+    sh = e.shape
+    if M > e.cap.max_action_tokens:
+        pytest.skip("above capacity")
+    layer = 0
+    rng = np.random.default_rng(7 + proj + M)
+    K_in = {0: sh.d_model, 1: sh.n_q_heads * sh.head_dim, 2: sh.d_model, 3: sh.d_mlp}[proj]
+    W = {0: w["w_qkv"], 1: w["w_o"], 2: w["w_up"], 3: w["w_down"]}[proj][layer].astype(np.float64)
+    a = bf16_round(rng.standard_normal((M, K_in)).astype(np.float32))
+    acc = a.astype(np.float64) @ W
+    a_dev = _tdev(a, "bf16")
+    h0 = rng.standard_normal((M, sh.d_model)).astype(np.float32)
+    gate = torch.from_numpy(rng.standard_normal((M, sh.d_model)).astype(np.float32)).cuda()
+    outs = []
+    n_cfg = e.gemm_config(-1)
+    try:
+        for cfg in range(n_cfg):
+            e.gemm_config(cfg)
+            if proj in (0, 2):
+                out = torch.full((M, W.shape[1]), float("nan"), dtype=a_dev.dtype, device="cuda")
+                e.gemm(proj, layer, a_dev, M, out)
+                got = _thost(out)
+                ref = acc if proj == 0 else gelu_tanh(acc)
+                err = rel_l2(got, ref)
+                assert err < 4e-3, (cfg, err)
+            else:
+                h = torch.from_numpy(h0).cuda()
+                e.gemm(proj, layer, a_dev, M, h, gate)
+                got = h.cpu().numpy()
+                err = rel_l2(got.astype(np.float64) - h0, gate.cpu().numpy() * acc)
+                assert err < 1e-5, (cfg, err)
+            outs.append(got)
+    finally:
+        e.gemm_config(-1)
+    for cfg in range(1, n_cfg):
+        assert np.array_equal(outs[cfg], outs[0]), cfg
+
+
 # ------------------------------------------------------------------ attention
 
 def _attn_case(e, shapes, seed, fill_q=None, tags=None):

@@ -227,6 +227,27 @@ def test_repeat_runs_are_bitwise_identical(pi0_expert):
             assert np.array_equal(a, b)
 
 
+def test_projection_block_configs_bitwise_identical(pi0_expert):
+    """The whole call gives bitwise the same actions whichever projection
+    block configuration is forced."""
+    e, _ = pi0_expert
+    reqs = make_requests(PRESETS["factory_b256"], indices=[0, 7, 21, 40])
+    db = _rosa().DeviceBatch(reqs, "bf16")
+    outs = []
+    n_cfg = e.gemm_config(-1)
+    try:
+        for cfg in [-1] + list(range(n_cfg)):
+            e.gemm_config(cfg)
+            e.generate(db.structs)
+            torch.cuda.synchronize()
+            outs.append(db.results())
+    finally:
+        e.gemm_config(-1)
+    for o in outs[1:]:
+        for a, b in zip(o, outs[0]):
+            assert np.array_equal(a, b)
+
+
 # ------------------------------------------------------------------ ABI errors on a live handle
 
 def test_invalid_request_enqueues_nothing(pi0_expert):
