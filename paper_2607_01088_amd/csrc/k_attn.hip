@@ -5,11 +5,14 @@
 // prefix keys of this layer followed by its H_r action keys; no other request
 // and no padding is visible.  Scale 1/sqrt(head_dim); no causal mask.
 //
-// bf16 kernel (gfx950 MFMA).  A work item is (request, KV head, block of 128
-// query rows, key range).  Its four waves own 32 query rows each and stream the
-// key range through LDS in 64-key tiles (K and V tiles double-buffered; the
-// next tile's global loads are in flight while the current one is consumed).
-// Per 64-key tile a wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16
+// bf16 kernel (gfx950 MFMA).  A work item is (request, KV head, up to 128 NG
+// query rows, key range).  Its four waves stream the key range through LDS in
+// 32-key stages (K and V tiles; three stages in flight while one is used,
+// copied by global_load_lds_dwordx4).  Each wave owns NG groups of 32 query
+// rows (groups w and w + 4 of the item), so every K and V fragment it reads
+// from LDS feeds the MFMAs of all its groups; NG is 2 where Q^T and O^T of two
+// groups fit the register file (head_dim <= 128) and 1 otherwise.
+// Per 32-key tile a wave computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16
 // (K from LDS, Q^T held in registers for the whole item), so that each lane
 // owns one query column: the online-softmax max and sum are in-lane plus one
 // exchange between the two 32-lane halves, and rescaling the output is
@@ -75,7 +78,7 @@ __device__ __forceinline__ int xcd_item(int b, int n_items) {
   return q < len ? start + q : -1;
 }
 
-template <int HD>
+template <int HD, int NG>
 __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   using at::TK;
   using T = AttnTile<HD>;
@@ -98,22 +101,19 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
   const int half = lane >> 5;
   const int G = a.nq / a.nkv;
-  const int nrows = rq.H * G;
-  const int qloc = wave * 32 + (lane & 31);
-  const int qrow = it.qb * kAttnQB + qloc;
-  const bool qvalid = qrow < nrows;
-  const int qt = qvalid ? qrow / G : 0;
-  const int qg = it.kvh * G + (qvalid ? qrow % G : 0);
   const bf16 *qkv = reinterpret_cast<const bf16 *>(a.qkv);
 
-  // Q^T operand, held for the whole item: lane holds Q[qrow][16 s + 8 half .. + 7].
-  // Rows past the request's queries read its first row instead: their results
-  // are never stored.
-  bf16x8 qf[NS];
-  {
-    const bf16 *qp = qkv + (size_t)(rq.tok_off + qt) * a.ldqkv + (size_t)qg * HD + half * 8;
+  // Q^T operand of group g, held for the whole item: lane holds
+  // Q[row][16 s + 8 half .. + 7] for its row; rows past the item's queries
+  // read the item's first row instead (their results are never stored).
+  bf16x8 qf[NG][NS];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
+  for (int g = 0; g < NG; ++g) {
+    const int loc = 32 * (wave + 4 * g) + (lane & 31);
+    const int qrow = it.q0 + (loc < it.nq ? loc : 0);
+    const bf16 *qp = qkv + (size_t)(rq.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
   }
 
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
@@ -168,14 +168,19 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
     }
   };
 
-  f32x16 o[NT];
+  f32x16 o[NG][NT];
+  // Softmax without rescaling the output inside the key loop: each query's
+  // reference max m_ref is its max over the item's first 32-key tile, and
+  // P = 2^((s - m_ref) log2(e) / sqrt(hd)) may exceed 1.  The loop tracks the
+  // true max; if any query's later scores exceed its reference by more than
+  // 2^64 (room to spare below fp32 overflow for the sums), the block runs the
+  // item a second time with the true max as reference, where P <= 1.  Either
+  // way the output accumulators are only touched by MFMAs in the loop.
+  float m_ref[NG], m_true[NG], l_run[NG];
 #pragma unroll
-  for (int n = 0; n < NT; ++n)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[n][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;     // running max (raw score units) and sum
+  for (int g = 0; g < NG; ++g) m_true[g] = -INFINITY;
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
-  const float lazy = 8.0f / sl2;            // rescale only when the max grows by > 2^8
+  const float over = 64.0f / sl2;           // raw score excess that asks for the second pass
 
   // K operand: row lane%32, logical chunk 2 ks + half.
   const int krow = lane & 31;
@@ -187,62 +192,61 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   const int src16 = lane & 15, g16 = (lane >> 4) & 1;
   const int vcol = 16 * g16 + 4 * (src16 & 3);
 
-  auto tile = [&](const uint8_t *st, int kt0) {
-    // S^T (32 keys x 32 queries): lane holds query lane%32; register r holds
-    // key kt0 + (r/4)*8 + 4 half + r%4.
-    // Two independent accumulation chains (even and odd k-steps) so that
-    // consecutive MFMAs do not wait on each other's results.
-    f32x16 s, s2;
+  const int nkt = (it.kend - it.kbeg + TK - 1) / TK;
+  auto issue_t = [&](uint8_t *st, int t) { issue(st, it.kbeg + min(t, nkt - 1) * TK); };
+
+  // A wave's groups past the item's rows compute on a clamped row (each wave
+  // has its own SIMD; the results are never stored).
+  int ovf = 0;
+  auto tile = [&](const uint8_t *st, int kt0, bool first, bool pass0) {
+    // S^T (32 keys x 32 queries) per group: lane holds query lane%32;
+    // register r holds key kt0 + (r/4)*8 + 4 half + r%4.
+    f32x16 s[NG];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) { s[r] = 0.f; s2[r] = 0.f; }
+    for (int g = 0; g < NG; ++g)
 #pragma unroll
-    for (int ks = 0; ks < NS; ks += 2) {
-      const bf16x8 kf0 = *reinterpret_cast<const bf16x8 *>(st + kbase + (((2 * ks + half) ^ ksw) << 4));
-      const bf16x8 kf1 = *reinterpret_cast<const bf16x8 *>(st + kbase + (((2 * ks + 2 + half) ^ ksw) << 4));
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf0, qf[ks], s, 0, 0, 0);
-      s2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf1, qf[ks + 1], s2, 0, 0, 0);
+      for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks) {
+      const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(st + kbase + (((2 * ks + half) ^ ksw) << 4));
+#pragma unroll
+      for (int g = 0; g < NG; ++g) s[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[g][ks], s[g], 0, 0, 0);
     }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] += s2[r];
-    // Keep at most a couple of K fragments in flight (register budget of two
-    // blocks per CU): one LDS read, then one MFMA.
+    // Keep about two K fragments in flight: one LDS read, then the MFMAs
+    // that use it (the register file holds Q^T and O^T).
 #pragma unroll
     for (int ks = 0; ks < NS; ++ks) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NG, 0);
     }
-    if (kt0 + TK > it.kend) {               // last, partial tile
+    bf16x8 pf[NG][2];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (kt0 + TK > it.kend) {               // last, partial tile
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt0 + (r >> 2) * 8 + half * 4 + (r & 3);
+          if (key >= it.kend) s[g][r] = -INFINITY;
+        }
+      }
+      float tmax = s[g][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, s[g][r]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      if (first && pass0) m_ref[g] = tmax;
+      m_true[g] = fmaxf(m_true[g], tmax);
+      ovf |= tmax > m_ref[g] + over;
+      const float mb = -m_ref[g] * sl2;
+      float psum = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = kt0 + (r >> 2) * 8 + half * 4 + (r & 3);
-        if (key >= it.kend) s[r] = -INFINITY;
+        const float pe = __builtin_amdgcn_exp2f(fmaf(s[g][r], sl2, mb));
+        psum += pe;
+        pf[g][r >> 3][r & 7] = (bf16)pe;
       }
+      psum += __shfl_xor(psum, 32, 64);
+      l_run[g] += psum;
     }
-    float tmax = s[0];
-#pragma unroll
-    for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, s[r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    if (__builtin_amdgcn_ballot_w64(tmax > m_run + lazy) != 0) {   // wave-uniform rescale
-      const float m_new = fmaxf(m_run, tmax);
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * sl2);
-      l_run *= alpha;
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[n][r] *= alpha;
-      m_run = m_new;
-    }
-    const float mb = -m_run * sl2;
-    float psum = 0.f;
-    bf16x8 pf[2];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float p = __builtin_amdgcn_exp2f(fmaf(s[r], sl2, mb));
-      psum += p;
-      pf[r >> 3][r & 7] = (bf16)p;
-    }
-    psum += __shfl_xor(psum, 32, 64);
-    l_run += psum;
     // O^T (head_dim x queries) += V^T P^T; k-step ks uses P^T registers
     // 8 ks .. 8 ks + 7, i.e. keys 16 ks + 8 (i/4) + 4 half + i%4.
 #pragma unroll
@@ -257,67 +261,86 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
         const int off0 = (((x >> 3) ^ sw0) << 4) + ((x & 7) << 1);
         const int off1 = (((x >> 3) ^ sw1) << 4) + ((x & 7) << 1);
         const bf16x8 vf = lds_tr_pair(v0 + off0, v1 + off1);
-        o[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[ks], o[n], 0, 0, 0);
+#pragma unroll
+        for (int g = 0; g < NG; ++g) o[g][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[g][ks], o[g][n], 0, 0, 0);
       }
     }
 #pragma unroll
     for (int n = 0; n < 2 * NT; ++n) {
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, NG, 1);
     }
   };
-
   // Ring of four stages; tile t lives in stage t % 4.  Copies past the last
   // tile repeat it (harmless), so every step issues exactly one stage and the
   // wait count stays uniform.
-  const int nkt = (it.kend - it.kbeg + TK - 1) / TK;
-  auto issue_t = [&](uint8_t *st, int t) { issue(st, it.kbeg + min(t, nkt - 1) * TK); };
-  auto step = [&](uint8_t *cur, uint8_t *refill, int t) {
-    __builtin_amdgcn_s_waitcnt(T::WAIT);    // this wave's copies of tile t have landed
-    __builtin_amdgcn_s_barrier();           // ... and every wave's; tile t-1's stage is free
-    __builtin_amdgcn_sched_barrier(0);
-    issue_t(refill, t + 3);
-    tile(cur, it.kbeg + t * TK);
-  };
-  issue_t(S0, 0);
-  issue_t(S1, 1);
-  issue_t(S2, 2);
-  for (int t = 0; t < nkt; t += 4) {
-    step(S0, S3, t);
-    if (t + 1 < nkt) step(S1, S0, t + 1);
-    if (t + 2 < nkt) step(S2, S1, t + 2);
-    if (t + 3 < nkt) step(S3, S2, t + 3);
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool pass0 = pass == 0;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      l_run[g] = 0.f;
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[g][n][r] = 0.f;
+    }
+    auto step = [&](uint8_t *cur, uint8_t *refill, int t) {
+      __builtin_amdgcn_s_waitcnt(T::WAIT);    // this wave's copies of tile t have landed
+      __builtin_amdgcn_s_barrier();           // ... and every wave's; tile t-1's stage is free
+      __builtin_amdgcn_sched_barrier(0);
+      issue_t(refill, t + 3);
+      tile(cur, it.kbeg + t * TK, t == 0, pass0);
+    };
+    issue_t(S0, 0);
+    issue_t(S1, 1);
+    issue_t(S2, 2);
+    for (int t = 0; t < nkt; t += 4) {
+      step(S0, S3, t);
+      if (t + 1 < nkt) step(S1, S0, t + 1);
+      if (t + 2 < nkt) step(S2, S1, t + 2);
+      if (t + 3 < nkt) step(S3, S2, t + 3);
+    }
+    __builtin_amdgcn_s_waitcnt(T::WAIT0);   // no copy may outlive the pass (or the block's LDS)
+    // Block-uniform decision: every wave has finished reading the stages.
+    if (!pass0 || !__syncthreads_or(ovf)) break;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) m_ref[g] = m_true[g];
   }
-  __builtin_amdgcn_s_waitcnt(T::WAIT0);     // no copy may outlive the block's LDS
 
-  // Accumulator layout: lane holds query (lane & 31); register r of tile n holds
-  // head-dim index 32 n + (r/4)*8 + 4 half + r%4.
-  if (it.slot < 0) {
-    if (!qvalid) return;
-    const float inv = 1.0f / l_run;
-    bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(rq.tok_off + qt) * a.ldo + (size_t)qg * HD;
+  // Accumulator layout: lane holds query (lane & 31) of the group; register r
+  // of tile n holds head-dim index 32 n + (r/4)*8 + 4 half + r%4.
 #pragma unroll
-    for (int n = 0; n < NT; ++n)
+  for (int g = 0; g < NG; ++g) {
+    const int loc = 32 * (wave + 4 * g) + (lane & 31);
+    if (loc >= it.nq) continue;
+    if (it.slot < 0) {
+      const int qrow = it.q0 + loc;
+      const float inv = 1.0f / l_run[g];
+      bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(rq.tok_off + qrow / G) * a.ldo +
+                 (size_t)(it.kvh * G + qrow % G) * HD;
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        bf16x4 v;
+      for (int n = 0; n < NT; ++n)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[n][rg * 4 + e] * inv);
-        *reinterpret_cast<bf16x4 *>(op + n * 32 + rg * 8 + half * 4) = v;
+        for (int rg = 0; rg < 4; ++rg) {
+          bf16x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[g][n][rg * 4 + e] * inv);
+          *reinterpret_cast<bf16x4 *>(op + n * 32 + rg * 8 + half * 4) = v;
+        }
+    } else {
+      float *po = a.part_o + ((size_t)it.slot * kAttnQB + loc) * HD;
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const float4 v = make_float4(o[g][n][rg * 4 + 0], o[g][n][rg * 4 + 1], o[g][n][rg * 4 + 2], o[g][n][rg * 4 + 3]);
+          *reinterpret_cast<float4 *>(po + n * 32 + rg * 8 + half * 4) = v;
+        }
+      if (half == 0) {
+        float *pm = a.part_ml + ((size_t)it.slot * kAttnQB + loc) * 2;
+        pm[0] = m_ref[g] * sl2;     // log2 units, as the merge expects
+        pm[1] = l_run[g];
       }
-  } else {
-    float *po = a.part_o + ((size_t)it.slot * kAttnQB + qloc) * HD;
-#pragma unroll
-    for (int n = 0; n < NT; ++n)
-#pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const float4 v = make_float4(o[n][rg * 4 + 0], o[n][rg * 4 + 1], o[n][rg * 4 + 2], o[n][rg * 4 + 3]);
-        *reinterpret_cast<float4 *>(po + n * 32 + rg * 8 + half * 4) = v;
-      }
-    if (half == 0) {
-      float *pm = a.part_ml + ((size_t)it.slot * kAttnQB + qloc) * 2;
-      pm[0] = m_run * sl2;     // log2 units, as the merge expects
-      pm[1] = l_run;
     }
   }
 }
@@ -332,8 +355,9 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnArgs a) {
   const ReqDesc rq = a.reqs[it.req];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int G = a.nq / a.nkv;
-  const int qrow = it.qb * kAttnQB + blockIdx.y * 4 + wave;
-  if (qrow >= rq.H * G) return;
+  const int qloc = blockIdx.y * 4 + wave;
+  if (qloc >= it.nq) return;
+  const int qrow = it.q0 + qloc;
   const int qt = qrow / G, qg = it.kvh * G + qrow % G;
   const float *qkv = reinterpret_cast<const float *>(a.qkv);
   const float *qp = qkv + (size_t)(rq.tok_off + qt) * a.ldqkv + (size_t)qg * HD;
@@ -394,8 +418,8 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int qloc = blockIdx.x * 4 + wave;
   const int G = nq / nkv;
-  const int qrow = gr.qb * kAttnQB + qloc;
-  if (qrow >= rq.H * G) return;
+  if (qloc >= gr.nq) return;
+  const int qrow = gr.q0 + qloc;
   const int qt = qrow / G, qg = gr.kvh * G + qrow % G;
   float mx = -INFINITY;
   for (int c = 0; c < gr.n; ++c) mx = fmaxf(mx, part_ml[((size_t)(gr.first_slot + c) * kAttnQB + qloc) * 2]);
@@ -421,10 +445,10 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
   if (bf16_mode) {
     dim3 grid((a.n_items + 7) / 8 * 8);
     switch (a.hd) {
-      case 32: hipLaunchKernelGGL(attention_bf16_kernel<32>, grid, dim3(256), 0, s, a); break;
-      case 64: hipLaunchKernelGGL(attention_bf16_kernel<64>, grid, dim3(256), 0, s, a); break;
-      case 128: hipLaunchKernelGGL(attention_bf16_kernel<128>, grid, dim3(256), 0, s, a); break;
-      case 256: hipLaunchKernelGGL(attention_bf16_kernel<256>, grid, dim3(256), 0, s, a); break;
+      case 32: hipLaunchKernelGGL((attention_bf16_kernel<32, attn_groups_per_wave(32)>), grid, dim3(256), 0, s, a); break;
+      case 64: hipLaunchKernelGGL((attention_bf16_kernel<64, attn_groups_per_wave(64)>), grid, dim3(256), 0, s, a); break;
+      case 128: hipLaunchKernelGGL((attention_bf16_kernel<128, attn_groups_per_wave(128)>), grid, dim3(256), 0, s, a); break;
+      case 256: hipLaunchKernelGGL((attention_bf16_kernel<256, attn_groups_per_wave(256)>), grid, dim3(256), 0, s, a); break;
       default: return hipErrorInvalidValue;
     }
   } else {

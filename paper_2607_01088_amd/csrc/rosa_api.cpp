@@ -18,7 +18,7 @@ using namespace rosa;
 
 namespace {
 
-constexpr int kSplitTarget = 512;   // attention work items wanted per call before keys are split
+constexpr int kSplitTarget = 256;   // attention work items wanted per call before keys are split
 constexpr int kMinSplitKeys = 256;  // smallest key range worth a separate work item
 constexpr int kMaxSlots = 2 * kSplitTarget;
 
@@ -155,6 +155,11 @@ Dims make_dims(const rosa_model_config *c) {
   return d;
 }
 
+// Query blocks of R query rows: 32-row groups, at most `per` per block (4 per
+// wave group of the bf16 kernel; the fp32 kernel takes any block).
+int attn_query_blocks(int R, int per) { return ((R + 31) / 32 + per - 1) / per; }
+int attn_groups_per_block(const rosa_model_config *cfg) { return 4 * attn_groups_per_wave(cfg->head_dim); }
+
 // Validation of a request set (all-or-nothing) and the batch plan.
 rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
                        int n, bool sort_by_steps, bool allow_split, Plan &p, std::string &err) {
@@ -217,12 +222,13 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
     }
   }
 
-  // Attention work items: per request, KV head and block of kAttnQB query rows;
-  // keys split over several items only when the batch is too small to fill the GPU.
+  // Attention work items: per request and KV head, its query rows in blocks of
+  // at most kAttnQB rows (32-row groups spread evenly over the blocks); keys
+  // split over several items only when the batch is too small to fill the GPU.
   const int G = cfg->n_q_heads / cfg->n_kv_heads;
   int64_t total_qb = 0;
-  for (int i = 0; i < n; ++i)
-    total_qb += (int64_t)cfg->n_kv_heads * ((reqs[i].horizon * G + kAttnQB - 1) / kAttnQB);
+  const int gpb = attn_groups_per_block(cfg);
+  for (int i = 0; i < n; ++i) total_qb += (int64_t)cfg->n_kv_heads * attn_query_blocks(reqs[i].horizon * G, gpb);
   const bool split = allow_split && total_qb > 0 && total_qb < kSplitTarget;
   int slots = 0;
   p.items_upto.resize(n);
@@ -230,7 +236,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   for (int i = 0; i < n; ++i) {
     const rosa_request &r = reqs[p.order[i]];
     const int nk = r.prefix_len + r.horizon;
-    const int nqb = (r.horizon * G + kAttnQB - 1) / kAttnQB;
+    const int R = r.horizon * G, ngrp = (R + 31) / 32, nqb = attn_query_blocks(R, gpb);
     int nsplit = 1, chunk = nk;
     if (split) {
       const int want = (int)((kSplitTarget + total_qb - 1) / total_qb);
@@ -242,13 +248,15 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
     }
     for (int kvh = 0; kvh < cfg->n_kv_heads; ++kvh)
       for (int qb = 0; qb < nqb; ++qb) {
+        const int q0 = 32 * (qb * ngrp / nqb);
+        const int nq = std::min(R, 32 * ((qb + 1) * ngrp / nqb)) - q0;
         if (nsplit > 1) {
-          AttnGroup gr{i, kvh, qb, slots, nsplit, 0, 0, 0};
+          AttnGroup gr{i, kvh, q0, nq, slots, nsplit, 0, 0};
           p.groups.push_back(gr);
         }
         for (int c = 0; c < nsplit; ++c) {
           AttnItem it{};
-          it.req = i; it.kvh = kvh; it.qb = qb;
+          it.req = i; it.kvh = kvh; it.q0 = q0; it.nq = nq;
           it.kbeg = c * chunk;
           it.kend = std::min(nk, (c + 1) * chunk);
           it.slot = nsplit > 1 ? slots++ : -1;
@@ -499,7 +507,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
 
     // plan region
     const int G = D.nq / D.nkv;
-    const int64_t qb_bound = (int64_t)D.nkv * (((int64_t)maxM * G + kAttnQB - 1) / kAttnQB + cap->max_requests);
+    const int64_t qb_bound = (int64_t)D.nkv * (((int64_t)maxM * G + 127) / 128 + 2 * (int64_t)cap->max_requests);
     b->max_items = (int)std::max<int64_t>(kMaxSlots + qb_bound, qb_bound);
     auto align = [](size_t v) { return (v + 255) / 256 * 256; };
     b->off_reqs = 0;
@@ -674,7 +682,7 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
       counts[2] = 0;
       for (int i = 0; i < n; ++i) {
         const int G = cfg->n_q_heads / cfg->n_kv_heads;
-        counts[2] += cfg->n_kv_heads * ((reqs[i].horizon * G + kAttnQB - 1) / kAttnQB);
+        counts[2] += cfg->n_kv_heads * attn_query_blocks(reqs[i].horizon * G, attn_groups_per_block(cfg));
       }
       counts[3] = (int32_t)p.groups.size();
     }

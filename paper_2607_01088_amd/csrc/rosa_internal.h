@@ -17,23 +17,28 @@ struct ReqDesc {
 };
 static_assert(sizeof(ReqDesc) == 64, "ReqDesc is 64 bytes");
 
-// One attention work item: query block `qb` (kAttnQB query rows) of KV head
+// One attention work item: query rows [q0, q0 + nq) (nq <= kAttnQB) of KV head
 // `kvh` of request `req`, over keys [kbeg, kend) of the request's key sequence
-// (prefix keys first, then its action keys).  slot >= 0: write unnormalized
-// partial results to partial slot `slot`; slot < 0: write o directly.
+// (prefix keys first, then its action keys).  Query row q of a KV head is
+// action token q / G, query head kvh * G + q % G (G query heads per KV head).
+// slot >= 0: write unnormalized partial results to partial slot `slot`;
+// slot < 0: write o directly.
 struct AttnItem {
-  int32_t req, kvh, qb, kbeg, kend, slot, pad0, pad1;
+  int32_t req, kvh, q0, nq, kbeg, kend, slot, pad0;
 };
 static_assert(sizeof(AttnItem) == 32, "AttnItem is 32 bytes");
 
-// A query block whose keys were split over n items starting at `first`
-// (partial slots first_slot .. first_slot + n - 1).
+// A query block whose keys were split over n items (partial slots first_slot
+// .. first_slot + n - 1).
 struct AttnGroup {
-  int32_t req, kvh, qb, first_slot, n, pad0, pad1, pad2;
+  int32_t req, kvh, q0, nq, first_slot, n, pad0, pad1;
 };
 static_assert(sizeof(AttnGroup) == 32, "AttnGroup is 32 bytes");
 
-constexpr int kAttnQB = 128;       // query rows per attention work item (4 waves x 32)
+constexpr int kAttnQB = 256;       // most query rows per attention work item (4 waves x 2 x 32)
+// 32-row query groups per wave of the bf16 attention kernel: two where Q^T and
+// O^T of both fit the register file.  Work items hold at most 128 x this rows.
+constexpr int attn_groups_per_wave(int hd) { return hd <= 128 ? 2 : 1; }
 constexpr int kMaxTau = 128;       // distinct flow times per call
 constexpr int kMaxSteps = 64;
 

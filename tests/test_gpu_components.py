@@ -239,6 +239,34 @@ def test_attention_matches_oracle(which, case, layer_sel, request):
         assert err < tol, (P, H, err)
 
 
+@pytest.mark.parametrize("which", ["tiny_bf16", "pi0_bf16"])
+def test_attention_score_far_above_first_tile(which, request):
+    """One key in a late tile scores far above every key of the first tile
+    (2^130 for head_dim 32, 2^208 for 256 in exp2 units): a single pass
+    referenced to the first tile's max would overflow fp32, so the kernel must
+    take its second pass and match the oracle's near one-hot softmax."""
+    e, _ = request.getfixturevalue(which)
+    sh = e.shape
+    nq, nkv, hd = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    amp = 4.0 if hd == 32 else 3.0
+    P, H, hot = 200, 4, 150
+    qkv, qkv_d, o, structs, host, keep = _attn_case(e, [(P, H)], seed=3, fill_q=amp)
+    k, v, row, _ = host[0]
+    k[:] *= 0.01
+    k[:, hot] = amp
+    if e.dtype == "bf16":
+        k[:] = bf16_round(k)
+    kd, vd = keep[0], keep[1]
+    kd[: k.size].copy_(_tdev(np.ascontiguousarray(k).reshape(-1), e.dtype))
+    e.attention(structs, 1, qkv_d, o)
+    got = _thost(o)[row:row + H]
+    ref = _oracle_attn(sh, qkv, [(k, v, row, H)], 1)[0]
+    assert np.isfinite(got).all()
+    assert rel_l2(got, ref) < 1e-2
+    # the softmax is one-hot on the hot key: every head returns its value row
+    assert rel_l2(got.reshape(H, nq, hd), np.broadcast_to(v[1, hot, 0].astype(np.float64), (H, nq, hd))) < 1e-2
+
+
 def test_attention_unsplit_batch(pi0_bf16):
     """A batch with enough query blocks to fill the GPU runs every request's
     keys in one work item (no partials, no merge); sampled requests match."""
