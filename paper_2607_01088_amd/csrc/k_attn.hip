@@ -127,17 +127,12 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   // u % 4; lane i fills physical chunk i % CPR of row u * RPU + i / CPR, which
   // holds logical chunk (i % CPR) ^ swz(row).  Keys past the range load the
   // last valid key (finite values; their scores are masked).
-  auto copy_unit = [&](uint8_t *dst, const bf16 *pre_base, const bf16 *act_base, int kt0, int u) {
-    const int row = u * T::RPU + lane / CPR;
-    const int c = (lane % CPR) ^ at::swz(row, CPR);
-    const int key = min(kt0 + row, it.kend - 1);
-    const bool pre = key < rq.P;
-    const bf16 *base = pre ? pre_base : act_base;
-    const long roff = pre ? (long)key * (long)prow : (long)(key - rq.P) * ldq;
-    __builtin_amdgcn_global_load_lds((const void *)(base + roff + c * 8), ROSA_LDS_A(dst + u * 1024), 16, 0, 0);
-  };
-  // Tiles that lie wholly in the prefix (all but at most two per item) copy
-  // from a uniform base plus per-lane offsets fixed for the whole item.
+  // Tiles that lie wholly in the prefix (all but at most two per item) take
+  // their sources from a uniform base plus per-lane offsets fixed for the whole
+  // item; the others compute each lane's key.  Only the addresses depend on
+  // the case: the copies themselves are issued after the join, so the
+  // compiler's tracking of the pending LDS writes stays exact (a copy issued
+  // inside a branch makes it wait for every copy before the next LDS read).
   constexpr int UPW = (T::UNITS / 2 + 3) / 4;    // K (or V) units per copying wave
   int poff[UPW];
 #pragma unroll
@@ -146,26 +141,32 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
     poff[j] = row * (int)prow + (((lane % CPR) ^ at::swz(row, CPR)) << 3);
   }
   auto issue = [&](uint8_t *st, int kt0) {
+    const bf16 *ksrc[UPW], *vsrc[UPW];
     if (kt0 + TK <= rq.P && kt0 + TK <= it.kend) {
       const bf16 *kb = pk + (size_t)kt0 * prow;
       const bf16 *vb = pv + (size_t)kt0 * prow;
 #pragma unroll
-      for (int j = 0; j < UPW; ++j)
-        if (4 * j + wave < T::UNITS / 2)
-          __builtin_amdgcn_global_load_lds((const void *)(kb + poff[j]), ROSA_LDS_A(st + (4 * j + wave) * 1024), 16, 0, 0);
-#pragma unroll
-      for (int j = 0; j < UPW; ++j)
-        if (4 * j + wave < T::UNITS / 2)
-          __builtin_amdgcn_global_load_lds((const void *)(vb + poff[j]), ROSA_LDS_A(st + TILEB + (4 * j + wave) * 1024),
-                                           16, 0, 0);
+      for (int j = 0; j < UPW; ++j) { ksrc[j] = kb + poff[j]; vsrc[j] = vb + poff[j]; }
     } else {
 #pragma unroll
-      for (int u0 = 0; u0 < T::UNITS / 2; u0 += 4)
-        if (u0 + wave < T::UNITS / 2) copy_unit(st, pk, ak, kt0, u0 + wave);
-#pragma unroll
-      for (int u0 = 0; u0 < T::UNITS / 2; u0 += 4)
-        if (u0 + wave < T::UNITS / 2) copy_unit(st + TILEB, pv, av, kt0, u0 + wave);
+      for (int j = 0; j < UPW; ++j) {
+        const int row = (4 * j + wave) * T::RPU + lane / CPR;
+        const int c = (lane % CPR) ^ at::swz(row, CPR);
+        const int key = min(kt0 + row, it.kend - 1);
+        const bool pre = key < rq.P;
+        const long roff = (pre ? (long)key * (long)prow : (long)(key - rq.P) * ldq) + c * 8;
+        ksrc[j] = (pre ? pk : ak) + roff;
+        vsrc[j] = (pre ? pv : av) + roff;
+      }
     }
+#pragma unroll
+    for (int j = 0; j < UPW; ++j)
+      if (4 * j + wave < T::UNITS / 2)
+        __builtin_amdgcn_global_load_lds((const void *)ksrc[j], ROSA_LDS_A(st + (4 * j + wave) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < UPW; ++j)
+      if (4 * j + wave < T::UNITS / 2)
+        __builtin_amdgcn_global_load_lds((const void *)vsrc[j], ROSA_LDS_A(st + TILEB + (4 * j + wave) * 1024), 16, 0, 0);
   };
 
   f32x16 o[NG][NT];
@@ -294,11 +295,22 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
     issue_t(S0, 0);
     issue_t(S1, 1);
     issue_t(S2, 2);
-    for (int t = 0; t < nkt; t += 4) {
+    // Whole groups of four tiles without branches between the steps (a join
+    // would make the compiler wait for every pending copy before the next LDS
+    // read), then the last one to three tiles.
+    int t = 0;
+    for (; t + 4 <= nkt; t += 4) {
       step(S0, S3, t);
-      if (t + 1 < nkt) step(S1, S0, t + 1);
-      if (t + 2 < nkt) step(S2, S1, t + 2);
-      if (t + 3 < nkt) step(S3, S2, t + 3);
+      step(S1, S0, t + 1);
+      step(S2, S1, t + 2);
+      step(S3, S2, t + 3);
+    }
+    if (t < nkt) {
+      step(S0, S3, t);
+      if (t + 1 < nkt) {
+        step(S1, S0, t + 1);
+        if (t + 2 < nkt) step(S2, S1, t + 2);
+      }
     }
     __builtin_amdgcn_s_waitcnt(T::WAIT0);   // no copy may outlive the pass (or the block's LDS)
     // Block-uniform decision: every wave has finished reading the stages.
