@@ -222,4 +222,109 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ output projection + Euler (bf16)
+// v = u W_out + b_out on the final-normalized rows u (bf16, from modnorm), then
+// x += v / K and, on the request's last step, x is written to its actions.
+// W_out^T (bf16 [A][d], rows past A read as zero) is staged in LDS in chunks of
+// KC columns, each row's 16-byte chunks XOR-swizzled by row % 16 so that the 32
+// rows one MFMA operand read touches fall in distinct bank groups.  Each wave
+// takes 32-row blocks of u: A operand straight from global memory (16 bytes per
+// lane), B operand from LDS, v_mfma_f32_32x32x16_bf16, NB blocks of 32 outputs.
+template <int NB>
+__global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restrict__ u, int M, int d, int KC,
+                                                             const bf16 *__restrict__ wt, const float *__restrict__ b_out,
+                                                             int A, const int32_t *__restrict__ row_req,
+                                                             const ReqDesc *__restrict__ reqs, int step,
+                                                             float *__restrict__ x) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds_out[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
+  const int cpr = KC / 8;                       // 16-byte chunks per LDS row
+  const int nrb = (M + 31) / 32;
+  const int nchunk = d / KC;
+  for (int base = blockIdx.x * 4; base < nrb; base += gridDim.x * 4) {   // block-uniform
+    const int rb = base + wave;
+    const int arow = min(rb * 32 + l32, M - 1);
+    f32x16 acc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+    for (int c = 0; c < nchunk; ++c) {
+      if (nchunk > 1 || base == (int)blockIdx.x * 4) {
+        __syncthreads();                        // previous chunk consumed
+        for (int i = tid; i < NB * 32 * cpr; i += 256) {
+          const int r = i / cpr, ch = i % cpr;
+          uint4 v = make_uint4(0, 0, 0, 0);
+          if (r < A) v = *reinterpret_cast<const uint4 *>(wt + (size_t)r * d + c * KC + ch * 8);
+          *reinterpret_cast<uint4 *>(lds_out + ((size_t)r * cpr + (ch ^ (r & 15))) * 16) = v;
+        }
+        __syncthreads();
+      }
+      const bf16 *ap = u + (size_t)arow * d + c * KC + half * 8;
+      for (int k0 = 0; k0 < KC / 16; k0 += 8) {
+        bf16x8 af[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) af[j] = *reinterpret_cast<const bf16x8 *>(ap + (k0 + j) * 16);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int ch = 2 * (k0 + j) + half;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const int r = nb * 32 + l32;
+            const bf16x8 bfr = *reinterpret_cast<const bf16x8 *>(lds_out + ((size_t)r * cpr + (ch ^ (r & 15))) * 16);
+            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[j], bfr, acc[nb], 0, 0, 0);
+          }
+        }
+      }
+    }
+    if (rb >= nrb) continue;
+    // Lane holds output column nb 32 + lane % 32 of rows (r/4) 8 + 4 half + r%4.
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int col = nb * 32 + l32;
+      if (col >= A) continue;
+      const float bias = b_out[col];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = rb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+        if (row >= M) continue;
+        const ReqDesc q = reqs[row_req[row]];
+        const float v = acc[nb][r] + bias;
+        const float xn = x[(size_t)row * A + col] + (1.0f / (float)q.K) * v;
+        x[(size_t)row * A + col] = xn;
+        if (step == q.K - 1) q.actions[(size_t)(row - q.tok_off) * A + col] = xn;
+      }
+    }
+  }
+}
+
+size_t out_proj_lds_bytes(int d, int A) {
+  const int nb = A <= 32 ? 1 : 2;
+  const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
+  return (size_t)nb * 32 * kc * 2;
+}
+
+hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, const float *b_out, int A,
+                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (d % 128 || A < 1 || A > 64) return hipErrorInvalidValue;
+  const int nb = A <= 32 ? 1 : 2;
+  const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
+  const size_t lds = (size_t)nb * 32 * kc * 2;
+  static bool lds_raised[2] = {false, false};
+  if (!lds_raised[nb - 1]) {
+    const hipError_t e = hipFuncSetAttribute(nb == 1 ? (const void *)out_proj_euler_kernel<1> : (const void *)out_proj_euler_kernel<2>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+    if (e != hipSuccess) return e;
+    lds_raised[nb - 1] = true;
+  }
+  const int nrb = (M + 31) / 32;
+  const int blocks = std::min((nrb + 3) / 4, 256);
+  if (nb == 1)
+    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x);
+  else
+    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x);
+  return hipGetLastError();
+}
+
 }  // namespace rosa

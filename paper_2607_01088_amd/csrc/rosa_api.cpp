@@ -71,6 +71,7 @@ struct rosa_batch {
   // weights on the device
   float *w_in = nullptr, *b_in = nullptr, *b_t1 = nullptr, *b_t2 = nullptr, *b_modall = nullptr;
   float *w_out = nullptr, *b_out = nullptr;
+  void *wt_out = nullptr;            // bf16 mode: W_out transposed, [A][d]
   void *w_t1 = nullptr, *w_t2 = nullptr, *w_modall = nullptr;       // [K][N], activation dtype
   void *wt_qkv = nullptr, *wt_o = nullptr, *wt_up = nullptr, *wt_down = nullptr;  // [L][N][K]
 
@@ -487,6 +488,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->wt_down = dalloc<uint8_t>(b, L * d * D.dff * b->esz, e);
     b->w_out = dalloc<float>(b, d * D.A, e);
     b->b_out = dalloc<float>(b, D.A, e);
+    if (b->bf16) b->wt_out = dalloc<uint8_t>(b, (size_t)d * D.A * 2, e);
     // workspaces
     b->x = dalloc<float>(b, maxM * D.A, e);
     b->h = dalloc<float>(b, maxM * d, e);
@@ -551,6 +553,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     if (e == hipSuccess) e = upload_transposed(b, b->wt_down, w->w_down, D.L, D.dff, D.d);
     if (e == hipSuccess) e = hipMemcpy(b->w_out, w->w_out, d * D.A * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(b->b_out, w->b_out, D.A * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess && b->bf16) e = upload_transposed(b, b->wt_out, w->w_out, 1, D.d, D.A);
     if (e == hipSuccess) {
       std::vector<int32_t> id(maxM);
       for (size_t i = 0; i < maxM; ++i) id[i] = (int32_t)i;
@@ -630,11 +633,23 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
         gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
         e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, b->stream, b->gemm_cfg); });
       }
-      if (e == hipSuccess)
+      // Final norm with the final modulation, output projection and Euler step.
+      const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
+      if (e == hipSuccess && b->bf16) {
         e = timed(b, kcFinal, [&] {
-          return launch_final_euler(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, D.L * (int)d6, D.L * (int)d6 + D.d,
-                                    rowmod, b->w_out, b->b_out, D.A, b->row_req, d_reqs, k, b->x, b->stream);
+          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, b->u, true, b->stream);
         });
+        if (e == hipSuccess)
+          e = timed(b, kcFinal, [&] {
+            return launch_out_proj_euler((const __bf16 *)b->u, M, D.d, (const __bf16 *)b->wt_out, b->b_out, D.A, b->row_req,
+                                         d_reqs, k, b->x, b->stream);
+          });
+      } else if (e == hipSuccess) {
+        e = timed(b, kcFinal, [&] {
+          return launch_final_euler(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, b->w_out,
+                                    b->b_out, D.A, b->row_req, d_reqs, k, b->x, b->stream);
+        });
+      }
     }
     if (e != hipSuccess) return device_fail(b, e, "kernel launch");
     return ROSA_OK;

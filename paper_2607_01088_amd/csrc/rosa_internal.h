@@ -80,6 +80,11 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
                               const float *w_out, const float *b_out, int A, const int32_t *row_req,
                               const ReqDesc *reqs, int step, float *x, hipStream_t s);
 
+// bf16 mode: v = u W_out + b_out on final-normalized rows u (bf16 [M][d]), Euler step
+// x += v / K per row's request, actions written on its last step.  wt = W_out^T bf16 [A][d].
+hipError_t launch_out_proj_euler(const __bf16 *u, int M, int d, const __bf16 *wt, const float *b_out, int A,
+                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, hipStream_t s);
+
 // GEMM: C[M][N] = A[M][K] * W^T where Wt is [N][K] (K contiguous).
 struct GemmArgs {
   const void *a; int lda;
