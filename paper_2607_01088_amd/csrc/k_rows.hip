@@ -6,6 +6,7 @@
 // one 64-lane wavefront owns one row so that the RMS reduction is a single
 // wave reduction with no block barrier.
 #include <algorithm>
+#include <type_traits>
 
 #include "rosa_device.h"
 #include "rosa_internal.h"
@@ -75,8 +76,24 @@ hipError_t launch_in_proj(const float *x, int M, int A, const float *w_in, const
 }
 
 // u = h / sqrt(mean(h^2) + eps) * (1 + scale) + shift, with (shift, scale)
-// taken from the modulation-table row of the row's flow time.
+// taken from the modulation-table row of the row's flow time.  One wave per
+// row; the row is read once into registers (d <= 4096: at most 16 float4 per
+// lane), reduced, and written as 4-element vectors.
 template <typename OutT>
+__device__ __forceinline__ void store4(OutT *p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void store4<bf16>(bf16 *p, float a, float b, float c, float d) {
+  bf16x4 v;
+  v[0] = (bf16)a; v[1] = (bf16)b; v[2] = (bf16)c; v[3] = (bf16)d;
+  *reinterpret_cast<bf16x4 *>(p) = v;
+}
+template <>
+__device__ __forceinline__ void store4<float>(float *p, float a, float b, float c, float d) {
+  *reinterpret_cast<float4 *>(p) = make_float4(a, b, c, d);
+}
+
+constexpr int kNormChunks = 16;   // float4 per lane for d = 4096
+template <typename OutT, int NC>
 __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ h, int M, int d, float eps,
                                                       const float *__restrict__ modtab, int mod_stride,
                                                       int shift_off, int scale_off,
@@ -86,10 +103,15 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
   const float *hr = h + (size_t)row * d;
+  float4 v[NC];
   float ss = 0.f;
-  for (int i = lane * 4; i < d; i += 256) {
-    const float4 v = *reinterpret_cast<const float4 *>(hr + i);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) {
+      v[c] = *reinterpret_cast<const float4 *>(hr + i);
+      ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+    }
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
@@ -97,14 +119,15 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
   const float *shift = mrow + shift_off;
   const float *scale = mrow + scale_off;
   OutT *ur = u + (size_t)row * d;
-  for (int i = lane * 4; i < d; i += 256) {
-    const float4 v = *reinterpret_cast<const float4 *>(hr + i);
-    const float4 sc = *reinterpret_cast<const float4 *>(scale + i);
-    const float4 sh = *reinterpret_cast<const float4 *>(shift + i);
-    ur[i + 0] = from_f32<OutT>(v.x * r * (1.0f + sc.x) + sh.x);
-    ur[i + 1] = from_f32<OutT>(v.y * r * (1.0f + sc.y) + sh.y);
-    ur[i + 2] = from_f32<OutT>(v.z * r * (1.0f + sc.z) + sh.z);
-    ur[i + 3] = from_f32<OutT>(v.w * r * (1.0f + sc.w) + sh.w);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) {
+      const float4 sc = *reinterpret_cast<const float4 *>(scale + i);
+      const float4 sh = *reinterpret_cast<const float4 *>(shift + i);
+      store4<OutT>(ur + i, v[c].x * r * (1.0f + sc.x) + sh.x, v[c].y * r * (1.0f + sc.y) + sh.y,
+                   v[c].z * r * (1.0f + sc.z) + sh.z, v[c].w * r * (1.0f + sc.w) + sh.w);
+    }
   }
 }
 
@@ -112,13 +135,23 @@ hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *
                           int shift_off, int scale_off, const int32_t *rowmod, void *u, bool bf16_out,
                           hipStream_t s) {
   if (M <= 0) return hipSuccess;
+  if (d % 4 || d > kNormChunks * 256) return hipErrorInvalidValue;
   dim3 grid((M + 3) / 4);
-  if (bf16_out)
-    hipLaunchKernelGGL(modnorm_kernel<bf16>, grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
-                       shift_off, scale_off, rowmod, (bf16 *)u);
-  else
-    hipLaunchKernelGGL(modnorm_kernel<float>, grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
-                       shift_off, scale_off, rowmod, (float *)u);
+  const int nc = (d + 255) / 256;
+  auto go = [&](auto tag) {
+    constexpr int NC = decltype(tag)::value;
+    if (bf16_out)
+      hipLaunchKernelGGL((modnorm_kernel<bf16, NC>), grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
+                         shift_off, scale_off, rowmod, (bf16 *)u);
+    else
+      hipLaunchKernelGGL((modnorm_kernel<float, NC>), grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
+                         shift_off, scale_off, rowmod, (float *)u);
+  };
+  if (nc <= 1) go(std::integral_constant<int, 1>{});
+  else if (nc <= 2) go(std::integral_constant<int, 2>{});
+  else if (nc <= 4) go(std::integral_constant<int, 4>{});
+  else if (nc <= 8) go(std::integral_constant<int, 8>{});
+  else go(std::integral_constant<int, 16>{});
   return hipGetLastError();
 }
 
