@@ -59,6 +59,16 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
  * n_configs may be NULL. */
 rosa_status rosa_debug_gemm_config(rosa_batch *b, int32_t cfg, int32_t *n_configs);
 
+/* Number of lanes: a call with at least 64 requests per lane splits its
+ * requests into that many sub-batches of similar work, each on its own stream
+ * (the handle's stream for lane 0, internal default-priority streams for the
+ * others), forked after the time conditioning and joined back on the handle's
+ * stream before the call returns.  Requests are independent, so results are
+ * bitwise identical for any lane count; only the overlap of the sub-batches'
+ * kernels changes.  n in [1, 4]; the default is 2 in bf16 mode, 1 in fp32
+ * mode.  While per-kernel profiling is enabled every call runs one lane. */
+rosa_status rosa_debug_set_lanes(rosa_batch *b, int32_t n);
+
 /* Per-kernel timing.  While enabled, every launch of the handle is bracketed
  * by HIP events on the handle's stream and its duration is added to its
  * kernel class.  rosa_debug_get_profile synchronizes the stream, then fills up

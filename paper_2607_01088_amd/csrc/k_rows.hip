@@ -172,7 +172,7 @@ __global__ void __launch_bounds__(256) final_euler_kernel(
     int mod_stride, int shift_off, int scale_off, const int32_t *__restrict__ rowmod,
     const float *__restrict__ w_out, const float *__restrict__ b_out, int A,
     const int32_t *__restrict__ row_req, const ReqDesc *__restrict__ reqs, int step,
-    float *__restrict__ x, int resident) {
+    float *__restrict__ x, int resident, int first_row) {
   extern __shared__ float lds_final[];
   const int a_pad = A <= 32 ? 32 : 64;
   const int R = 256 / a_pad;                       // rows per group
@@ -224,7 +224,7 @@ __global__ void __launch_bounds__(256) final_euler_kernel(
       const float v = acc + b_out[my_a];
       const float xn = x[(size_t)row * A + my_a] + (1.0f / (float)q.K) * v;
       x[(size_t)row * A + my_a] = xn;
-      if (step == q.K - 1) q.actions[(size_t)(row - q.tok_off) * A + my_a] = xn;
+      if (step == q.K - 1) q.actions[(size_t)(first_row + row - q.tok_off) * A + my_a] = xn;
     }
   }
 }
@@ -232,7 +232,7 @@ __global__ void __launch_bounds__(256) final_euler_kernel(
 hipError_t launch_final_euler(const float *h, int M, int d, float eps, const float *modtab,
                               int mod_stride, int shift_off, int scale_off, const int32_t *rowmod,
                               const float *w_out, const float *b_out, int A, const int32_t *row_req,
-                              const ReqDesc *reqs, int step, float *x, hipStream_t s) {
+                              const ReqDesc *reqs, int step, float *x, int row0, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int a_pad = A <= 32 ? 32 : 64;
   const int R = 256 / a_pad;
@@ -251,7 +251,7 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
   // Resident: one block per CU walks the groups (W_out is loaded once per block).
   const int blocks = resident ? std::min(groups, 256) : std::min(groups, 1024);
   hipLaunchKernelGGL(final_euler_kernel, dim3(blocks), dim3(256), lds, s, h, M, d, eps, modtab, mod_stride,
-                     shift_off, scale_off, rowmod, w_out, b_out, A, row_req, reqs, step, x, resident);
+                     shift_off, scale_off, rowmod, w_out, b_out, A, row_req, reqs, step, x, resident, row0);
   return hipGetLastError();
 }
 
@@ -268,7 +268,7 @@ __global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restr
                                                              const bf16 *__restrict__ wt, const float *__restrict__ b_out,
                                                              int A, const int32_t *__restrict__ row_req,
                                                              const ReqDesc *__restrict__ reqs, int step,
-                                                             float *__restrict__ x) {
+                                                             float *__restrict__ x, int row0) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_out[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int cpr = KC / 8;                       // 16-byte chunks per LDS row
@@ -325,7 +325,7 @@ __global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restr
         const float v = acc[nb][r] + bias;
         const float xn = x[(size_t)row * A + col] + (1.0f / (float)q.K) * v;
         x[(size_t)row * A + col] = xn;
-        if (step == q.K - 1) q.actions[(size_t)(row - q.tok_off) * A + col] = xn;
+        if (step == q.K - 1) q.actions[(size_t)(row0 + row - q.tok_off) * A + col] = xn;
       }
     }
   }
@@ -338,7 +338,8 @@ size_t out_proj_lds_bytes(int d, int A) {
 }
 
 hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, const float *b_out, int A,
-                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, hipStream_t s) {
+                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, int row0,
+                                 hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (d % 128 || A < 1 || A > 64) return hipErrorInvalidValue;
   const int nb = A <= 32 ? 1 : 2;
@@ -354,9 +355,9 @@ hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, co
   const int nrb = (M + 31) / 32;
   const int blocks = std::min((nrb + 3) / 4, 256);
   if (nb == 1)
-    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x);
+    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x, row0);
   else
-    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x);
+    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x, row0);
   return hipGetLastError();
 }
 

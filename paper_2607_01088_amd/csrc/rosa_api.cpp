@@ -21,6 +21,8 @@ namespace {
 constexpr int kSplitTarget = 256;   // attention work items wanted per call before keys are split
 constexpr int kMinSplitKeys = 256;  // smallest key range worth a separate work item
 constexpr int kMaxSlots = 2 * kSplitTarget;
+constexpr int kMaxLanes = 4;
+constexpr int kMinLaneRequests = 64;  // a batch splits into lanes only with at least this many requests per lane
 
 enum KernelClass {
   kcTime = 0, kcSetup, kcInProj, kcModNorm, kcGemmQKV, kcAttention, kcMerge, kcGemmO, kcGemmUp,
@@ -52,6 +54,15 @@ struct Plan {
   std::vector<int32_t> items_upto;   // items of plan requests [0, r]
   std::vector<int32_t> groups_upto;
   int M0 = 0, Kmax = 0;
+  // Lanes: disjoint request sets run as independent sub-batches on their own
+  // streams.  Lane l owns plan positions [req_lo, req_hi) and stacked rows
+  // [row_lo, row_hi); at step k its active requests and rows are the prefixes
+  // n_act[k] and m[k] of those ranges (each lane is sorted by K descending).
+  struct Lane {
+    int req_lo = 0, req_hi = 0, row_lo = 0, row_hi = 0;
+    std::vector<int32_t> n_act, m;
+  };
+  std::vector<Lane> lanes;
 };
 
 }  // namespace
@@ -66,6 +77,11 @@ struct rosa_batch {
   hipStream_t stream = nullptr;
   bool poisoned = false;
   int gemm_cfg = -1;                 // forced projection block configuration, -1: cost model
+  // Lanes: sub-batches run concurrently; lane 0 uses `stream`, lane l > 0 its own
+  // stream (default priority), forked after the time conditioning and joined back.
+  int lanes = 1;
+  hipStream_t lane_stream[kMaxLanes] = {};
+  hipEvent_t ev_fork = nullptr, ev_join[kMaxLanes] = {};
   std::string last_error;
 
   // weights on the device
@@ -163,7 +179,7 @@ int attn_groups_per_block(const rosa_model_config *cfg) { return 4 * attn_groups
 
 // Validation of a request set (all-or-nothing) and the batch plan.
 rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
-                       int n, bool sort_by_steps, bool allow_split, Plan &p, std::string &err) {
+                       int n, bool sort_by_steps, bool allow_split, int lanes_wanted, Plan &p, std::string &err) {
   if (n < 0) { err = "n_reqs < 0"; return ROSA_E_INVALID; }
   if (n > 0 && !reqs) { err = "reqs is NULL"; return ROSA_E_INVALID; }
   if (n > cap->max_requests) { err = "more requests than max_requests"; return ROSA_E_CAPACITY; }
@@ -191,11 +207,40 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   if (sumP > cap->max_prefix_tokens) { err = "sum of prefix lengths above max_prefix_tokens"; return ROSA_E_CAPACITY; }
 
   p = Plan();
-  p.order.resize(n);
-  for (int i = 0; i < n; ++i) p.order[i] = i;
-  if (sort_by_steps)
-    std::stable_sort(p.order.begin(), p.order.end(),
-                     [&](int a, int b) { return reqs[a].num_steps > reqs[b].num_steps; });
+  // Lanes: requests dealt longest-first to the lane with the least estimated
+  // work (token-steps weighted by the attention's key count), then each lane
+  // sorted by step count, descending (stable).
+  const int n_lanes = std::max(1, std::min(lanes_wanted, n));
+  std::vector<int> lane_of(n, 0);
+  if (n_lanes > 1) {
+    std::vector<int> byw(n);
+    for (int i = 0; i < n; ++i) byw[i] = i;
+    auto work = [&](int i) {
+      const rosa_request &r = reqs[i];
+      return (double)r.horizon * r.num_steps * (1.0 + (double)(r.prefix_len + r.horizon) / 1800.0);
+    };
+    std::stable_sort(byw.begin(), byw.end(), [&](int a, int b2) { return work(a) > work(b2); });
+    std::vector<double> load(n_lanes, 0.0);
+    for (int i : byw) {
+      int best = 0;
+      for (int l = 1; l < n_lanes; ++l)
+        if (load[l] < load[best]) best = l;
+      lane_of[i] = best;
+      load[best] += work(i);
+    }
+  }
+  p.order.clear();
+  p.lanes.resize(n_lanes);
+  for (int l = 0; l < n_lanes; ++l) {
+    const size_t lo = p.order.size();
+    for (int i = 0; i < n; ++i)
+      if (lane_of[i] == l) p.order.push_back(i);
+    if (sort_by_steps)
+      std::stable_sort(p.order.begin() + lo, p.order.end(),
+                       [&](int a, int b2) { return reqs[a].num_steps > reqs[b2].num_steps; });
+    p.lanes[l].req_lo = (int)lo;
+    p.lanes[l].req_hi = (int)p.order.size();
+  }
   p.tok_off.resize(n);
   int M = 0;
   for (int i = 0; i < n; ++i) { p.tok_off[i] = M; M += reqs[p.order[i]].horizon; p.Kmax = std::max(p.Kmax, reqs[p.order[i]].num_steps); }
@@ -204,6 +249,14 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   p.n_active.assign(p.Kmax, 0);
   for (int i = 0; i < n; ++i)
     for (int k = 0; k < reqs[p.order[i]].num_steps; ++k) { p.m_k[k] += reqs[p.order[i]].horizon; p.n_active[k] += 1; }
+  for (Plan::Lane &ln : p.lanes) {
+    ln.row_lo = ln.req_lo < n ? p.tok_off[ln.req_lo] : M;
+    ln.row_hi = ln.req_hi < n ? p.tok_off[ln.req_hi] : M;
+    ln.n_act.assign(p.Kmax, 0);
+    ln.m.assign(p.Kmax, 0);
+    for (int i = ln.req_lo; i < ln.req_hi; ++i)
+      for (int k = 0; k < reqs[p.order[i]].num_steps; ++k) { ln.m[k] += reqs[p.order[i]].horizon; ln.n_act[k] += 1; }
+  }
 
   // Distinct flow times tau = k / K (fp32 division) and each (step, request)'s index.
   p.tau_idx.assign((size_t)p.Kmax * n, 0);
@@ -391,23 +444,27 @@ hipError_t run_time_conditioning(rosa_batch *b, const float *d_taus, int n_tau, 
   return e;
 }
 
-hipError_t run_attention(rosa_batch *b, const Plan &p, int n_act, int layer, const void *qkv, void *o) {
+// Attention of one layer for the requests at plan positions [r0, r0 + n_act).
+hipError_t run_attention(rosa_batch *b, const Plan &p, int r0, int n_act, int layer, const void *qkv, void *o,
+                         hipStream_t st) {
   const Dims &D = b->dims;
   const ReqDesc *reqs = (const ReqDesc *)((uint8_t *)b->d_plan + b->off_reqs);
   const AttnItem *items = (const AttnItem *)((uint8_t *)b->d_plan + b->off_items);
   const AttnGroup *groups = (const AttnGroup *)((uint8_t *)b->d_plan + b->off_groups);
   if (n_act <= 0) return hipSuccess;
+  const int it_lo = r0 > 0 ? p.items_upto[r0 - 1] : 0, it_hi = p.items_upto[r0 + n_act - 1];
+  const int gr_lo = r0 > 0 ? p.groups_upto[r0 - 1] : 0, gr_hi = p.groups_upto[r0 + n_act - 1];
   AttnArgs a{};
-  a.items = items; a.n_items = p.items_upto[n_act - 1];
+  a.items = items + it_lo; a.n_items = it_hi - it_lo;
   a.reqs = reqs; a.layer = layer;
   a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
   a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
   a.part_o = b->part_o; a.part_ml = b->part_ml;
-  hipError_t e = timed(b, kcAttention, [&] { return launch_attention(a, b->bf16, b->stream); });
-  const int ng = p.groups_upto[n_act - 1];
-  if (e == hipSuccess && ng > 0)
+  hipError_t e = timed(b, kcAttention, [&] { return launch_attention(a, b->bf16, st); });
+  if (e == hipSuccess && gr_hi > gr_lo)
     e = timed(b, kcMerge, [&] {
-      return launch_attn_merge(groups, ng, reqs, b->part_o, b->part_ml, o, D.o_dim, D.nq, D.nkv, D.hd, b->bf16, b->stream);
+      return launch_attn_merge(groups + gr_lo, gr_hi - gr_lo, reqs, b->part_o, b->part_ml, o, D.o_dim, D.nq, D.nkv,
+                               D.hd, b->bf16, st);
     });
   return e;
 }
@@ -421,6 +478,14 @@ void free_all(rosa_batch *b) {
   }
   for (auto &p : b->pending) { hipEventDestroy(p.a); hipEventDestroy(p.b); }
   for (auto e : b->free_events) hipEventDestroy(e);
+  for (int l = 1; l < kMaxLanes; ++l) {
+    if (b->lane_stream[l]) hipStreamDestroy(b->lane_stream[l]);
+    if (b->ev_join[l]) hipEventDestroy(b->ev_join[l]);
+    b->lane_stream[l] = nullptr;
+    b->ev_join[l] = nullptr;
+  }
+  if (b->ev_fork) hipEventDestroy(b->ev_fork);
+  b->ev_fork = nullptr;
 }
 
 }  // namespace
@@ -528,6 +593,13 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
       e = hipHostMalloc(&b->h_plan[i], b->plan_bytes, hipHostMallocDefault);
       if (e == hipSuccess) e = hipEventCreateWithFlags(&b->plan_copied[i], hipEventDisableTiming);
     }
+    b->lanes = b->bf16 ? 2 : 1;
+    b->lane_stream[0] = b->stream;
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&b->ev_fork, hipEventDisableTiming);
+    for (int l = 1; l < kMaxLanes && e == hipSuccess; ++l) {
+      e = hipStreamCreateWithFlags(&b->lane_stream[l], hipStreamNonBlocking);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&b->ev_join[l], hipEventDisableTiming);
+    }
     if (e != hipSuccess) { rosa_status s2 = fail(nullptr, ROSA_E_NOMEM, "pinned host allocation failed"); free_all(b); delete b; return s2; }
 
     // upload weights
@@ -576,7 +648,10 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
     if (b->poisoned) return fail(b, ROSA_E_DEVICE, "handle is poisoned by an earlier device error");
     Plan p;
     std::string err;
-    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, true, b->bf16, p, err);
+    // Lanes only without per-kernel profiling (its events live on one stream)
+    // and with enough requests for each lane.
+    const int lanes = b->prof ? 1 : std::max(1, std::min(b->lanes, n / kMinLaneRequests));
+    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, true, b->bf16, lanes, p, err);
     if (st != ROSA_OK) return fail(b, st, err);
     if (n == 0) return ROSA_OK;
     hipError_t e = hipSetDevice(b->device);
@@ -593,63 +668,88 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
       e = timed(b, kcSetup, [&] {
         return launch_setup_rows(d_reqs, n, d_tau_idx, p.Kmax, D.A, b->row_req, b->rowmod, p.M0, b->x, b->stream);
       });
+    // Fork: every other lane's stream waits for the plan, the modulation table
+    // and the row setup.
+    const int nl = (int)p.lanes.size();
+    if (e == hipSuccess && nl > 1) {
+      e = hipEventRecord(b->ev_fork, b->stream);
+      for (int li = 1; li < nl && e == hipSuccess; ++li) e = hipStreamWaitEvent(b->lane_stream[li], b->ev_fork, 0);
+    }
     const size_t d6 = (size_t)6 * D.d;
+    const size_t es = b->esz;
     for (int k = 0; k < p.Kmax && e == hipSuccess; ++k) {
-      const int M = p.m_k[k];
-      const int n_act = p.n_active[k];
-      const int32_t *rowmod = b->rowmod + (size_t)k * p.M0;
-      e = timed(b, kcInProj, [&] { return launch_in_proj(b->x, M, D.A, b->w_in, b->b_in, D.d, b->h, b->stream); });
-      for (int l = 0; l < D.L && e == hipSuccess; ++l) {
-        const int base = (int)(l * d6);
-        e = timed(b, kcModNorm, [&] {
-          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, b->u, b->bf16, b->stream);
-        });
-        if (e != hipSuccess) break;
-        GemmArgs g{};
-        g.a = b->u; g.lda = D.d; g.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * b->esz;
-        g.M = M; g.N = D.qkv_dim; g.K = D.d; g.epi = kEpiStore; g.out = b->qkv; g.ldo = D.qkv_dim;
-        e = timed(b, kcGemmQKV, [&] { return launch_gemm(g, b->bf16, b->stream, b->gemm_cfg); });
-        if (e != hipSuccess) break;
-        e = run_attention(b, p, n_act, l, b->qkv, b->o);
-        if (e != hipSuccess) break;
-        GemmArgs go{};
-        go.a = b->o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * b->esz;
-        go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = b->h; go.ldo = D.d;
-        go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
-        e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, b->stream, b->gemm_cfg); });
-        if (e != hipSuccess) break;
-        e = timed(b, kcModNorm, [&] {
-          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, b->u, b->bf16, b->stream);
-        });
-        if (e != hipSuccess) break;
-        GemmArgs gu{};
-        gu.a = b->u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * b->esz;
-        gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = b->g; gu.ldo = D.dff;
-        e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, b->stream, b->gemm_cfg); });
-        if (e != hipSuccess) break;
-        GemmArgs gd{};
-        gd.a = b->g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * b->esz;
-        gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = b->h; gd.ldo = D.d;
-        gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
-        e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, b->stream, b->gemm_cfg); });
-      }
-      // Final norm with the final modulation, output projection and Euler step.
-      const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
-      if (e == hipSuccess && b->bf16) {
-        e = timed(b, kcFinal, [&] {
-          return launch_modnorm(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, b->u, true, b->stream);
-        });
-        if (e == hipSuccess)
-          e = timed(b, kcFinal, [&] {
-            return launch_out_proj_euler((const __bf16 *)b->u, M, D.d, (const __bf16 *)b->wt_out, b->b_out, D.A, b->row_req,
-                                         d_reqs, k, b->x, b->stream);
+      for (int li = 0; li < nl && e == hipSuccess; ++li) {
+        const Plan::Lane &ln = p.lanes[li];
+        const int M = ln.m[k];
+        const int n_act = ln.n_act[k];
+        if (M == 0) continue;
+        const hipStream_t st = b->lane_stream[li];
+        const size_t r0 = (size_t)ln.row_lo;
+        // This lane's rows of every per-row buffer.
+        float *x = b->x + r0 * D.A, *h = b->h + r0 * D.d;
+        uint8_t *u = (uint8_t *)b->u + r0 * D.d * es, *qkv = (uint8_t *)b->qkv + r0 * D.qkv_dim * es;
+        uint8_t *o = (uint8_t *)b->o + r0 * D.o_dim * es, *g = (uint8_t *)b->g + r0 * D.dff * es;
+        const int32_t *rowmod = b->rowmod + (size_t)k * p.M0 + r0;
+        const int32_t *row_req = b->row_req + r0;
+        e = timed(b, kcInProj, [&] { return launch_in_proj(x, M, D.A, b->w_in, b->b_in, D.d, h, st); });
+        for (int l = 0; l < D.L && e == hipSuccess; ++l) {
+          const int base = (int)(l * d6);
+          e = timed(b, kcModNorm, [&] {
+            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16, st);
           });
-      } else if (e == hipSuccess) {
-        e = timed(b, kcFinal, [&] {
-          return launch_final_euler(b->h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, b->w_out,
-                                    b->b_out, D.A, b->row_req, d_reqs, k, b->x, b->stream);
-        });
+          if (e != hipSuccess) break;
+          GemmArgs gq{};
+          gq.a = u; gq.lda = D.d; gq.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * es;
+          gq.M = M; gq.N = D.qkv_dim; gq.K = D.d; gq.epi = kEpiStore; gq.out = qkv; gq.ldo = D.qkv_dim;
+          e = timed(b, kcGemmQKV, [&] { return launch_gemm(gq, b->bf16, st, b->gemm_cfg); });
+          if (e != hipSuccess) break;
+          e = run_attention(b, p, ln.req_lo, n_act, l, b->qkv, b->o, st);
+          if (e != hipSuccess) break;
+          GemmArgs go{};
+          go.a = o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
+          go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = h; go.ldo = D.d;
+          go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
+          e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg); });
+          if (e != hipSuccess) break;
+          e = timed(b, kcModNorm, [&] {
+            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, u,
+                                  b->bf16, st);
+          });
+          if (e != hipSuccess) break;
+          GemmArgs gu{};
+          gu.a = u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * es;
+          gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = g; gu.ldo = D.dff;
+          e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, st, b->gemm_cfg); });
+          if (e != hipSuccess) break;
+          GemmArgs gd{};
+          gd.a = g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * es;
+          gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = h; gd.ldo = D.d;
+          gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
+          e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, st, b->gemm_cfg); });
+        }
+        // Final norm with the final modulation, output projection and Euler step.
+        const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
+        if (e == hipSuccess && b->bf16) {
+          e = timed(b, kcFinal, [&] {
+            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, u, true, st);
+          });
+          if (e == hipSuccess)
+            e = timed(b, kcFinal, [&] {
+              return launch_out_proj_euler((const __bf16 *)u, M, D.d, (const __bf16 *)b->wt_out, b->b_out, D.A, row_req,
+                                           d_reqs, k, x, (int)r0, st);
+            });
+        } else if (e == hipSuccess) {
+          e = timed(b, kcFinal, [&] {
+            return launch_final_euler(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, b->w_out,
+                                      b->b_out, D.A, row_req, d_reqs, k, x, (int)r0, st);
+          });
+        }
       }
+    }
+    // Join: the caller's stream waits for every lane.
+    for (int li = 1; li < nl && e == hipSuccess; ++li) {
+      e = hipEventRecord(b->ev_join[li], b->lane_stream[li]);
+      if (e == hipSuccess) e = hipStreamWaitEvent(b->stream, b->ev_join[li], 0);
     }
     if (e != hipSuccess) return device_fail(b, e, "kernel launch");
     return ROSA_OK;
@@ -683,7 +783,7 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
     if (st != ROSA_OK) return st;
     Plan p;
     std::string err;
-    st = build_plan(cfg, cap, reqs, n, true, cfg->dtype == ROSA_BF16, p, err);
+    st = build_plan(cfg, cap, reqs, n, true, cfg->dtype == ROSA_BF16, 1, p, err);
     if (st != ROSA_OK) return st;
     for (int i = 0; i < n; ++i) {
       if (order) order[i] = p.order[i];
@@ -732,12 +832,12 @@ rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_
     if (!qkv || !o || layer < 0 || layer >= b->dims.L) return fail(b, ROSA_E_INVALID, "bad qkv/o/layer");
     Plan p;
     std::string err;
-    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, false, b->bf16, p, err);
+    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, false, b->bf16, 1, p, err);
     if (st != ROSA_OK) return fail(b, st, err);
     if (n == 0) return ROSA_OK;
     hipError_t e = hipSetDevice(b->device);
     if (e == hipSuccess) e = upload_plan(b, p, reqs, n);
-    if (e == hipSuccess) e = run_attention(b, p, n, layer, qkv, o);
+    if (e == hipSuccess) e = run_attention(b, p, 0, n, layer, qkv, o, b->stream);
     if (e != hipSuccess) return device_fail(b, e, "attention");
     return ROSA_OK;
   } catch (...) {
@@ -776,6 +876,13 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
   } catch (...) {
     return fail(b, ROSA_E_DEVICE, "unexpected exception");
   }
+}
+
+rosa_status rosa_debug_set_lanes(rosa_batch *b, int32_t n) {
+  if (!b) return ROSA_E_INVALID;
+  if (n < 1 || n > kMaxLanes) return fail(b, ROSA_E_INVALID, "lane count out of range");
+  b->lanes = n;
+  return ROSA_OK;
 }
 
 rosa_status rosa_debug_gemm_config(rosa_batch *b, int32_t cfg, int32_t *n_configs) {

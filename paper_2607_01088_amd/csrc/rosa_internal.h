@@ -78,12 +78,14 @@ hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *
 hipError_t launch_final_euler(const float *h, int M, int d, float eps, const float *modtab,
                               int mod_stride, int shift_off, int scale_off, const int32_t *rowmod,
                               const float *w_out, const float *b_out, int A, const int32_t *row_req,
-                              const ReqDesc *reqs, int step, float *x, hipStream_t s);
+                              const ReqDesc *reqs, int step, float *x, int row0, hipStream_t s);
 
 // bf16 mode: v = u W_out + b_out on final-normalized rows u (bf16 [M][d]), Euler step
 // x += v / K per row's request, actions written on its last step.  wt = W_out^T bf16 [A][d].
+// u, row_req and x point at the first of the M rows, which is stacked row row0.
 hipError_t launch_out_proj_euler(const __bf16 *u, int M, int d, const __bf16 *wt, const float *b_out, int A,
-                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, hipStream_t s);
+                                 const int32_t *row_req, const ReqDesc *reqs, int step, float *x, int row0,
+                                 hipStream_t s);
 
 // GEMM: C[M][N] = A[M][K] * W^T where Wt is [N][K] (K contiguous).
 struct GemmArgs {

@@ -86,6 +86,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_attention.restype = C.c_int
     lib.rosa_debug_gemm.argtypes = [vp, i32, i32, vp, i32, vp, vp]
     lib.rosa_debug_gemm.restype = C.c_int
+    lib.rosa_debug_set_lanes.argtypes = [vp, i32]
+    lib.rosa_debug_set_lanes.restype = C.c_int
     lib.rosa_debug_gemm_config.argtypes = [vp, i32, C.POINTER(i32)]
     lib.rosa_debug_gemm_config.restype = C.c_int
     lib.rosa_debug_set_profiling.argtypes = [vp, i32]
@@ -192,6 +194,10 @@ class ActionExpert:
     def gemm(self, which: int, layer: int, a, M: int, out, gate=None) -> None:
         self._check(self.lib.rosa_debug_gemm(self.handle, which, layer, a.data_ptr(), M, out.data_ptr(),
                                              None if gate is None else gate.data_ptr()))
+
+    def set_lanes(self, n: int) -> None:
+        """Number of concurrent sub-batches (streams) per call."""
+        self._check(self.lib.rosa_debug_set_lanes(self.handle, n))
 
     def gemm_config(self, cfg: int) -> int:
         """Force the projection block configuration (-1: cost model); returns

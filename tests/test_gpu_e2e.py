@@ -248,6 +248,26 @@ def test_projection_block_configs_bitwise_identical(pi0_expert):
             assert np.array_equal(a, b)
 
 
+def test_lane_counts_bitwise_identical(pi0_expert):
+    """Splitting the call into concurrent sub-batches (lanes) does not change
+    any request's actions."""
+    e, _ = pi0_expert
+    reqs = make_requests(PRESETS["factory_b256"], indices=list(range(128)))
+    db = _rosa().DeviceBatch(reqs, "bf16")
+    outs = []
+    try:
+        for lanes in (1, 2):
+            e.set_lanes(lanes)
+            e.generate(db.structs)
+            torch.cuda.synchronize()
+            outs.append(db.results())
+    finally:
+        e.set_lanes(2)
+    for o in outs[1:]:
+        for a, b in zip(o, outs[0]):
+            assert np.array_equal(a, b)
+
+
 # ------------------------------------------------------------------ ABI errors on a live handle
 
 def test_invalid_request_enqueues_nothing(pi0_expert):
