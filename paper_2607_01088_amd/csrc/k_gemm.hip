@@ -36,20 +36,29 @@ namespace rosa {
 // round-robin) works on a contiguous range of the row-major tile list: the
 // column tiles of one row panel share an XCD's L2.
 namespace gb {
-constexpr int BK = 32;
 constexpr int NST = 4;
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 }  // namespace gb
 
 #define ROSA_LDS(p) ((__attribute__((address_space(3))) void *)(p))
 
-template <int MB_, int TN_, int WM_, int WN_>
+// Chunk swizzle of an LDS row of CPR 16-byte chunks: chunk c of row r is
+// stored at c ^ gswz(r).  64-byte rows (CPR 4): (r / 4) % 4; 128-byte rows
+// (CPR 8): (r / 2) % 8.  Either way the 16 rows a 16-lane group reads at one
+// logical chunk fall in 16 distinct bank groups.
+template <int CPR>
+__device__ __forceinline__ int gswz(int r) { return CPR == 4 ? (r >> 2) & 3 : (r >> 1) & 7; }
+
+template <int MB_, int TN_, int WM_, int WN_, int BK_ = 32>
 struct GemmTile {
   static constexpr int MB = MB_, TN = TN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
   static constexpr int MBW = MB / WM;                                   // 32-row blocks per wave
   static constexpr int BM = 32 * MB, BN = 32 * TN * WN;
-  static constexpr int ABYTES = BM * gb::BK * 2, SBYTES = ABYTES + BN * gb::BK * 2;
-  static constexpr int U = (BM + BN) / 16;                              // 1 KB copies per stage
+  static constexpr int BK = BK_;                                        // K per stage
+  static constexpr int ROWB = BK * 2, CPR = ROWB / 16, RPU = 1024 / ROWB;   // row bytes, chunks per row, rows per 1 KB
+  static constexpr int ABYTES = BM * BK * 2, SBYTES = ABYTES + BN * BK * 2;
+  static constexpr int U = (BM + BN) / RPU;                             // 1 KB copies per stage
+  static_assert(BK == 32 || BK == 64, "stage K");
   static constexpr int CHI = (U + NW - 1) / NW, CLO = U / NW;           // copies per wave
   static constexpr int NHI = U % NW == 0 ? NW : U % NW;                 // waves with CHI copies
   static constexpr int PERB = SBYTES / 4096;                            // 4 KB epilogue slots per stage
@@ -82,23 +91,26 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
   const bf16 *W = reinterpret_cast<const bf16 *>(g.wt);
 
   // Copy sources: 1 KB unit u (A rows first, then W rows) is copied by wave
-  // u % NW; lane i writes physical chunk i % 4 of row i / 4 of the unit, which
-  // holds logical chunk (i % 4) ^ ((i / 16) % 4).  Rows past M (or N) re-read
-  // the last row; their results are never stored.
-  const int csrc = (lane & 3) ^ ((lane >> 4) & 3);
+  // u % NW; lane i writes physical chunk i % CPR of row i / CPR of the unit,
+  // which holds logical chunk (i % CPR) ^ gswz(row).  Rows past M (or N)
+  // re-read the last row; their results are never stored.
+  constexpr int CPR = T::CPR, RPU = T::RPU;
   const bf16 *src[CHI];
 #pragma unroll
   for (int j = 0; j < CHI; ++j) {
     const int u = min(j * NW + wave, T::U - 1);
-    if (u < T::BM / 16) {
-      const int row = min(m0 + u * 16 + (lane >> 2), g.M - 1);
+    const int lrow = u * RPU + lane / CPR;                   // row within the stage
+    const int csrc = (lane % CPR) ^ gswz<CPR>(lrow);
+    if (u < T::BM / RPU) {
+      const int row = min(m0 + lrow, g.M - 1);
       src[j] = A + (size_t)row * g.lda + csrc * 8;
     } else {
-      const int row = min(n0 + (u - T::BM / 16) * 16 + (lane >> 2), g.N - 1);
+      const int row = min(n0 + lrow - T::BM, g.N - 1);
       src[j] = W + (size_t)row * g.K + csrc * 8;
     }
   }
   const bool hi = wave < T::NHI;
+  constexpr int BK = T::BK, ROWB = T::ROWB;
   const int nk = g.K / BK;
   auto issue = [&](uint8_t *st, int kt) {
     const int k0 = min(kt, nk - 1) * BK;    // past the end: repeat the last stage (never read)
@@ -117,20 +129,23 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   // Operand reads: lane reads row (lane & 31) of a 32-row block, logical chunk
-  // 2 ks + lane / 32, at physical chunk (logical) ^ ((lane / 4) % 4).
-  const int swz = (lane >> 2) & 3;
-  const int ph0 = ((lane >> 5) ^ swz) * 16, ph1 = ((2 + (lane >> 5)) ^ swz) * 16;
-  const int arow = (wm * MBW * 32 + (lane & 31)) * 64;
-  const int brow = ABYTES + (wn * TN * 32 + (lane & 31)) * 64;
+  // 2 ks + lane / 32, at physical chunk (logical) ^ gswz(row); every 32-row
+  // block starts at a multiple of 32 rows, so the swizzle depends on lane & 31.
+  constexpr int NKS = BK / 16;
+  const int swz = gswz<CPR>(lane & 31);
+  int ph[NKS];
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) ph[ks] = ((2 * ks + (lane >> 5)) ^ swz) * 16;
+  const int arow = (wm * MBW * 32 + (lane & 31)) * ROWB;
+  const int brow = ABYTES + (wn * TN * 32 + (lane & 31)) * ROWB;
   auto compute = [&](const uint8_t *st) {
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int ph = ks == 0 ? ph0 : ph1;
+    for (int ks = 0; ks < NKS; ++ks) {
       bf16x8 af[MBW], bfr[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * 64 + ph);
+      for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * ROWB + ph[ks]);
 #pragma unroll
-      for (int i = 0; i < MBW; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * 64 + ph);
+      for (int i = 0; i < MBW; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * ROWB + ph[ks]);
 #pragma unroll
       for (int i = 0; i < MBW; ++i)
 #pragma unroll
@@ -235,22 +250,38 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
 
 // Block configurations and their measured cost on MI355X (one round of
 // blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
-// (store, GELU, gated residual).
-struct GemmCfg { int bm, bn; float a, b[3]; };
+// (store, GELU, gated residual); least-squares fits to the projection shapes
+// of the batch workloads at 2113 and 4241 rows.
+struct GemmCfg { int bm, bn, bk; float a, b[3]; };
 static constexpr GemmCfg kCfgs[kGemmConfigs] = {
-    {384, 128, 17.4f, {11.0f, 14.9f, 18.7f}},   // 0: 8 waves, 96 x 64 each
-    {256, 256, 21.2f, {9.7f, 17.3f, 15.9f}},    // 1: 16 waves, 64 x 64 each
-    {128, 256, 12.9f, {5.9f, 11.6f, 13.3f}},    // 2: 8 waves, 64 x 64 each
-    {192, 128, 13.7f, {2.2f, 5.1f, 7.8f}},      // 3: 8 waves, 96 x 32 each
-    {288, 128, 20.4f, {2.6f, 9.4f, 10.7f}},     // 4: 12 waves, 96 x 32 each
+    {384, 128, 32, 16.3f, {9.2f, 13.9f, 18.8f}},    // 0: 8 waves, 96 x 64 each
+    {256, 256, 32, 20.6f, {10.1f, 14.5f, 15.9f}},   // 1: 16 waves, 64 x 64 each
+    {128, 256, 32, 12.8f, {6.2f, 8.9f, 13.9f}},     // 2: 8 waves, 64 x 64 each
+    {192, 128, 32, 12.6f, {3.1f, 4.7f, 7.9f}},      // 3: 8 waves, 96 x 32 each
+    {288, 128, 32, 18.5f, {5.0f, 10.5f, 12.2f}},    // 4: 12 waves, 96 x 32 each
+    {128, 64, 64, 5.0f, {2.2f, 3.2f, 5.0f}},        // 5: 4 waves, 64 x 32 each
+    {192, 128, 64, 9.8f, {4.7f, 7.6f, 9.8f}},       // 6: 8 waves, 96 x 32 each
+    {128, 128, 64, 7.7f, {3.9f, 6.5f, 10.3f}},      // 7: 4 waves, 64 x 64 each
+    {160, 128, 64, 10.3f, {3.5f, 7.3f, 12.9f}},     // 8: 4 waves, 160 x 32 each
+    {96, 128, 64, 6.9f, {2.7f, 5.6f, 7.6f}},        // 9: 4 waves, 96 x 32 each
+    {256, 64, 64, 7.9f, {3.2f, 4.9f, 6.6f}},        // 10: 8 waves, 64 x 32 each
 };
 using Cfg0 = GemmTile<12, 2, 4, 2>;
 using Cfg1 = GemmTile<8, 2, 4, 4>;
 using Cfg2 = GemmTile<4, 2, 2, 4>;
 using Cfg3 = GemmTile<6, 1, 2, 4>;
 using Cfg4 = GemmTile<9, 1, 3, 4>;
+using Cfg5 = GemmTile<4, 1, 2, 2, 64>;
+using Cfg6 = GemmTile<6, 1, 2, 4, 64>;
+using Cfg7 = GemmTile<4, 2, 2, 2, 64>;
+using Cfg8 = GemmTile<5, 1, 1, 4, 64>;
+using Cfg9 = GemmTile<3, 1, 1, 4, 64>;
+using Cfg10 = GemmTile<8, 1, 4, 2, 64>;
 static_assert(Cfg0::BM == 384 && Cfg0::BN == 128 && Cfg1::BM == 256 && Cfg1::BN == 256 && Cfg2::BM == 128 &&
-              Cfg2::BN == 256 && Cfg3::BM == 192 && Cfg3::BN == 128 && Cfg4::BM == 288 && Cfg4::BN == 128,
+              Cfg2::BN == 256 && Cfg3::BM == 192 && Cfg3::BN == 128 && Cfg4::BM == 288 && Cfg4::BN == 128 &&
+              Cfg5::BM == 128 && Cfg5::BN == 64 && Cfg5::BK == 64 && Cfg6::BM == 192 && Cfg6::BN == 128 &&
+              Cfg6::BK == 64 && Cfg7::BM == 128 && Cfg7::BN == 128 && Cfg7::BK == 64 && Cfg8::BM == 160 &&
+              Cfg8::BN == 128 && Cfg9::BM == 96 && Cfg9::BN == 128 && Cfg10::BM == 256 && Cfg10::BN == 64,
               "cost table matches the tiles");
 
 template <typename T>
@@ -268,12 +299,21 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s) {
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   if (g.K % 128 != 0 || g.N % 8 != 0) return hipErrorInvalidValue;
+  // A configuration whose four-stage ring does not divide K runs as
+  // configuration 3 (same instruction sequence per output, so same results).
+  if (cfg >= 0 && cfg < kGemmConfigs && g.K % (4 * kCfgs[cfg].bk) != 0) cfg = 3;
   switch (cfg) {
     case 0: return launch_tile<Cfg0>(g, s);
     case 1: return launch_tile<Cfg1>(g, s);
     case 2: return launch_tile<Cfg2>(g, s);
     case 3: return launch_tile<Cfg3>(g, s);
     case 4: return launch_tile<Cfg4>(g, s);
+    case 5: return launch_tile<Cfg5>(g, s);
+    case 6: return launch_tile<Cfg6>(g, s);
+    case 7: return launch_tile<Cfg7>(g, s);
+    case 8: return launch_tile<Cfg8>(g, s);
+    case 9: return launch_tile<Cfg9>(g, s);
+    case 10: return launch_tile<Cfg10>(g, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -282,10 +322,11 @@ int gemm_pick_config(int M, int N, int K, int epi, int n_cu) {
   int best = 0;
   float best_t = 0.f;
   for (int c = 0; c < kGemmConfigs; ++c) {
+    if (K % (4 * kCfgs[c].bk) != 0) continue;
     const long tiles = (long)((M + kCfgs[c].bm - 1) / kCfgs[c].bm) * ((N + kCfgs[c].bn - 1) / kCfgs[c].bn);
     const long rounds = (tiles + n_cu - 1) / n_cu;
     const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].b[epi < 0 || epi > 2 ? 2 : epi]);
-    if (c == 0 || t < best_t) { best = c; best_t = t; }
+    if (best_t == 0.f || t < best_t) { best = c; best_t = t; }
   }
   return best;
 }

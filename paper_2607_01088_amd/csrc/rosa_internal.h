@@ -100,7 +100,7 @@ struct GemmArgs {
 hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1);
 // bf16 GEMM with a given block configuration (0: 384x128, 1: 256x256, 2: 128x256,
 // 3: 192x128, 4: 288x128).
-constexpr int kGemmConfigs = 5;
+constexpr int kGemmConfigs = 11;
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s);
 int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 
