@@ -56,8 +56,6 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
  * returned in *n_configs, or -1 for the built-in cost model (the default).
  * Every configuration computes each output with the same instruction sequence,
  * so results are bitwise identical whichever is used; only speed differs.
- * Configurations that stage 64 of K at a time need K to be a multiple of 256;
- * for other K a forced one runs as configuration 3 (the model never picks it).
  * n_configs may be NULL. */
 rosa_status rosa_debug_gemm_config(rosa_batch *b, int32_t cfg, int32_t *n_configs);
 

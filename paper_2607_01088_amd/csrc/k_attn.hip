@@ -35,6 +35,7 @@ namespace rosa {
 namespace at {
 constexpr int TK = 32;   // keys per LDS stage
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int waitcnt_lgkm0 = 15 | (3 << 14) | (7 << 4);   // lgkmcnt(0), others unconstrained
 // Chunk swizzle of LDS rows: 16-byte chunk c of row r is stored at c ^ swz(r),
 // swz(r) = the two 2-bit halves of r % 16 swapped.  The 16 consecutive rows
 // that one 16-lane group reads at one chunk (K operand), and the 4 rows x 4
@@ -88,18 +89,6 @@ struct AttnTile {
   static_assert((UNITS / 2) % 4 == 0 || UNITS / 2 < 4, "copy split");
 };
 
-// Maps block b to a work item so that the items of one request (consecutive
-// in the list) run on the same XCD at about the same time and share its L2:
-// blocks are handed to the 8 XCDs round-robin, and XCD x takes the x-th
-// eighth of the list in order.
-__device__ __forceinline__ int xcd_item(int b, int n_items) {
-  const int x = b & 7, q = b >> 3;
-  const int per = n_items >> 3, extra = n_items & 7;
-  const int start = x * per + min(x, extra);
-  const int len = per + (x < extra ? 1 : 0);
-  return q < len ? start + q : -1;
-}
-
 template <int HD, int NG>
 __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   using at::TK;
@@ -115,8 +104,11 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[8 * TILEB];
   static_assert(4 * TILEB <= 65536, "stage offsets must fit the LDS immediate");
 
-  const int item = xcd_item(blockIdx.x, a.n_items);
-  if (item < 0) return;
+  // Block b runs item list[9 + list[b % 8] + b / 8] if XCD b % 8 has that many.
+  const int x = blockIdx.x & 7, q = blockIdx.x >> 3;
+  const int l0 = a.list[x];
+  if (q >= a.list[x + 1] - l0) return;
+  const int item = a.list[9 + l0 + q];
   const AttnItem it = a.items[item];
   const ReqDesc rq = a.reqs[it.req];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -128,21 +120,24 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   // Q^T operand of group g, held for the whole item: lane holds
   // Q[row][16 s + 8 half .. + 7] for its row; rows past the item's queries
   // read the item's first row instead (their results are never stored).
+  // Loaded right after the first copy group is issued, so the two latencies
+  // overlap: the compiler does not see the copies, and its wait for Q (all
+  // loads it knows of) then also covers the copy group issued before it.
   bf16x8 qf[NG][NS];
+  auto load_q = [&]() __attribute__((always_inline)) {
 #pragma unroll
-  for (int g = 0; g < NG; ++g) {
-    const int loc = 32 * (wave + 4 * g) + (lane & 31);
-    const int qrow = it.q0 + (loc < it.nq ? loc : 0);
-    const bf16 *qp = qkv + (size_t)(rq.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
+    for (int g = 0; g < NG; ++g) {
+      const int loc = 32 * (wave + 4 * g) + (lane & 31);
+      const int qrow = it.q0 + (loc < it.nq ? loc : 0);
+      const bf16 *qp = qkv + (size_t)(rq.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
-  }
-  // Q must have landed before the first copy: the compiler does not see the
-  // copies, so a later wait of its own for Q would wait for them too.
+      for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
+    }
 #pragma unroll
-  for (int g = 0; g < NG; ++g)
+    for (int g = 0; g < NG; ++g)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) asm volatile("" : "+v"(qf[g][s]));
+      for (int s = 0; s < NS; ++s) asm volatile("" : "+v"(qf[g][s]));
+  };
 
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
   const bf16 *pk = reinterpret_cast<const bf16 *>(rq.pk) + (size_t)a.layer * rq.P * prow + (size_t)it.kvh * HD;
@@ -415,6 +410,7 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
       sources(j - 1, pv, av, vsrc);
 #pragma unroll
       for (int c = 0; c < NCP; ++c) copy(ksrc, vsrc, j, (j + 3) & 3, c);
+      if (j == 0 && pass0) load_q();        // lands with copy group 0
     }
     {   // step 0: S and P of the first tile, refill with group 3
       __builtin_amdgcn_s_waitcnt(T::WAIT);
@@ -460,16 +456,21 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
 
   // Accumulator layout: lane holds query (lane & 31) of the group; register r
   // of tile n holds head-dim index 32 n + (r/4)*8 + 4 half + r%4.
+  constexpr int CPRO = HD / 8;              // 16-byte chunks per output row
+  static_assert(4 * NG * 32 * 2 * HD <= 8 * TILEB, "output staging fits the rings");
+  __syncthreads();                          // every wave is done with the rings
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
     const float l_all = l_run[g] + __shfl_xor(l_run[g], 32, 64);
     const int loc = 32 * (wave + 4 * g) + (lane & 31);
     if (loc >= it.nq) continue;
     if (it.slot < 0) {
-      const int qrow = it.q0 + loc;
+      // Through LDS (the K ring, free now): lane q writes its query row's 8-byte
+      // pieces, chunk c of a row at c ^ (q % CPRO); then rows go out as whole
+      // 16-byte chunks, consecutive lanes on consecutive chunks of a row.
       const float inv = 1.0f / l_all;
-      bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(rq.tok_off + qrow / G) * a.ldo +
-                 (size_t)(it.kvh * G + qrow % G) * HD;
+      uint8_t *stg = smem + (wave * NG + g) * (32 * 2 * HD);
+      const int q = lane & 31;
 #pragma unroll
       for (int n = 0; n < NT; ++n)
 #pragma unroll
@@ -477,9 +478,36 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
           bf16x4 v;
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[g][n][rg * 4 + e] * inv);
-          *reinterpret_cast<bf16x4 *>(op + n * 32 + rg * 8 + half * 4) = v;
+          const int c = (4 * n + rg) ^ (q & (CPRO - 1));
+          *reinterpret_cast<bf16x4 *>(stg + q * 2 * HD + c * 16 + half * 8) = v;
         }
-    } else {
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(at::waitcnt_lgkm0);   // this wave's staging writes are done
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int base = 32 * (wave + 4 * g);
+    if (it.slot >= 0 || base >= it.nq) continue;
+    const uint8_t *stg = smem + (wave * NG + g) * (32 * 2 * HD);
+    constexpr int RPI = 64 / CPRO;          // rows per instruction
+#pragma unroll
+    for (int i = 0; i < 32 / RPI; ++i) {
+      const int r = i * RPI + lane / CPRO, c = lane % CPRO;
+      if (base + r < it.nq) {
+        const int qrow = it.q0 + base + r;
+        const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * 2 * HD + ((c ^ (r & (CPRO - 1))) * 16));
+        bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(rq.tok_off + qrow / G) * a.ldo +
+                   (size_t)(it.kvh * G + qrow % G) * HD;
+        *reinterpret_cast<uint4 *>(op + c * 8) = v;
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const float l_all = l_run[g] + __shfl_xor(l_run[g], 32, 64);
+    const int loc = 32 * (wave + 4 * g) + (lane & 31);
+    if (loc >= it.nq) continue;
+    if (it.slot >= 0) {
       float *po = a.part_o + ((size_t)it.slot * kAttnQB + loc) * HD;
 #pragma unroll
       for (int n = 0; n < NT; ++n)
@@ -595,7 +623,8 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
 hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
   if (bf16_mode) {
-    dim3 grid((a.n_items + 7) / 8 * 8);
+    if (a.n_blocks <= 0) return hipSuccess;
+    dim3 grid(a.n_blocks);
     switch (a.hd) {
       case 32: hipLaunchKernelGGL((attention_bf16_kernel<32, attn_groups_per_wave(32)>), grid, dim3(256), 0, s, a); break;
       case 64: hipLaunchKernelGGL((attention_bf16_kernel<64, attn_groups_per_wave(64)>), grid, dim3(256), 0, s, a); break;

@@ -36,7 +36,6 @@ namespace rosa {
 // round-robin) works on a contiguous range of the row-major tile list: the
 // column tiles of one row panel share an XCD's L2.
 namespace gb {
-constexpr int NST = 4;
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 }  // namespace gb
 
@@ -52,6 +51,7 @@ __device__ __forceinline__ int gswz(int r) { return CPR == 4 ? (r >> 2) & 3 : (r
 template <int MB_, int TN_, int WM_, int WN_, int BK_ = 32>
 struct GemmTile {
   static constexpr int MB = MB_, TN = TN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
+  static constexpr int NST = 4;                                         // LDS ring depth
   static constexpr int MBW = MB / WM;                                   // 32-row blocks per wave
   static constexpr int BM = 32 * MB, BN = 32 * TN * WN;
   static constexpr int BK = BK_;                                        // K per stage
@@ -63,27 +63,18 @@ struct GemmTile {
   static constexpr int NHI = U % NW == 0 ? NW : U % NW;                 // waves with CHI copies
   static constexpr int PERB = SBYTES / 4096;                            // 4 KB epilogue slots per stage
   static_assert(MBW * WM == MB, "row split");
-  static_assert(gb::NST * PERB >= NW, "epilogue staging space");
+  static_assert(NST * PERB >= NW, "epilogue staging space");
 };
 
-template <typename T, int EPI>
-__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct) {
+// K stages [kt0, kt0 + nk) of the tile at (m0, n0) into acc (zeroed first).
+// Ends with every copy landed and every wave past its last LDS read.
+template <typename T>
+__device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0, int kt0, int nk, uint8_t *L0,
+                                              uint8_t *L1, uint8_t *L2, uint8_t *L3,
+                                              f32x16 (&acc)[T::MBW][T::TN]) {
   using namespace gb;
-  constexpr int NW = T::NW, MBW = T::MBW, TN = T::TN, CHI = T::CHI, CLO = T::CLO;
-  constexpr int ABYTES = T::ABYTES, SBYTES = T::SBYTES;
-  __shared__ __attribute__((aligned(1024))) uint8_t L0[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L1[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L2[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L3[SBYTES];
-
-  // Tile of this block: XCD x = b % 8 takes the x-th eighth of the tile list.
-  const int n_tiles = nrt * nct;
-  const int b = blockIdx.x, x = b & 7, q = b >> 3;
-  const int per = n_tiles >> 3, extra = n_tiles & 7;
-  if (q >= per + (x < extra ? 1 : 0)) return;
-  const int tile = x * per + min(x, extra) + q;
-  const int m0 = (tile / nct) * T::BM, n0 = (tile % nct) * T::BN;
-
+  constexpr int NW = T::NW, MBW = T::MBW, TN = T::TN, CHI = T::CHI, CLO = T::CLO, NST = T::NST;
+  constexpr int ABYTES = T::ABYTES;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % NW;   // wave-uniform, in an SGPR
   const int wm = wave / T::WN, wn = wave % T::WN;
@@ -111,16 +102,14 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
   }
   const bool hi = wave < T::NHI;
   constexpr int BK = T::BK, ROWB = T::ROWB;
-  const int nk = g.K / BK;
   auto issue = [&](uint8_t *st, int kt) {
-    const int k0 = min(kt, nk - 1) * BK;    // past the end: repeat the last stage (never read)
+    const int k0 = (kt0 + min(kt, nk - 1)) * BK;   // past the end: repeat the last stage (never read)
 #pragma unroll
     for (int j = 0; j < CHI; ++j)
       if (j < CLO || hi)
         __builtin_amdgcn_global_load_lds((const void *)(src[j] + k0), ROSA_LDS(st + (j * NW + wave) * 1024), 16, 0, 0);
   };
 
-  f32x16 acc[MBW][TN];
 #pragma unroll
   for (int i = 0; i < MBW; ++i)
 #pragma unroll
@@ -164,18 +153,37 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
     compute(cur);
   };
 
+  // Stage s (relative to kt0) lives in L(s % 4).
   issue(L0, 0);
   issue(L1, 1);
   issue(L2, 2);
-  for (int kt = 0; kt < nk; kt += 4) {      // nk is a multiple of 4
+  int kt = 0;
+  for (; kt + 4 <= nk; kt += 4) {
     step(L0, L3, kt);
     step(L1, L0, kt + 1);
     step(L2, L1, kt + 2);
     step(L3, L2, kt + 3);
   }
+  if (kt < nk) {
+    step(L0, L3, kt);
+    if (kt + 1 < nk) {
+      step(L1, L0, kt + 1);
+      if (kt + 2 < nk) step(L2, L1, kt + 2);
+    }
+  }
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();                          // every wave is past its last stage read: LDS is free
+}
 
+// Epilogue of the tile at (m0, n0) from acc; stages through the ring's LDS,
+// which must be free (gemm_mainloop ends that way).
+template <typename T, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0, uint8_t *L0, uint8_t *L1,
+                                              uint8_t *L2, uint8_t *L3, f32x16 (&acc)[T::MBW][T::TN]) {
+  constexpr int MBW = T::MBW, TN = T::TN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % T::NW;
+  const int wm = wave / T::WN, wn = wave % T::WN;
   // Epilogue.  Register r of tile (i, j) holds row m0 + 32 (wm MBW + i) + lane % 32,
   // columns n0 + 32 (wn TN + j) + 8 (r / 4) + 4 (lane / 32) + r % 4: four
   // consecutive columns per 4 registers.  Each wave stages one 32 x 32 tile at a
@@ -248,6 +256,26 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
     }
 }
 
+template <typename T, int EPI>
+__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct) {
+  constexpr int SBYTES = T::SBYTES;
+  __shared__ __attribute__((aligned(1024))) uint8_t L0[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t L1[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t L2[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t L3[SBYTES];
+
+  // Tile of this block: XCD x = b % 8 takes the x-th eighth of the tile list.
+  const int n_tiles = nrt * nct;
+  const int b = blockIdx.x, x = b & 7, q = b >> 3;
+  const int per = n_tiles >> 3, extra = n_tiles & 7;
+  if (q >= per + (x < extra ? 1 : 0)) return;
+  const int tile = x * per + min(x, extra) + q;
+  const int m0 = (tile / nct) * T::BM, n0 = (tile % nct) * T::BN;
+  f32x16 acc[T::MBW][T::TN];
+  gemm_mainloop<T>(g, m0, n0, 0, g.K / T::BK, L0, L1, L2, L3, acc);
+  gemm_epilogue<T, EPI>(g, m0, n0, L0, L1, L2, L3, acc);
+}
+
 // Block configurations and their measured cost on MI355X (one round of
 // blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
 // (store, GELU, gated residual); least-squares fits to the projection shapes
@@ -277,11 +305,12 @@ using Cfg7 = GemmTile<4, 2, 2, 2, 64>;
 using Cfg8 = GemmTile<5, 1, 1, 4, 64>;
 using Cfg9 = GemmTile<3, 1, 1, 4, 64>;
 using Cfg10 = GemmTile<8, 1, 4, 2, 64>;
-static_assert(Cfg0::BM == 384 && Cfg0::BN == 128 && Cfg1::BM == 256 && Cfg1::BN == 256 && Cfg2::BM == 128 &&
-              Cfg2::BN == 256 && Cfg3::BM == 192 && Cfg3::BN == 128 && Cfg4::BM == 288 && Cfg4::BN == 128 &&
-              Cfg5::BM == 128 && Cfg5::BN == 64 && Cfg5::BK == 64 && Cfg6::BM == 192 && Cfg6::BN == 128 &&
-              Cfg6::BK == 64 && Cfg7::BM == 128 && Cfg7::BN == 128 && Cfg7::BK == 64 && Cfg8::BM == 160 &&
-              Cfg8::BN == 128 && Cfg9::BM == 96 && Cfg9::BN == 128 && Cfg10::BM == 256 && Cfg10::BN == 64,
+template <typename T>
+constexpr bool cfg_matches(const GemmCfg &c) { return T::BM == c.bm && T::BN == c.bn && T::BK == c.bk; }
+static_assert(cfg_matches<Cfg0>(kCfgs[0]) && cfg_matches<Cfg1>(kCfgs[1]) && cfg_matches<Cfg2>(kCfgs[2]) &&
+              cfg_matches<Cfg3>(kCfgs[3]) && cfg_matches<Cfg4>(kCfgs[4]) && cfg_matches<Cfg5>(kCfgs[5]) &&
+              cfg_matches<Cfg6>(kCfgs[6]) && cfg_matches<Cfg7>(kCfgs[7]) && cfg_matches<Cfg8>(kCfgs[8]) &&
+              cfg_matches<Cfg9>(kCfgs[9]) && cfg_matches<Cfg10>(kCfgs[10]),
               "cost table matches the tiles");
 
 template <typename T>
@@ -299,9 +328,6 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s) {
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   if (g.K % 128 != 0 || g.N % 8 != 0) return hipErrorInvalidValue;
-  // A configuration whose four-stage ring does not divide K runs as
-  // configuration 3 (same instruction sequence per output, so same results).
-  if (cfg >= 0 && cfg < kGemmConfigs && g.K % (4 * kCfgs[cfg].bk) != 0) cfg = 3;
   switch (cfg) {
     case 0: return launch_tile<Cfg0>(g, s);
     case 1: return launch_tile<Cfg1>(g, s);
@@ -319,13 +345,13 @@ hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) {
 }
 
 int gemm_pick_config(int M, int N, int K, int epi, int n_cu) {
+  const int e = epi < 0 || epi > 2 ? 2 : epi;
   int best = 0;
   float best_t = 0.f;
   for (int c = 0; c < kGemmConfigs; ++c) {
-    if (K % (4 * kCfgs[c].bk) != 0) continue;
     const long tiles = (long)((M + kCfgs[c].bm - 1) / kCfgs[c].bm) * ((N + kCfgs[c].bn - 1) / kCfgs[c].bn);
     const long rounds = (tiles + n_cu - 1) / n_cu;
-    const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].b[epi < 0 || epi > 2 ? 2 : epi]);
+    const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].b[e]);
     if (best_t == 0.f || t < best_t) { best = c; best_t = t; }
   }
   return best;

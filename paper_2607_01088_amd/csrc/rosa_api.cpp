@@ -23,6 +23,9 @@ constexpr int kMinSplitKeys = 256;  // smallest key range worth a separate work 
 constexpr int kMaxSlots = 2 * kSplitTarget;
 constexpr int kMaxLanes = 4;
 constexpr int kMinLaneRequests = 64;  // a batch splits into lanes only with at least this many requests per lane
+// Fixed cost of one attention work item (query loads, first copies, output
+// write, dispatch), in units of one 32-key step; measured on MI355X.
+constexpr int kItemOverheadSteps = 12;
 
 enum KernelClass {
   kcTime = 0, kcSetup, kcInProj, kcModNorm, kcGemmQKV, kcAttention, kcMerge, kcGemmO, kcGemmUp,
@@ -61,8 +64,14 @@ struct Plan {
   struct Lane {
     int req_lo = 0, req_hi = 0, row_lo = 0, row_hi = 0;
     std::vector<int32_t> n_act, m;
+    // Per step: offset of the attention launch order in attn_lists, and the
+    // launch's block count (8 x the longest per-XCD list).
+    std::vector<int32_t> list_at, list_blocks;
   };
   std::vector<Lane> lanes;
+  // Attention launch orders, one per distinct set of active requests of a
+  // lane: 9 offsets (XCD x's items at [off[x], off[x+1])) then item indices.
+  std::vector<int32_t> attn_lists;
 };
 
 }  // namespace
@@ -107,7 +116,8 @@ struct rosa_batch {
   bool plan_pending[2] = {false, false};
   int plan_flip = 0;
   size_t plan_bytes = 0;
-  size_t off_reqs = 0, off_tau_idx = 0, off_taus = 0, off_items = 0, off_groups = 0;
+  size_t off_reqs = 0, off_tau_idx = 0, off_taus = 0, off_items = 0, off_groups = 0, off_lists = 0;
+  size_t max_list_ints = 0;
 
   std::vector<void *> allocations;
 
@@ -321,6 +331,57 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
     p.groups_upto[i] = (int)p.groups.size();
   }
   if (slots > kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
+
+  // Attention launch orders.  Blocks reach the 8 XCDs round-robin (block b
+  // on XCD b % 8) and each XCD starts its blocks in order as CUs free up, so
+  // per set of active requests of a lane: requests go whole to an XCD (their
+  // query blocks share its L2), longest first to the least-loaded XCD, and
+  // each XCD's items run longest first.  Item cost = 32-key steps + a fixed
+  // overhead.  The order never changes what an item computes.
+  auto icost = [&](int it) -> int64_t { return (p.items[it].kend - p.items[it].kbeg + 31) / 32 + kItemOverheadSteps; };
+  for (Plan::Lane &ln : p.lanes) {
+    ln.list_at.assign(p.Kmax, -1);
+    ln.list_blocks.assign(p.Kmax, 0);
+    int prev_n = -1;
+    for (int k = 0; k < p.Kmax; ++k) {
+      const int na = ln.n_act[k];
+      if (na == 0) continue;
+      if (na == prev_n) { ln.list_at[k] = ln.list_at[k - 1]; ln.list_blocks[k] = ln.list_blocks[k - 1]; continue; }
+      prev_n = na;
+      struct RC { int lo, hi; int64_t cost; };
+      std::vector<RC> rc;
+      for (int i = ln.req_lo; i < ln.req_lo + na; ++i) {
+        const int lo = i > 0 ? p.items_upto[i - 1] : 0, hi = p.items_upto[i];
+        int64_t c = 0;
+        for (int j = lo; j < hi; ++j) c += icost(j);
+        rc.push_back({lo, hi, c});
+      }
+      std::stable_sort(rc.begin(), rc.end(), [](const RC &a, const RC &b2) { return a.cost > b2.cost; });
+      int64_t xload[8] = {};
+      std::vector<std::vector<int>> xitems(8);
+      for (const RC &r : rc) {
+        int best = 0;
+        for (int x = 1; x < 8; ++x)
+          if (xload[x] < xload[best]) best = x;
+        xload[best] += r.cost;
+        for (int it = r.lo; it < r.hi; ++it) xitems[best].push_back(it);
+      }
+      const int at = (int)p.attn_lists.size();
+      p.attn_lists.resize(at + 9);
+      int most = 0, cnt = 0;
+      for (int x = 0; x < 8; ++x) {
+        std::vector<int> &its = xitems[x];
+        std::stable_sort(its.begin(), its.end(), [&](int a, int b2) { return icost(a) > icost(b2); });
+        p.attn_lists[at + x] = cnt;
+        cnt += (int)its.size();
+        most = std::max(most, (int)its.size());
+      }
+      p.attn_lists[at + 8] = cnt;
+      for (int x = 0; x < 8; ++x) p.attn_lists.insert(p.attn_lists.end(), xitems[x].begin(), xitems[x].end());
+      ln.list_at[k] = at;
+      ln.list_blocks[k] = 8 * most;
+    }
+  }
   return ROSA_OK;
 }
 
@@ -403,7 +464,9 @@ hipError_t harvest_profile(rosa_batch *b) {
 
 // Copy the plan through a pinned staging buffer into the device plan region.
 hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, int n) {
-  if ((int64_t)p.items.size() > b->max_items || (int64_t)p.groups.size() > kMaxSlots) return hipErrorInvalidValue;
+  if ((int64_t)p.items.size() > b->max_items || (int64_t)p.groups.size() > kMaxSlots ||
+      p.attn_lists.size() > b->max_list_ints)
+    return hipErrorInvalidValue;
   const int slot = b->plan_flip;
   b->plan_flip ^= 1;
   if (b->plan_pending[slot]) {
@@ -423,7 +486,8 @@ hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, i
   std::memcpy(hp + b->off_taus, p.taus.data(), p.taus.size() * 4);
   std::memcpy(hp + b->off_items, p.items.data(), p.items.size() * sizeof(AttnItem));
   std::memcpy(hp + b->off_groups, p.groups.data(), p.groups.size() * sizeof(AttnGroup));
-  const size_t used = b->off_groups + p.groups.size() * sizeof(AttnGroup);
+  std::memcpy(hp + b->off_lists, p.attn_lists.data(), p.attn_lists.size() * 4);
+  const size_t used = b->off_lists + p.attn_lists.size() * 4;
   hipError_t e = hipMemcpyAsync(b->d_plan, hp, used, hipMemcpyHostToDevice, b->stream);
   if (e != hipSuccess) return e;
   e = hipEventRecord(b->plan_copied[slot], b->stream);
@@ -444,18 +508,25 @@ hipError_t run_time_conditioning(rosa_batch *b, const float *d_taus, int n_tau, 
   return e;
 }
 
-// Attention of one layer for the requests at plan positions [r0, r0 + n_act).
-hipError_t run_attention(rosa_batch *b, const Plan &p, int r0, int n_act, int layer, const void *qkv, void *o,
-                         hipStream_t st) {
+// Attention of one layer for the requests active at step k of lane ln.
+hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int k, int layer, const void *qkv,
+                         void *o, hipStream_t st) {
   const Dims &D = b->dims;
   const ReqDesc *reqs = (const ReqDesc *)((uint8_t *)b->d_plan + b->off_reqs);
   const AttnItem *items = (const AttnItem *)((uint8_t *)b->d_plan + b->off_items);
   const AttnGroup *groups = (const AttnGroup *)((uint8_t *)b->d_plan + b->off_groups);
+  const int32_t *lists = (const int32_t *)((uint8_t *)b->d_plan + b->off_lists);
+  const int r0 = ln.req_lo, n_act = ln.n_act[k];
   if (n_act <= 0) return hipSuccess;
   const int it_lo = r0 > 0 ? p.items_upto[r0 - 1] : 0, it_hi = p.items_upto[r0 + n_act - 1];
   const int gr_lo = r0 > 0 ? p.groups_upto[r0 - 1] : 0, gr_hi = p.groups_upto[r0 + n_act - 1];
   AttnArgs a{};
   a.items = items + it_lo; a.n_items = it_hi - it_lo;
+  if (b->bf16) {   // launch order of this step's active set (indices into the whole item array)
+    a.items = items;
+    a.list = lists + ln.list_at[k];
+    a.n_blocks = ln.list_blocks[k];
+  }
   a.reqs = reqs; a.layer = layer;
   a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
   a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
@@ -582,7 +653,10 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->off_taus = align(b->off_tau_idx + (size_t)cap->max_requests * cap->max_steps * 4);
     b->off_items = align(b->off_taus + kMaxTau * 4);
     b->off_groups = align(b->off_items + (size_t)b->max_items * sizeof(AttnItem));
-    b->plan_bytes = align(b->off_groups + (size_t)kMaxSlots * sizeof(AttnGroup));
+    b->off_lists = align(b->off_groups + (size_t)kMaxSlots * sizeof(AttnGroup));
+    // one launch order per step and lane at most: 9 offsets + the lane's items
+    b->max_list_ints = (size_t)cap->max_steps * ((size_t)b->max_items + 9 * kMaxLanes);
+    b->plan_bytes = align(b->off_lists + b->max_list_ints * 4);
     b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
     if (e != hipSuccess) {
       rosa_status s2 = e == hipErrorOutOfMemory ? fail(nullptr, ROSA_E_NOMEM, "device allocation failed")
@@ -703,7 +777,7 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
           gq.M = M; gq.N = D.qkv_dim; gq.K = D.d; gq.epi = kEpiStore; gq.out = qkv; gq.ldo = D.qkv_dim;
           e = timed(b, kcGemmQKV, [&] { return launch_gemm(gq, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
-          e = run_attention(b, p, ln.req_lo, n_act, l, b->qkv, b->o, st);
+          e = run_attention(b, p, ln, k, l, b->qkv, b->o, st);
           if (e != hipSuccess) break;
           GemmArgs go{};
           go.a = o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
@@ -837,7 +911,7 @@ rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_
     if (n == 0) return ROSA_OK;
     hipError_t e = hipSetDevice(b->device);
     if (e == hipSuccess) e = upload_plan(b, p, reqs, n);
-    if (e == hipSuccess) e = run_attention(b, p, 0, n, layer, qkv, o, b->stream);
+    if (e == hipSuccess) e = run_attention(b, p, p.lanes[0], 0, layer, qkv, o, b->stream);
     if (e != hipSuccess) return device_fail(b, e, "attention");
     return ROSA_OK;
   } catch (...) {

@@ -107,6 +107,10 @@ int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 // Attention of one layer.
 struct AttnArgs {
   const AttnItem *items; int n_items;
+  // bf16: launch order.  Block b runs item items[list[9 + list[b % 8] + b / 8]]
+  // if b / 8 < list[b % 8 + 1] - list[b % 8] (XCD b % 8's items), else exits;
+  // n_blocks blocks.  n_items is then unused.
+  const int32_t *list; int n_blocks;
   const ReqDesc *reqs;
   int layer;
   const void *qkv; int ldqkv;      // q at column g*hd, k_a at (nq+j)*hd, v_a at (nq+nkv+j)*hd
