@@ -184,20 +184,22 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % T::NW;
   const int wm = wave / T::WN, wn = wave % T::WN;
-  // Epilogue.  Register r of tile (i, j) holds row m0 + 32 (wm MBW + i) + lane % 32,
+  // Register r of tile (i, j) holds row m0 + 32 (wm MBW + i) + lane % 32,
   // columns n0 + 32 (wn TN + j) + 8 (r / 4) + 4 (lane / 32) + r % 4: four
-  // consecutive columns per 4 registers.  Each wave stages one 32 x 32 tile at a
-  // time in its own 4 KB slot, then reads it back row-contiguous.
-  const int sb = wave / T::PERB;
-  uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+  // consecutive columns per 4 registers.
   const int r32 = lane & 31, half = lane >> 5;
+  if constexpr (EPI == kEpiGatedResidual) {
+    // h += gate[rowmod[row]] * acc.  Each wave stages one 32 x 32 tile at a
+    // time in its own 4 KB slot (fp32: 32 rows x 8 chunks of 16 B, chunk c of
+    // row r at c ^ ((r / 2) % 8)), then reads it back row-contiguous.
+    const int sb = wave / T::PERB;
+    uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+    float *H = reinterpret_cast<float *>(g.out);
 #pragma unroll
-  for (int i = 0; i < MBW; ++i)
+    for (int i = 0; i < MBW; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
-      if constexpr (EPI == kEpiGatedResidual) {
-        // fp32 slot: 32 rows x 8 chunks of 16 B, chunk c of row r at c ^ ((r / 2) % 8).
+      for (int j = 0; j < TN; ++j) {
+        const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
           const int c = (2 * gq + half) ^ ((r32 >> 1) & 7);
@@ -213,7 +215,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           v[p] = *reinterpret_cast<const float4 *>(stg + rr * 128 + ((c ^ ((rr >> 1) & 7)) * 16));
           const int row = rb + rr;
           if (row < g.M && col < g.N) {
-            hv[p] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(g.out) + (size_t)row * g.ldo + col);
+            hv[p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
             gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
           }
         }
@@ -226,10 +228,20 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
             h.y = h.y + gt[p].y * v[p].y;
             h.z = h.z + gt[p].z * v[p].z;
             h.w = h.w + gt[p].w * v[p].w;
-            *reinterpret_cast<float4 *>(reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo + col) = h;
+            *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
           }
         }
-      } else {
+      }
+  } else {
+    // Each wave stages one 32 x 32 tile at a time in its own 4 KB slot, then
+    // reads it back row-contiguous.
+    const int sb = wave / T::PERB;
+    uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
         // bf16 slot: 32 rows x 4 chunks of 16 B (8 bf16), chunk c of row r at
         // c ^ ((r / 4) % 4); this lane's 4 values are half `half` of chunk gq.
 #pragma unroll
@@ -253,7 +265,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
             *reinterpret_cast<bf16x8 *>(reinterpret_cast<bf16 *>(g.out) + (size_t)row * g.ldo + col) = v;
         }
       }
-    }
+  }
 }
 
 template <typename T, int EPI>
@@ -279,20 +291,20 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
 // Block configurations and their measured cost on MI355X (one round of
 // blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
 // (store, GELU, gated residual); least-squares fits to the projection shapes
-// of the batch workloads at 2113 and 4241 rows.
+// of the batch workloads at 1060, 2113, 4241 and 8482 rows.
 struct GemmCfg { int bm, bn, bk; float a, b[3]; };
 static constexpr GemmCfg kCfgs[kGemmConfigs] = {
-    {384, 128, 32, 16.3f, {9.2f, 13.9f, 18.8f}},    // 0: 8 waves, 96 x 64 each
-    {256, 256, 32, 20.6f, {10.1f, 14.5f, 15.9f}},   // 1: 16 waves, 64 x 64 each
-    {128, 256, 32, 12.8f, {6.2f, 8.9f, 13.9f}},     // 2: 8 waves, 64 x 64 each
-    {192, 128, 32, 12.6f, {3.1f, 4.7f, 7.9f}},      // 3: 8 waves, 96 x 32 each
-    {288, 128, 32, 18.5f, {5.0f, 10.5f, 12.2f}},    // 4: 12 waves, 96 x 32 each
-    {128, 64, 64, 5.0f, {2.2f, 3.2f, 5.0f}},        // 5: 4 waves, 64 x 32 each
-    {192, 128, 64, 9.8f, {4.7f, 7.6f, 9.8f}},       // 6: 8 waves, 96 x 32 each
-    {128, 128, 64, 7.7f, {3.9f, 6.5f, 10.3f}},      // 7: 4 waves, 64 x 64 each
-    {160, 128, 64, 10.3f, {3.5f, 7.3f, 12.9f}},     // 8: 4 waves, 160 x 32 each
-    {96, 128, 64, 6.9f, {2.7f, 5.6f, 7.6f}},        // 9: 4 waves, 96 x 32 each
-    {256, 64, 64, 7.9f, {3.2f, 4.9f, 6.6f}},        // 10: 8 waves, 64 x 32 each
+    {384, 128, 32, 15.5f, {9.7f, 13.1f, 19.8f}},  // 0: 8 waves, 96 x 64 each
+    {256, 256, 32, 20.1f, {8.8f, 12.5f, 16.0f}},  // 1: 16 waves, 64 x 64 each
+    {128, 256, 32, 12.5f, {7.5f, 7.9f, 13.8f}},   // 2: 8 waves, 64 x 64 each
+    {192, 128, 32, 12.3f, {5.3f, 4.2f, 9.1f}},    // 3: 8 waves, 96 x 32 each
+    {288, 128, 32, 17.1f, {7.5f, 9.9f, 13.6f}},   // 4: 12 waves, 96 x 32 each
+    {128, 64, 64, 4.6f, {3.0f, 3.2f, 6.9f}},      // 5: 4 waves, 64 x 32 each
+    {192, 128, 64, 8.9f, {6.8f, 8.4f, 13.1f}},    // 6: 8 waves, 96 x 32 each
+    {128, 128, 64, 6.8f, {4.5f, 6.2f, 11.5f}},    // 7: 4 waves, 64 x 64 each
+    {160, 128, 64, 9.5f, {4.6f, 6.5f, 15.1f}},    // 8: 4 waves, 160 x 32 each
+    {96, 128, 64, 6.5f, {3.5f, 4.8f, 9.0f}},      // 9: 4 waves, 96 x 32 each
+    {256, 64, 64, 7.1f, {4.0f, 5.0f, 9.2f}},      // 10: 8 waves, 64 x 32 each
 };
 using Cfg0 = GemmTile<12, 2, 4, 2>;
 using Cfg1 = GemmTile<8, 2, 4, 4>;

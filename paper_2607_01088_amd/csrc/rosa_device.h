@@ -39,8 +39,11 @@ __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x));
 // exponential and one reciprocal instead of a tanh.  For large |x| the
 // exponential saturates to 0 or +inf, giving x or -0 exactly.
 __device__ __forceinline__ float gelu_tanh_f(float x) {
+  // x / (1 + 2^(k2 (x + 0.044715 x^3))); the hardware exp2 flushes results
+  // below 2^-126 to 0, where 1 + e is 1 in fp32 anyway.
   const float k2 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
-  const float e = exp2f(k2 * (x + 0.044715f * x * x * x));
+  const float u = fmaf(x * x, k2 * 0.044715f, k2);
+  const float e = __builtin_amdgcn_exp2f(x * u);
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
