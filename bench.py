@@ -139,6 +139,59 @@ def copy_probe(torch):
                       "launches": 5}), flush=True)
 
 
+def batch_profile(torch, rosa, expert, db, reqs, preset, args):
+    """Latency / throughput of one call per batch size B (the first B requests
+    of the workload, the System-1 batching profile of the paper's scheduler),
+    then the library's batch-size choice for closed-loop fleets."""
+    sizes, rows = [], []
+    B = len(reqs)
+    b = 1
+    while b <= B:
+        sizes.append(b)
+        b *= 2
+    stream = torch.cuda.current_stream()
+    for b in sizes:
+        sub = db.structs[:b]
+        for _ in range(max(2, args.warmup)):
+            expert.generate(sub)
+        n = max(5, args.steps)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        torch.cuda.synchronize()
+        for e0, e1 in evs:
+            e0.record(stream)
+            expert.generate(sub)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        lat = np.array([e0.elapsed_time(e1) for e0, e1 in evs])
+        rows.append({"batch": b, "p50_ms": round(float(np.percentile(lat, 50)), 3),
+                     "p99_ms": round(float(np.percentile(lat, 99)), 3),
+                     "chunks_per_s": round(b / (lat.mean() * 1e-3), 1),
+                     "actions_per_s": round(sum(r.horizon for r in reqs[:b]) / (lat.mean() * 1e-3), 1)})
+        print(f"[bench] B={b}: p50 {rows[-1]['p50_ms']} ms, {rows[-1]['chunks_per_s']} chunks/s",
+              file=sys.stderr, flush=True)
+    ms = [r["p50_ms"] for r in rows]
+    choices = []
+    for robots in [1, 16, 64, 256]:
+        for t_act in [50.0, 200.0]:
+            for slo in [0.0, 200.0]:
+                best, outs = rosa.s1_select_batch(sizes, ms, robots, t_act, slo, 2000)
+                entry = {"robots": robots, "t_act_ms": t_act, "slo_ms": slo,
+                         "batch": None if best is None else sizes[best]}
+                if best is not None:
+                    o = outs[best]
+                    one = outs[0]
+                    entry.update({"action_rate_hz": round(o["action_rate_hz"], 2),
+                                  "throughput_hz": round(o["throughput_hz"], 1),
+                                  "p99_ms": round(o["latency_p99_ms"], 2),
+                                  "gain_vs_batch1": round(o["throughput_hz"] / one["throughput_hz"], 2)
+                                  if one["feasible"] else None})
+                choices.append(entry)
+    print(json.dumps({"kind": "s1_batch_profile", "workload": preset.name, "dtype": preset.dtype,
+                      "profile": rows, "choices": choices,
+                      "server_model": "closed loop, FIFO, a batch starts when the worker is idle and B "
+                                      "requests wait; batch latency = measured p50"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -147,6 +200,10 @@ def main():
     ap.add_argument("--workload", default="factory_b256")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--batch-profile", action="store_true",
+                    help="System-1 batch-size profile: latency and throughput of one call on the first B "
+                         "requests of the workload for B = 1, 2, 4, ..., then the batch size the library "
+                         "chooses for a few robot fleets (prints its own JSON line)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -177,6 +234,10 @@ def main():
     print(f"[bench] uploaded (prefix KV {kv_bytes / 1e9:.2f} GB resident)", file=sys.stderr, flush=True)
 
     stream = torch.cuda.current_stream()
+    if args.batch_profile:
+        batch_profile(torch, rosa, expert, db, reqs, preset, args)
+        expert.close()
+        return
     for _ in range(args.warmup):
         expert.generate(db.structs)
     torch.cuda.synchronize()

@@ -46,6 +46,15 @@ class Request(C.Structure):
                 ("num_steps", C.c_int32), ("reserved", C.c_int32)]
 
 
+class S1Outcome(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("feasible", C.c_int32), ("throughput_hz", C.c_double),
+                ("action_rate_hz", C.c_double), ("latency_mean_ms", C.c_double),
+                ("latency_p50_ms", C.c_double), ("latency_p99_ms", C.c_double)]
+
+    def as_dict(self) -> Dict[str, float]:
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
 class RosaError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"rosa status {status}: {msg}")
@@ -95,6 +104,11 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64), C.POINTER(C.c_double),
                                            i32, C.POINTER(i32)]
     lib.rosa_debug_get_profile.restype = C.c_int
+    lib.rosa_s1_simulate.argtypes = [i32, i32, C.c_double, C.c_double, i32, C.POINTER(S1Outcome)]
+    lib.rosa_s1_simulate.restype = C.c_int
+    lib.rosa_s1_select_batch.argtypes = [C.POINTER(i32), C.POINTER(C.c_double), i32, i32, C.c_double, C.c_double,
+                                         i32, C.POINTER(i32), C.POINTER(S1Outcome)]
+    lib.rosa_s1_select_batch.restype = C.c_int
     _lib = lib
     return lib
 
@@ -142,6 +156,32 @@ def plan(shape, dtype: str, cap: Capacity, reqs: Sequence[Request]):
     counts = (C.c_int32 * 4)()
     st = lib.rosa_debug_plan(C.byref(cfg), C.byref(cap), arr, n, order, tok, mk, counts)
     return st, list(order)[:n], list(tok)[:n], list(mk)[:cap.max_steps], list(counts)
+
+
+def s1_simulate(robots: int, batch: int, batch_ms: float, t_act_ms: float, n_batches: int = 256) -> Dict[str, float]:
+    """Closed-loop simulation of one System-1 worker (rosa_s1_simulate)."""
+    lib = load()
+    o = S1Outcome()
+    st = lib.rosa_s1_simulate(robots, batch, batch_ms, t_act_ms, n_batches, C.byref(o))
+    if st != ROSA_OK:
+        raise RosaError(st, "rosa_s1_simulate: invalid arguments")
+    return o.as_dict()
+
+
+def s1_select_batch(batch_sizes: Sequence[int], batch_ms: Sequence[float], robots: int, t_act_ms: float,
+                    slo_ms: float, n_batches: int = 256):
+    """Batch-size choice from a measured profile (rosa_s1_select_batch):
+    returns (index or None, list of outcome dicts in input order)."""
+    lib = load()
+    n = len(batch_sizes)
+    sizes = (C.c_int32 * max(1, n))(*batch_sizes)
+    ms = (C.c_double * max(1, n))(*batch_ms)
+    outs = (S1Outcome * max(1, n))()
+    best = C.c_int32(-2)
+    st = lib.rosa_s1_select_batch(sizes, ms, n, robots, t_act_ms, slo_ms, n_batches, C.byref(best), outs)
+    if st != ROSA_OK:
+        raise RosaError(st, "rosa_s1_select_batch: invalid arguments")
+    return (None if best.value < 0 else best.value), [outs[i].as_dict() for i in range(n)]
 
 
 class ActionExpert:
