@@ -104,13 +104,9 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[8 * TILEB];
   static_assert(4 * TILEB <= 65536, "stage offsets must fit the LDS immediate");
 
-  // Block b runs item list[9 + list[b % 8] + b / 8] if XCD b % 8 has that many.
-  const int x = blockIdx.x & 7, q = blockIdx.x >> 3;
-  const int l0 = a.list[x];
-  if (q >= a.list[x + 1] - l0) return;
-  const int item = a.list[9 + l0 + q];
+  const int item = a.list[blockIdx.x];
+  if (item < 0) return;
   const AttnItem it = a.items[item];
-  const ReqDesc rq = a.reqs[it.req];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
   const int half = lane >> 5;
@@ -129,7 +125,7 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
     for (int g = 0; g < NG; ++g) {
       const int loc = 32 * (wave + 4 * g) + (lane & 31);
       const int qrow = it.q0 + (loc < it.nq ? loc : 0);
-      const bf16 *qp = qkv + (size_t)(rq.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
+      const bf16 *qp = qkv + (size_t)(it.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
 #pragma unroll
       for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
     }
@@ -140,10 +136,10 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   };
 
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
-  const bf16 *pk = reinterpret_cast<const bf16 *>(rq.pk) + (size_t)a.layer * rq.P * prow + (size_t)it.kvh * HD;
-  const bf16 *pv = reinterpret_cast<const bf16 *>(rq.pv) + (size_t)a.layer * rq.P * prow + (size_t)it.kvh * HD;
-  const bf16 *ak = qkv + (size_t)rq.tok_off * a.ldqkv + (size_t)(a.nq + it.kvh) * HD;
-  const bf16 *av = qkv + (size_t)rq.tok_off * a.ldqkv + (size_t)(a.nq + a.nkv + it.kvh) * HD;
+  const bf16 *pk = reinterpret_cast<const bf16 *>(it.pk) + (size_t)a.layer * it.P * prow + (size_t)it.kvh * HD;
+  const bf16 *pv = reinterpret_cast<const bf16 *>(it.pv) + (size_t)a.layer * it.P * prow + (size_t)it.kvh * HD;
+  const bf16 *ak = qkv + (size_t)it.tok_off * a.ldqkv + (size_t)(a.nq + it.kvh) * HD;
+  const bf16 *av = qkv + (size_t)it.tok_off * a.ldqkv + (size_t)(a.nq + a.nkv + it.kvh) * HD;
   const long ldq = a.ldqkv;
   // Tile t covers keys [k0 + 32 t, k0 + 32 t + 32) with k0 = kend - 32 nkt:
   // only tile 0 can reach below kbeg (those keys are masked), so the key
@@ -173,7 +169,7 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   };
   auto sources = [&](int t, const bf16 *pbase, const bf16 *abase, TileSrc &ts) __attribute__((always_inline)) {
     const int kt0 = k0 + max(0, min(t, nkt - 1)) * TK;
-    if (kt0 >= it.kbeg && kt0 + TK <= rq.P) {
+    if (kt0 >= it.kbeg && kt0 + TK <= it.P) {
       const bf16 *b = pbase + (size_t)kt0 * prow;
 #pragma unroll
       for (int j = 0; j < UPW; ++j) ts.lane[j] = b + poff[j];
@@ -188,8 +184,8 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
         const int row = (4 * j + wave) * T::RPU + ln / CPR;
         const int c = (ln % CPR) ^ at::swz(row, CPR);
         const int key = max(kt0 + row, it.kbeg);
-        const bool pre = key < rq.P;
-        const long roff = (pre ? (long)key * (long)prow : (long)(key - rq.P) * ldq) + c * 8;
+        const bool pre = key < it.P;
+        const long roff = (pre ? (long)key * (long)prow : (long)(key - it.P) * ldq) + c * 8;
         ts.lane[j] = (pre ? pbase : abase) + roff;
       }
     }
@@ -496,7 +492,7 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
       if (base + r < it.nq) {
         const int qrow = it.q0 + base + r;
         const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * 2 * HD + ((c ^ (r & (CPRO - 1))) * 16));
-        bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(rq.tok_off + qrow / G) * a.ldo +
+        bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(it.tok_off + qrow / G) * a.ldo +
                    (size_t)(it.kvh * G + qrow % G) * HD;
         *reinterpret_cast<uint4 *>(op + c * 8) = v;
       }

@@ -65,12 +65,12 @@ struct Plan {
     int req_lo = 0, req_hi = 0, row_lo = 0, row_hi = 0;
     std::vector<int32_t> n_act, m;
     // Per step: offset of the attention launch order in attn_lists, and the
-    // launch's block count (8 x the longest per-XCD list).
+    // launch's block count (8 x the longest per-XCD item list).
     std::vector<int32_t> list_at, list_blocks;
   };
   std::vector<Lane> lanes;
   // Attention launch orders, one per distinct set of active requests of a
-  // lane: 9 offsets (XCD x's items at [off[x], off[x+1])) then item indices.
+  // lane: the item index of each block (-1: the block exits).
   std::vector<int32_t> attn_lists;
 };
 
@@ -320,6 +320,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
         }
         for (int c = 0; c < nsplit; ++c) {
           AttnItem it{};
+          it.pk = r.prefix_k; it.pv = r.prefix_v; it.P = r.prefix_len; it.tok_off = p.tok_off[i];
           it.req = i; it.kvh = kvh; it.q0 = q0; it.nq = nq;
           it.kbeg = c * chunk;
           it.kend = std::min(nk, (c + 1) * chunk);
@@ -366,20 +367,19 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
         xload[best] += r.cost;
         for (int it = r.lo; it < r.hi; ++it) xitems[best].push_back(it);
       }
-      const int at = (int)p.attn_lists.size();
-      p.attn_lists.resize(at + 9);
-      int most = 0, cnt = 0;
+      size_t most = 0;
       for (int x = 0; x < 8; ++x) {
         std::vector<int> &its = xitems[x];
         std::stable_sort(its.begin(), its.end(), [&](int a, int b2) { return icost(a) > icost(b2); });
-        p.attn_lists[at + x] = cnt;
-        cnt += (int)its.size();
-        most = std::max(most, (int)its.size());
+        most = std::max(most, its.size());
       }
-      p.attn_lists[at + 8] = cnt;
-      for (int x = 0; x < 8; ++x) p.attn_lists.insert(p.attn_lists.end(), xitems[x].begin(), xitems[x].end());
+      // Block b = x + 8 q runs XCD x's q-th item (or exits).
+      const int at = (int)p.attn_lists.size();
+      p.attn_lists.resize(at + 8 * most, -1);
+      for (int x = 0; x < 8; ++x)
+        for (size_t q = 0; q < xitems[x].size(); ++q) p.attn_lists[at + x + 8 * q] = xitems[x][q];
       ln.list_at[k] = at;
-      ln.list_blocks[k] = 8 * most;
+      ln.list_blocks[k] = (int)(8 * most);
     }
   }
   return ROSA_OK;
@@ -654,8 +654,9 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->off_items = align(b->off_taus + kMaxTau * 4);
     b->off_groups = align(b->off_items + (size_t)b->max_items * sizeof(AttnItem));
     b->off_lists = align(b->off_groups + (size_t)kMaxSlots * sizeof(AttnGroup));
-    // one launch order per step and lane at most: 9 offsets + the lane's items
-    b->max_list_ints = (size_t)cap->max_steps * ((size_t)b->max_items + 9 * kMaxLanes);
+    // one launch order per step and lane at most: the lane's items plus at most
+    // 7 empty slots per XCD row of blocks
+    b->max_list_ints = (size_t)cap->max_steps * (8 * (size_t)b->max_items + 8 * kMaxLanes);
     b->plan_bytes = align(b->off_lists + b->max_list_ints * 4);
     b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
     if (e != hipSuccess) {

@@ -23,10 +23,14 @@ static_assert(sizeof(ReqDesc) == 64, "ReqDesc is 64 bytes");
 // action token q / G, query head kvh * G + q % G (G query heads per KV head).
 // slot >= 0: write unnormalized partial results to partial slot `slot`;
 // slot < 0: write o directly.
+// The request's prefix pointers, prefix length and first stacked row are
+// copied in, so a block needs one load to start its copies.
 struct AttnItem {
-  int32_t req, kvh, q0, nq, kbeg, kend, slot, pad0;
+  const void *pk, *pv;   // the request's prefix K and V, [L][P][n_kv][hd]
+  int32_t req, kvh, q0, nq, kbeg, kend, slot;
+  int32_t P, tok_off, pad0, pad1, pad2;
 };
-static_assert(sizeof(AttnItem) == 32, "AttnItem is 32 bytes");
+static_assert(sizeof(AttnItem) == 64, "AttnItem is 64 bytes");
 
 // A query block whose keys were split over n items (partial slots first_slot
 // .. first_slot + n - 1).
@@ -107,9 +111,8 @@ int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 // Attention of one layer.
 struct AttnArgs {
   const AttnItem *items; int n_items;
-  // bf16: launch order.  Block b runs item items[list[9 + list[b % 8] + b / 8]]
-  // if b / 8 < list[b % 8 + 1] - list[b % 8] (XCD b % 8's items), else exits;
-  // n_blocks blocks.  n_items is then unused.
+  // bf16: launch order.  Block b runs item items[list[b]], or exits if
+  // list[b] < 0; n_blocks blocks.  n_items is then unused.
   const int32_t *list; int n_blocks;
   const ReqDesc *reqs;
   int layer;
