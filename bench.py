@@ -200,6 +200,9 @@ def main():
     ap.add_argument("--workload", default="factory_b256")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lanes", type=int, default=0,
+                    help="concurrent sub-batches per call (0: the library default); the per-kernel timing "
+                         "pass always runs one lane")
     ap.add_argument("--batch-profile", action="store_true",
                     help="System-1 batch-size profile: latency and throughput of one call on the first B "
                          "requests of the workload for B = 1, 2, 4, ..., then the batch size the library "
@@ -228,6 +231,8 @@ def main():
     cap = rosa.capacity(len(reqs), max(r.horizon for r in reqs), sum(r.horizon for r in reqs),
                         max(r.steps for r in reqs), sum(r.prefix_len for r in reqs))
     expert = rosa.ActionExpert(preset.shape, preset.dtype, weights, cap)
+    if args.lanes > 0:
+        expert.set_lanes(args.lanes)
     db = rosa.DeviceBatch(reqs, preset.dtype)
     kv_bytes = sum(k.numel() * k.element_size() * 2 for k in db.k if k is not None)
     torch.cuda.synchronize()
