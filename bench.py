@@ -124,6 +124,84 @@ def cpu_baseline(preset, weights, reqs_meta, budget_s: float):
     }
 
 
+def _csv_rows(pattern):
+    import csv
+    import glob
+    f = glob.glob(pattern, recursive=True)
+    if not f:
+        raise SystemExit(f"missing {pattern}")
+    return list(csv.DictReader(open(f[0])))
+
+
+def _counter_avg(rs, kernel_prefix):
+    v = [float(r["Counter_Value"]) for r in rs if r["Kernel_Name"].startswith(kernel_prefix)]
+    return sum(v) / len(v), len(v)
+
+
+def summarize_profiles(out):
+    """Turn rocprofv3 outputs of this script into the summaries under
+    profiles/ (kernel-time table, calibrated HBM traffic of the attention
+    kernel).  `out` holds a --kernel-trace --stats run (prof_factory/),
+    FETCH_SIZE and WRITE_SIZE --pmc runs (pmc_fetch/, pmc_write/) and the same
+    counters for --copy-probe (pmc_cfetch/, pmc_cwrite/); the commands are
+    written into the summaries."""
+    import csv
+    import glob
+    stats = _csv_rows(f"{out}/prof_factory/**/*kernel_stats.csv")
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["# Kernel-time summary: factory_b256 workload (256 ragged requests, pi0-shaped expert, bf16)", "",
+             "Command (one MI355X, repository root, library built in-tree; one lane, so every dispatch",
+             "runs alone as in bench.py's per-kernel timing pass):", "", "```",
+             "export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_factory "
+             "-o factory -- python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --lanes 1", "```", "",
+             "The profiled process runs 1 warm-up + 3 timed + 2 per-kernel-timing generate calls (6 calls).",
+             "Table from `factory_kernel_stats.csv`, sorted by total time.", "",
+             "| Kernel | Calls | Avg (us) | Total (ms) | % |", "|---|---:|---:|---:|---:|"]
+    for r in stats:
+        name = r["Name"].split("(")[0]
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    open(os.path.join(PROFILES, "kernel_stats_factory_b256.md"), "w").write("\n".join(lines) + "\n")
+
+    fetch, nf = _counter_avg(_csv_rows(f"{out}/pmc_fetch/**/*counter_collection.csv"), "void rosa::attention_bf16")
+    write, nw = _counter_avg(_csv_rows(f"{out}/pmc_write/**/*counter_collection.csv"), "void rosa::attention_bf16")
+    cf, _ = _counter_avg(_csv_rows(f"{out}/pmc_cfetch/**/*counter_collection.csv"), "__amd_rocclr_copyBuffer")
+    cw, _ = _counter_avg(_csv_rows(f"{out}/pmc_cwrite/**/*counter_collection.csv"), "__amd_rocclr_copyBuffer")
+    gib_kib = float(1 << 20)
+    ff, wf = gib_kib / cf, gib_kib / cw
+    rd, wr = fetch * ff * 1024, write * wf * 1024
+    sha = hashlib.sha256(open(os.path.join(ROOT, "paper_2607_01088_amd", "csrc", "k_attn.hip"), "rb").read())
+    t = {"kernel": "attention", "workload": "factory_b256", "source_sha": sha.hexdigest()[:16], "dispatches": nf,
+         "fetch_size_kib_avg": round(fetch, 1), "write_size_kib_avg": round(write, 1),
+         "copy_probe_fetch_kib": round(cf, 1), "copy_probe_write_kib": round(cw, 1),
+         "fetch_factor": round(ff, 4), "write_factor": round(wf, 4), "hbm_bytes_per_launch": int(rd + wr)}
+    json.dump(t, open(os.path.join(PROFILES, "traffic_attention_factory_b256.json"), "w"), indent=1)
+    md = ["# HBM traffic of the attention kernel, factory_b256 workload", "",
+          "Commands (one MI355X, repository root, library built in-tree; one counter per run, one lane):", "", "```",
+          "export TMPDIR=/tmp",
+          "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o f -- "
+          "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
+          "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o w -- "
+          "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
+          "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_cfetch -o f -- "
+          "python -u bench.py --copy-probe",
+          "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_cwrite -o w -- "
+          "python -u bench.py --copy-probe",
+          "python bench.py --summarize-profiles gpurun_out", "```", "",
+          f"Calibration: the copy probe reads and writes 1 GiB (1048576 KiB) per launch; FETCH_SIZE reads "
+          f"{cf:.1f} KiB and WRITE_SIZE {cw:.1f} KiB per dispatch, so FETCH_SIZE is scaled by {ff:.4f} and "
+          f"WRITE_SIZE by {wf:.4f}.", "",
+          "| Kernel | Dispatches | FETCH_SIZE (KiB, avg) | WRITE_SIZE (KiB, avg) | HBM read (MB) | HBM write (MB) |",
+          "|---|---:|---:|---:|---:|---:|",
+          f"| `rosa::attention_bf16_kernel<256, 1>` | {nf} | {fetch:.1f} | {write:.1f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} |",
+          "", f"Per launch: {(rd + wr) / 1e6:.1f} MB of HBM traffic.  Algorithmic bytes per launch (each active "
+          "request's prefix K and V of the layer read once) are 174 MB averaged over the 180 launches of one call; "
+          "queries, action keys and the output add about 26 MB written and 30 MB read.", "",
+          f"Kernel source sha256 (first 16 hex digits) of `k_attn.hip` when measured: `{t['source_sha']}`."]
+    open(os.path.join(PROFILES, "traffic_attention_factory_b256.md"), "w").write("\n".join(md) + "\n")
+    print(json.dumps(t))
+
+
 def copy_probe(torch):
     """A plain copy of known size: each launch reads and writes exactly 1 GiB.
     Its FETCH_SIZE / WRITE_SIZE readings give the factor that turns those
@@ -207,9 +285,14 @@ def main():
                     help="System-1 batch-size profile: latency and throughput of one call on the first B "
                          "requests of the workload for B = 1, 2, 4, ..., then the batch size the library "
                          "chooses for a few robot fleets (prints its own JSON line)")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="write the profiles/ summaries from rocprofv3 outputs under DIR and exit (no GPU)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (calibrates HBM byte counters)")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported in this build "
               "(requests shard across GPUs with no exchange; see DESIGN.md).", file=sys.stderr)
