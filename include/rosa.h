@@ -111,8 +111,14 @@ typedef struct rosa_capacity {
  *   prefix_k, prefix_v: the request's cached prefix, layout [L][P][n_kv][head_dim]
  *       in the model dtype (bf16 or fp32), contiguous; layer stride P*n_kv*head_dim.
  *       Read only.  May be NULL when P == 0.  Several requests may share them.
- *   noise:   [H][A] fp32, the initial action chunk x_0.
- *   actions: [H][A] fp32, receives x_K.  May alias noise.                       */
+ *   noise:   [H][A] fp32, the initial action chunk x_0 (read when start_step
+ *            is 0; may be NULL otherwise).
+ *   actions: [H][A] fp32, receives the Euler state after the last step the call
+ *            runs for this request: x_K once every step is done.  When
+ *            start_step > 0 it must hold x_{start_step}, as a previous call left
+ *            it.  May alias noise.
+ *   start_step: Euler steps already done (0 <= start_step < K): a request can
+ *            be advanced over several calls and join a batch between steps.   */
 typedef struct rosa_request {
   const void  *prefix_k;
   const void  *prefix_v;
@@ -121,7 +127,7 @@ typedef struct rosa_request {
   int32_t      prefix_len;    /* P >= 0 */
   int32_t      horizon;       /* 1 <= H <= max_horizon */
   int32_t      num_steps;     /* 1 <= K <= max_steps; dt = 1/K, tau_k = k/K */
-  int32_t      reserved;      /* must be 0 */
+  int32_t      start_step;    /* 0 <= start_step < K */
 } rosa_request;
 
 /* Create a handle: validate the configuration, upload and repack the weights,
@@ -134,13 +140,27 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
                               const rosa_capacity *cap, void *hip_stream, rosa_batch **out);
 
 /* Generate the action chunks of n_reqs requests (the batch), asynchronously on
- * the handle's stream.  Requests may differ in P, H and K; each result equals
- * that request computed alone (up to floating-point summation order).
+ * the handle's stream: every request runs its Euler steps start_step .. K-1.
+ * Requests may differ in P, H, K and start_step; each result equals that
+ * request computed alone (up to floating-point summation order).
  * n_reqs == 0 is a no-op returning ROSA_OK.  Errors: ROSA_E_INVALID (NULL
- * pointers, P < 0, H < 1, K < 1, H > max_horizon, K > max_steps, reserved != 0,
- * NULL prefix with P > 0), ROSA_E_CAPACITY (n_reqs, sum H or sum P above the
- * capacity), ROSA_E_DEVICE (HIP failure or poisoned handle). */
+ * pointers, P < 0, H < 1, K < 1, H > max_horizon, K > max_steps, start_step
+ * outside [0, K), NULL prefix with P > 0, NULL noise with start_step 0),
+ * ROSA_E_CAPACITY (n_reqs, sum H or sum P above the capacity), ROSA_E_DEVICE
+ * (HIP failure or poisoned handle). */
 rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32_t n_reqs);
+
+/* Step-level batching: like rosa_generate_actions, but each request runs at
+ * most max_steps (>= 1) of its remaining steps, from start_step, and its
+ * actions buffer receives the state after the last of them.  A caller that
+ * advances a set of requests a step or a few at a time can admit new requests
+ * (start_step 0) and retire finished ones (start_step + steps run == K)
+ * between calls, so a request never waits for a whole batch to finish.  The
+ * paper batches its autoregressive models this way (continuous batching) and
+ * System-1 in discrete batches (Sec. 3.4.1); for the flow-matching expert the
+ * Euler steps are the natural boundaries.  Errors as rosa_generate_actions,
+ * and ROSA_E_INVALID for max_steps < 1. */
+rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t n_reqs, int32_t max_steps);
 
 /* Wait for the handle's stream, then free everything.  NULL-safe. */
 void rosa_destroy(rosa_batch *b);

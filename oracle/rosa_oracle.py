@@ -168,6 +168,19 @@ class OracleModel:
             x = x + dt * self.velocity(x, tau, prefix_k, prefix_v)
         return x
 
+    def advance(self, x: np.ndarray, num_steps: int, k0: int, k1: int, prefix_k: np.ndarray,
+                prefix_v: np.ndarray) -> np.ndarray:
+        """Euler steps k0 .. k1-1 of the same grid from the state x_{k0}:
+        returns x_{k1}.  Step-level batching (admission and retirement between
+        steps, the continuous batching the paper applies to its
+        autoregressive models, Sec. 3.4.1) only regroups these steps."""
+        x = np.asarray(x, dtype=F).copy()
+        dt = 1.0 / num_steps
+        taus = tau_grid(num_steps)
+        for k in range(k0, k1):
+            x = x + dt * self.velocity(x, taus[k], prefix_k, prefix_v)
+        return x
+
     def generate(self, requests: Sequence) -> List[np.ndarray]:
         """A batch is a list of independent requests; each result depends on its
         own request only."""

@@ -13,17 +13,19 @@
 
 namespace rosa {
 
-// One block per request: copy its noise into the Euler state x, record the
-// owning request of each of its rows, and for every step k < K_r the row of
-// the modulation table that holds tau = k / K_r.
+// One block per request: copy its Euler state into x (the noise for a fresh
+// request, else the state a previous call left in its actions), record the
+// owning request of each of its rows, and for every step j < S_r of this call
+// the row of the modulation table that holds tau = (k0_r + j) / K_r.
 __global__ void setup_rows_kernel(const ReqDesc *__restrict__ reqs, const int32_t *__restrict__ tau_idx,
                                   int n_req, int A, int32_t *__restrict__ row_req,
                                   int32_t *__restrict__ rowmod, int M0, float *__restrict__ x) {
   const int r = blockIdx.x;
   const ReqDesc q = reqs[r];
-  for (int i = threadIdx.x; i < q.H * A; i += blockDim.x) x[(size_t)q.tok_off * A + i] = q.noise[i];
+  const float *x0 = q.k0 == 0 ? q.noise : q.actions;
+  for (int i = threadIdx.x; i < q.H * A; i += blockDim.x) x[(size_t)q.tok_off * A + i] = x0[i];
   for (int t = threadIdx.x; t < q.H; t += blockDim.x) row_req[q.tok_off + t] = r;
-  for (int i = threadIdx.x; i < q.H * q.K; i += blockDim.x) {
+  for (int i = threadIdx.x; i < q.H * q.S; i += blockDim.x) {
     const int k = i / q.H, t = i - k * q.H;
     rowmod[(size_t)k * M0 + q.tok_off + t] = tau_idx[k * n_req + r];
   }
@@ -156,7 +158,7 @@ hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *
 }
 
 // Final modulated RMSNorm, velocity v = norm W_out + b_out, Euler step
-// x += (1/K_r) v, and on the request's last step the store of x into the
+// x += (1/K_r) v, and on the request's last step of this call the store of x into the
 // caller's action chunk.
 //
 // A block takes groups of R rows (R = 256 / A_pad, A_pad = 32 or 64): its
@@ -224,7 +226,7 @@ __global__ void __launch_bounds__(256) final_euler_kernel(
       const float v = acc + b_out[my_a];
       const float xn = x[(size_t)row * A + my_a] + (1.0f / (float)q.K) * v;
       x[(size_t)row * A + my_a] = xn;
-      if (step == q.K - 1) q.actions[(size_t)(first_row + row - q.tok_off) * A + my_a] = xn;
+      if (step == q.S - 1) q.actions[(size_t)(first_row + row - q.tok_off) * A + my_a] = xn;
     }
   }
 }
@@ -257,7 +259,7 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
 
 // ------------------------------------------------------------------ output projection + Euler (bf16)
 // v = u W_out + b_out on the final-normalized rows u (bf16, from modnorm), then
-// x += v / K and, on the request's last step, x is written to its actions.
+// x += v / K and, on the request's last step of this call, x is written to its actions.
 // W_out^T (bf16 [A][d], rows past A read as zero) is staged in LDS in chunks of
 // KC columns, each row's 16-byte chunks XOR-swizzled by row % 16 so that the 32
 // rows one MFMA operand read touches fall in distinct bank groups.  Each wave
@@ -325,7 +327,7 @@ __global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restr
         const float v = acc[nb][r] + bias;
         const float xn = x[(size_t)row * A + col] + (1.0f / (float)q.K) * v;
         x[(size_t)row * A + col] = xn;
-        if (step == q.K - 1) q.actions[(size_t)(row0 + row - q.tok_off) * A + col] = xn;
+        if (step == q.S - 1) q.actions[(size_t)(row0 + row - q.tok_off) * A + col] = xn;
       }
     }
   }

@@ -48,6 +48,7 @@ uint16_t f32_to_bf16_rne(float f) {
 struct Plan {
   std::vector<int32_t> order;        // plan position -> caller index
   std::vector<int32_t> tok_off;      // by plan position
+  std::vector<int32_t> steps;        // by plan position: Euler steps this call runs
   std::vector<int32_t> m_k;          // per step
   std::vector<int32_t> n_active;     // per step
   std::vector<float> taus;
@@ -189,7 +190,8 @@ int attn_groups_per_block(const rosa_model_config *cfg) { return 4 * attn_groups
 
 // Validation of a request set (all-or-nothing) and the batch plan.
 rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
-                       int n, bool sort_by_steps, bool allow_split, int lanes_wanted, Plan &p, std::string &err) {
+                       int n, bool sort_by_steps, bool allow_split, int lanes_wanted, Plan &p, std::string &err,
+                       int max_steps_call = INT32_MAX) {
   if (n < 0) { err = "n_reqs < 0"; return ROSA_E_INVALID; }
   if (n > 0 && !reqs) { err = "reqs is NULL"; return ROSA_E_INVALID; }
   if (n > cap->max_requests) { err = "more requests than max_requests"; return ROSA_E_CAPACITY; }
@@ -197,7 +199,6 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   for (int i = 0; i < n; ++i) {
     const rosa_request &r = reqs[i];
     char buf[160];
-    if (r.reserved != 0) { snprintf(buf, sizeof buf, "request %d: reserved != 0", i); err = buf; return ROSA_E_INVALID; }
     if (r.prefix_len < 0 || r.horizon < 1 || r.num_steps < 1) {
       snprintf(buf, sizeof buf, "request %d: P=%d H=%d K=%d out of range", i, r.prefix_len, r.horizon, r.num_steps);
       err = buf; return ROSA_E_INVALID;
@@ -207,7 +208,11 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
                r.num_steps, cap->max_horizon, cap->max_steps);
       err = buf; return ROSA_E_INVALID;
     }
-    if (!r.noise || !r.actions || (r.prefix_len > 0 && (!r.prefix_k || !r.prefix_v))) {
+    if (r.start_step < 0 || r.start_step >= r.num_steps) {
+      snprintf(buf, sizeof buf, "request %d: start_step=%d outside [0, K=%d)", i, r.start_step, r.num_steps);
+      err = buf; return ROSA_E_INVALID;
+    }
+    if ((r.start_step == 0 && !r.noise) || !r.actions || (r.prefix_len > 0 && (!r.prefix_k || !r.prefix_v))) {
       snprintf(buf, sizeof buf, "request %d: NULL pointer", i); err = buf; return ROSA_E_INVALID;
     }
     sumH += r.horizon;
@@ -216,7 +221,11 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   if (sumH > cap->max_action_tokens) { err = "sum of horizons above max_action_tokens"; return ROSA_E_CAPACITY; }
   if (sumP > cap->max_prefix_tokens) { err = "sum of prefix lengths above max_prefix_tokens"; return ROSA_E_CAPACITY; }
 
+  if (max_steps_call < 1) { err = "max_steps < 1"; return ROSA_E_INVALID; }
   p = Plan();
+  // Euler steps each request runs in this call (by caller index).
+  std::vector<int> nsteps(n);
+  for (int i = 0; i < n; ++i) nsteps[i] = std::min(reqs[i].num_steps - reqs[i].start_step, max_steps_call);
   // Lanes: requests dealt longest-first to the lane with the least estimated
   // work (token-steps weighted by the attention's key count), then each lane
   // sorted by step count, descending (stable).
@@ -227,7 +236,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
     for (int i = 0; i < n; ++i) byw[i] = i;
     auto work = [&](int i) {
       const rosa_request &r = reqs[i];
-      return (double)r.horizon * r.num_steps * (1.0 + (double)(r.prefix_len + r.horizon) / 1800.0);
+      return (double)r.horizon * nsteps[i] * (1.0 + (double)(r.prefix_len + r.horizon) / 1800.0);
     };
     std::stable_sort(byw.begin(), byw.end(), [&](int a, int b2) { return work(a) > work(b2); });
     std::vector<double> load(n_lanes, 0.0);
@@ -247,33 +256,40 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
       if (lane_of[i] == l) p.order.push_back(i);
     if (sort_by_steps)
       std::stable_sort(p.order.begin() + lo, p.order.end(),
-                       [&](int a, int b2) { return reqs[a].num_steps > reqs[b2].num_steps; });
+                       [&](int a, int b2) { return nsteps[a] > nsteps[b2]; });
     p.lanes[l].req_lo = (int)lo;
     p.lanes[l].req_hi = (int)p.order.size();
   }
   p.tok_off.resize(n);
   int M = 0;
-  for (int i = 0; i < n; ++i) { p.tok_off[i] = M; M += reqs[p.order[i]].horizon; p.Kmax = std::max(p.Kmax, reqs[p.order[i]].num_steps); }
+  p.steps.resize(n);
+  for (int i = 0; i < n; ++i) {
+    p.tok_off[i] = M;
+    M += reqs[p.order[i]].horizon;
+    p.steps[i] = nsteps[p.order[i]];
+    p.Kmax = std::max(p.Kmax, p.steps[i]);
+  }
   p.M0 = M;
   p.m_k.assign(p.Kmax, 0);
   p.n_active.assign(p.Kmax, 0);
   for (int i = 0; i < n; ++i)
-    for (int k = 0; k < reqs[p.order[i]].num_steps; ++k) { p.m_k[k] += reqs[p.order[i]].horizon; p.n_active[k] += 1; }
+    for (int k = 0; k < p.steps[i]; ++k) { p.m_k[k] += reqs[p.order[i]].horizon; p.n_active[k] += 1; }
   for (Plan::Lane &ln : p.lanes) {
     ln.row_lo = ln.req_lo < n ? p.tok_off[ln.req_lo] : M;
     ln.row_hi = ln.req_hi < n ? p.tok_off[ln.req_hi] : M;
     ln.n_act.assign(p.Kmax, 0);
     ln.m.assign(p.Kmax, 0);
     for (int i = ln.req_lo; i < ln.req_hi; ++i)
-      for (int k = 0; k < reqs[p.order[i]].num_steps; ++k) { ln.m[k] += reqs[p.order[i]].horizon; ln.n_act[k] += 1; }
+      for (int k = 0; k < p.steps[i]; ++k) { ln.m[k] += reqs[p.order[i]].horizon; ln.n_act[k] += 1; }
   }
 
-  // Distinct flow times tau = k / K (fp32 division) and each (step, request)'s index.
+  // Distinct flow times tau = k / K (fp32 division) of every (call step j,
+  // request) with k = start_step + j, and their indices.
   p.tau_idx.assign((size_t)p.Kmax * n, 0);
   for (int i = 0; i < n; ++i) {
-    const int K = reqs[p.order[i]].num_steps;
-    for (int k = 0; k < K; ++k) {
-      const float tau = (float)k / (float)K;
+    const int K = reqs[p.order[i]].num_steps, k0 = reqs[p.order[i]].start_step;
+    for (int k = 0; k < p.steps[i]; ++k) {
+      const float tau = (float)(k0 + k) / (float)K;
       int idx = -1;
       for (size_t j = 0; j < p.taus.size(); ++j)
         if (p.taus[j] == tau) { idx = (int)j; break; }
@@ -480,6 +496,7 @@ hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, i
     ReqDesc d{};
     d.pk = r.prefix_k; d.pv = r.prefix_v; d.noise = r.noise; d.actions = r.actions;
     d.P = r.prefix_len; d.H = r.horizon; d.K = r.num_steps; d.tok_off = p.tok_off[i]; d.orig = p.order[i];
+    d.k0 = r.start_step; d.S = p.steps[i];
     rd[i] = d;
   }
   std::memcpy(hp + b->off_tau_idx, p.tau_idx.data(), p.tau_idx.size() * 4);
@@ -717,6 +734,10 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
 }
 
 rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32_t n) {
+  return rosa_generate_steps(b, reqs, n, INT32_MAX);
+}
+
+rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t n, int32_t max_steps) {
   if (!b) return ROSA_E_INVALID;
   try {
     b->last_error.clear();
@@ -726,7 +747,7 @@ rosa_status rosa_generate_actions(rosa_batch *b, const rosa_request *reqs, int32
     // Lanes only without per-kernel profiling (its events live on one stream)
     // and with enough requests for each lane.
     const int lanes = b->prof ? 1 : std::max(1, std::min(b->lanes, n / kMinLaneRequests));
-    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, true, b->bf16, lanes, p, err);
+    rosa_status st = build_plan(&b->cfg, &b->cap, reqs, n, true, b->bf16, lanes, p, err, max_steps);
     if (st != ROSA_OK) return fail(b, st, err);
     if (n == 0) return ROSA_OK;
     hipError_t e = hipSetDevice(b->device);

@@ -13,7 +13,10 @@ struct ReqDesc {
   const float *noise;    // [H][A]
   float *actions;        // [H][A]
   int32_t P, H, K, tok_off;
-  int32_t orig, pad0, pad1, pad2;
+  int32_t orig;
+  int32_t k0;            // Euler steps done before this call (x starts from actions if > 0)
+  int32_t S;             // steps this call runs; the state goes to actions after step S-1
+  int32_t pad0;
 };
 static_assert(sizeof(ReqDesc) == 64, "ReqDesc is 64 bytes");
 

@@ -43,7 +43,7 @@ class Capacity(C.Structure):
 class Request(C.Structure):
     _fields_ = [("prefix_k", C.c_void_p), ("prefix_v", C.c_void_p), ("noise", C.c_void_p),
                 ("actions", C.c_void_p), ("prefix_len", C.c_int32), ("horizon", C.c_int32),
-                ("num_steps", C.c_int32), ("reserved", C.c_int32)]
+                ("num_steps", C.c_int32), ("start_step", C.c_int32)]
 
 
 class S1Outcome(C.Structure):
@@ -80,6 +80,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_batch_create.restype = C.c_int
     lib.rosa_generate_actions.argtypes = [vp, C.POINTER(Request), i32]
     lib.rosa_generate_actions.restype = C.c_int
+    lib.rosa_generate_steps.argtypes = [vp, C.POINTER(Request), i32, i32]
+    lib.rosa_generate_steps.restype = C.c_int
     lib.rosa_destroy.argtypes = [vp]
     lib.rosa_destroy.restype = None
     lib.rosa_status_string.argtypes = [C.c_int]
@@ -128,13 +130,13 @@ def _f32_ptr(a: np.ndarray):
     return a.ctypes.data_as(C.POINTER(C.c_float))
 
 
-def request_struct(prefix_k, prefix_v, noise, actions, P: int, H: int, K: int, reserved: int = 0) -> Request:
+def request_struct(prefix_k, prefix_v, noise, actions, P: int, H: int, K: int, start_step: int = 0) -> Request:
     """Build a request from torch device tensors (or raw integer device pointers)."""
     def ptr(t):
         if t is None:
             return None
         return t if isinstance(t, int) else t.data_ptr()
-    return Request(ptr(prefix_k), ptr(prefix_v), ptr(noise), ptr(actions), P, H, K, reserved)
+    return Request(ptr(prefix_k), ptr(prefix_v), ptr(noise), ptr(actions), P, H, K, start_step)
 
 
 def request_array(reqs: Sequence[Request]):
@@ -214,6 +216,14 @@ class ActionExpert:
         """Enqueue rosa_generate_actions; returns the status (raises on error)."""
         arr = request_array(reqs)
         st = self.lib.rosa_generate_actions(self.handle, arr, len(reqs))
+        self._check(st)
+        return st
+
+    def generate_steps(self, reqs: Sequence[Request], max_steps: int) -> int:
+        """Enqueue rosa_generate_steps (each request runs at most max_steps of
+        its remaining Euler steps from its start_step); raises on error."""
+        arr = request_array(reqs)
+        st = self.lib.rosa_generate_steps(self.handle, arr, len(reqs), max_steps)
         self._check(st)
         return st
 

@@ -13,8 +13,8 @@ from tests.helpers import declared_functions
 FAKE = 0x1000   # non-NULL device address; host planning never dereferences it
 
 
-def req(P, H, K, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, reserved=0):
-    return rosa.request_struct(k, v, noise, out, P, H, K, reserved)
+def req(P, H, K, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, start_step=0):
+    return rosa.request_struct(k, v, noise, out, P, H, K, start_step)
 
 
 def test_library_exports_every_declared_function():
@@ -95,15 +95,25 @@ def test_plan_no_split_for_a_full_batch():
     (dict(noise=None), rosa.ROSA_E_INVALID),
     (dict(out=None), rosa.ROSA_E_INVALID),
     (dict(k=None), rosa.ROSA_E_INVALID),
-    (dict(reserved=1), rosa.ROSA_E_INVALID),
+    (dict(start_step=5), rosa.ROSA_E_INVALID),
+    (dict(start_step=-1), rosa.ROSA_E_INVALID),
 ])
 def test_plan_validation_all_or_nothing(bad, status):
-    args = dict(P=10, H=16, K=5, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, reserved=0)
+    args = dict(P=10, H=16, K=5, k=FAKE, v=FAKE, noise=FAKE, out=FAKE, start_step=0)
     args.update(bad)
     good = req(5, 8, 5)
-    bad_req = req(args["P"], args["H"], args["K"], args["k"], args["v"], args["noise"], args["out"], args["reserved"])
+    bad_req = req(args["P"], args["H"], args["K"], args["k"], args["v"], args["noise"], args["out"], args["start_step"])
     st, *_ = _plan([good, bad_req, good])
     assert st == status
+
+
+def test_plan_resumed_request_needs_no_noise():
+    # a request resumed at step 2 of 5 reads its state from actions and runs
+    # its remaining 3 steps; the fresh one runs all 4 and comes first
+    st, order, tok, m_k, counts = _plan([req(10, 16, 5, noise=None, start_step=2), req(5, 8, 4)])
+    assert st == rosa.ROSA_OK
+    assert order == [1, 0]
+    assert m_k[:5] == [24, 24, 24, 8, 0]
 
 
 def test_plan_null_prefix_allowed_when_empty():

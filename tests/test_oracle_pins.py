@@ -181,6 +181,34 @@ def test_constant_velocity_other_steps(K):
     np.testing.assert_allclose(x, req.noise.astype(np.float64) + c, rtol=0, atol=1e-14)
 
 
+def test_advance_constant_velocity_partial_steps():
+    # steps k0 .. k1-1 of K under v = c add c (k1 - k0) / K
+    w = _zero_weights(TINY_SHAPE)
+    rng = np.random.default_rng(21)
+    c = (np.round(rng.uniform(-2, 2, size=TINY_SHAPE.action_dim) * 16) / 16).astype(np.float32)
+    w["b_out"] = c
+    om = OracleModel(w, TINY_SHAPE)
+    req = custom_request(TINY_SHAPE, "fp32", 6, 3, 8, seed=22)
+    x0 = _grid_noise(rng, 3, TINY_SHAPE.action_dim).astype(np.float64)
+    pk, pv = req.prefix_f32("k"), req.prefix_f32("v")
+    for k0, k1 in [(0, 3), (3, 8), (5, 6)]:
+        np.testing.assert_array_equal(om.advance(x0, 8, k0, k1, pk, pv), x0 + c * (k1 - k0) / 8.0)
+
+
+def test_advance_in_pieces_equals_one_shot():
+    # regrouping the Euler steps (as step-level batching does) reproduces the
+    # whole chunk exactly: each piece keeps its own flow times k / K
+    w = make_weights(TINY_SHAPE, "fp32", seed=3)
+    om = OracleModel(w, TINY_SHAPE)
+    req = custom_request(TINY_SHAPE, "fp32", 20, 4, 5, seed=23)
+    pk, pv = req.prefix_f32("k"), req.prefix_f32("v")
+    whole = om.generate_chunk(req.noise, 5, pk, pv)
+    x = req.noise.astype(np.float64)
+    for k0, k1 in [(0, 2), (2, 3), (3, 5)]:
+        x = om.advance(x, 5, k0, k1, pk, pv)
+    np.testing.assert_array_equal(x, whole)
+
+
 def test_zero_velocity_keeps_noise():
     w = make_weights(TINY_SHAPE, "fp32", seed=0)
     w["w_out"][:] = 0.0
