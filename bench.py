@@ -270,6 +270,98 @@ def batch_profile(torch, rosa, expert, db, reqs, preset, args):
                                       "requests wait; batch latency = measured p50"}), flush=True)
 
 
+def step_batching(torch, rosa, expert, db, reqs, preset, args, n_req=1024, seed=0):
+    """One worker serving requests that arrive at exponential intervals (the
+    workload's request mix, cycling over its resident prefixes).  The clock is
+    virtual: it advances by each call's measured duration (HIP events), so
+    every call runs on the GPU and queueing follows from the measurements.
+      whole: when idle, the worker takes every waiting request (up to the
+        handle's capacity) and runs their whole chunks (rosa_generate_actions);
+      step: every call advances all requests in flight by one Euler step
+        (rosa_generate_steps); arrivals join, finished requests leave, between
+        calls.
+    Latency = completion - arrival."""
+    rng = np.random.default_rng(seed)
+    arrive = np.cumsum(rng.exponential(1000.0 / args.arrival_rate, n_req))     # ms
+    src = [i % len(reqs) for i in range(n_req)]
+    outs = [torch.empty_like(db.noise[j]) for j in src]
+    cap_n = len(reqs)
+    cap_tok = sum(r.horizon for r in reqs)
+    stream = torch.cuda.current_stream()
+
+    def struct(i, done):
+        j = src[i]
+        r = reqs[j]
+        return rosa.request_struct(db.k[j], db.v[j], db.noise[j] if done == 0 else None, outs[i],
+                                   r.prefix_len, r.horizon, r.steps, done)
+
+    def timed_call(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1)
+
+    def run(mode):
+        t, nxt = 0.0, 0
+        waiting, flight, done_steps = [], [], {}
+        finish = np.zeros(n_req)
+        calls, sizes = 0, []
+        while nxt < n_req or waiting or flight:
+            while nxt < n_req and arrive[nxt] <= t:
+                waiting.append(nxt)
+                nxt += 1
+            if mode == "whole":
+                if not waiting:
+                    t = arrive[nxt]
+                    continue
+                batch, tok = [], 0
+                while waiting and len(batch) < cap_n and tok + reqs[src[waiting[0]]].horizon <= cap_tok:
+                    tok += reqs[src[waiting[0]]].horizon
+                    batch.append(waiting.pop(0))
+                t += timed_call(lambda: expert.generate([struct(i, 0) for i in batch]))
+                finish[batch] = t
+                sizes.append(len(batch))
+            else:
+                tok = sum(reqs[src[i]].horizon for i in flight)
+                while waiting and len(flight) < cap_n and tok + reqs[src[waiting[0]]].horizon <= cap_tok:
+                    tok += reqs[src[waiting[0]]].horizon
+                    i = waiting.pop(0)
+                    done_steps[i] = 0
+                    flight.append(i)
+                if not flight:
+                    t = arrive[nxt]
+                    continue
+                t += timed_call(lambda: expert.generate_steps([struct(i, done_steps[i]) for i in flight], 1))
+                sizes.append(len(flight))
+                keep = []
+                for i in flight:
+                    done_steps[i] += 1
+                    if done_steps[i] == reqs[src[i]].steps:
+                        finish[i] = t
+                    else:
+                        keep.append(i)
+                flight = keep
+            calls += 1
+        lat = finish - arrive
+        return {"chunks_per_s": round(n_req / ((finish.max() - arrive[0]) * 1e-3), 1),
+                "latency_mean_ms": round(float(lat.mean()), 2),
+                "latency_p50_ms": round(float(np.percentile(lat, 50)), 2),
+                "latency_p99_ms": round(float(np.percentile(lat, 99)), 2),
+                "calls": calls, "mean_requests_per_call": round(float(np.mean(sizes)), 1)}
+
+    for _ in range(2):                         # warm-up of both paths
+        expert.generate([struct(0, 0)])
+        expert.generate_steps([struct(0, 0)], 1)
+    torch.cuda.synchronize()
+    res = {m: run(m) for m in ["whole", "step"]}
+    print(json.dumps({"kind": "step_batching", "workload": preset.name, "requests": n_req,
+                      "arrival_rate_per_s": args.arrival_rate, "whole_chunk_batches": res["whole"],
+                      "step_level_batches": res["step"],
+                      "clock": "virtual: advanced by each call's measured duration"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -285,6 +377,10 @@ def main():
                     help="System-1 batch-size profile: latency and throughput of one call on the first B "
                          "requests of the workload for B = 1, 2, 4, ..., then the batch size the library "
                          "chooses for a few robot fleets (prints its own JSON line)")
+    ap.add_argument("--step-batching", action="store_true",
+                    help="open-loop request arrivals served by one worker with whole-chunk batches vs "
+                         "step-level batches (rosa_generate_steps); prints its own JSON line")
+    ap.add_argument("--arrival-rate", type=float, default=2000.0, help="requests per second for --step-batching")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="write the profiles/ summaries from rocprofv3 outputs under DIR and exit (no GPU)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -324,6 +420,10 @@ def main():
     stream = torch.cuda.current_stream()
     if args.batch_profile:
         batch_profile(torch, rosa, expert, db, reqs, preset, args)
+        expert.close()
+        return
+    if args.step_batching:
+        step_batching(torch, rosa, expert, db, reqs, preset, args)
         expert.close()
         return
     for _ in range(args.warmup):
