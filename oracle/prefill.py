@@ -1,0 +1,57 @@
+"""CPU oracle for the prefix producer (test infrastructure only).
+
+The paper's System-1 models run a vision-language backbone over each robot's
+observation and instruction, and its cached prefix feeds the action head
+(Sec. 2.2.1: a VLM backbone followed by an action-generation head such as a
+diffusion transformer).  The action expert reads, at layer l, the keys and
+values the backbone's layer l produced for the prefix tokens.  The paper does
+not write out the backbone; the reading taken here (each step restated where
+it is used):
+
+* input: the prefix tokens already embedded (image patches and text), [P][d];
+* each layer: RMSNorm (eps 1e-6, no learned gain), fused QKV projection,
+  attention of every prefix token over all prefix tokens of its own request
+  (bidirectional, no positions), output projection and residual; RMSNorm, a
+  plain two-matrix tanh-GELU MLP and residual; no biases;
+* the layer's cache: its K and V projections of the prefix tokens,
+  [L][P][n_kv][hd].
+
+Plain NumPy float64, one request at a time, one layer at a time; matrix
+products and the pinned attention, RMSNorm and GELU of ``rosa_oracle`` are
+its only steps.
+
+Pins (tests marked ``not gpu``): a scalar brute force on nested lists for a
+tiny backbone; with the residual branches zeroed every layer's cache is the
+closed form RMSNorm(x) W_k, W_v of that layer; permuting the prefix tokens
+permutes the cache rows (no causal mask, no positions).
+"""
+from __future__ import annotations
+
+from typing import Dict, Tuple
+
+import numpy as np
+
+from .rosa_oracle import attention, gelu_tanh, rms_norm
+
+F = np.float64
+
+
+def prefill(x: np.ndarray, w: Dict[str, np.ndarray], shape) -> Tuple[np.ndarray, np.ndarray]:
+    """Prefix caches (K, V), each [L][P][n_kv][hd] float64, of one request whose
+    embedded prefix tokens are x [P][d]."""
+    L, nq, nkv, hd, eps = shape.n_layers, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.rms_eps
+    P = x.shape[0]
+    h = np.asarray(x, dtype=F).copy()
+    K = np.zeros((L, P, nkv, hd), dtype=F)
+    V = np.zeros((L, P, nkv, hd), dtype=F)
+    for l in range(L):
+        qkv = rms_norm(h, eps) @ np.asarray(w["w_qkv"][l], dtype=F)
+        q = qkv[:, :nq * hd].reshape(P, nq, hd)
+        k = qkv[:, nq * hd:(nq + nkv) * hd].reshape(P, nkv, hd)
+        v = qkv[:, (nq + nkv) * hd:].reshape(P, nkv, hd)
+        K[l], V[l] = k, v
+        o = attention(q, k, v) if P > 0 else np.zeros((0, nq, hd), dtype=F)
+        h = h + o.reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
+        u = rms_norm(h, eps)
+        h = h + gelu_tanh(u @ np.asarray(w["w_up"][l], dtype=F)) @ np.asarray(w["w_down"][l], dtype=F)
+    return K, V

@@ -39,7 +39,8 @@ __all__ = [
     "ModelShape", "Preset", "RequestData", "PRESETS", "WEIGHT_ORDER",
     "TINY_SHAPE", "PI0_SHAPE", "bf16_round", "bf16_bits", "bits_to_f32",
     "make_weights", "make_metadata", "make_request", "make_requests",
-    "weight_shapes",
+    "weight_shapes", "VlmShape", "TINY_VLM", "PI0_VLM", "VLM_WEIGHT_ORDER", "vlm_weight_shapes",
+    "make_vlm_weights", "make_prefix_embeddings",
 ]
 
 
@@ -240,3 +241,59 @@ def custom_request(shape: ModelShape, dtype: str, prefix_len: int, horizon: int,
     """A request outside any preset (test edge cases: P = 0, H = 1, ...)."""
     return _draw_request(shape, dtype, RequestMeta(prefix_len, horizon, steps),
                          np.random.SeedSequence(seed))
+
+
+# ---------------------------------------------------------------- vision-language prefix producer
+
+@dataclasses.dataclass(frozen=True)
+class VlmShape:
+    """A VLM backbone whose per-layer keys and values are the action expert's
+    prefix cache: same layer count, KV heads and head width as the expert."""
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_mlp: int
+    rms_eps: float = 1e-6
+
+    @property
+    def qkv_dim(self) -> int:
+        return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim
+
+
+# Pairs with TINY_SHAPE (2 layers, 1 KV head of 32) and PI0_SHAPE (18 layers,
+# 1 KV head of 256; a PaliGemma-sized backbone: width 2048, 8 heads, MLP 16384).
+TINY_VLM = VlmShape(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=1, head_dim=32, d_mlp=1024)
+PI0_VLM = VlmShape(n_layers=18, d_model=2048, n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384)
+
+VLM_WEIGHT_ORDER = ["w_qkv", "w_o", "w_up", "w_down"]
+
+
+def vlm_weight_shapes(s: VlmShape) -> Dict[str, tuple]:
+    """Host weight shapes of the backbone, row-major [in][out] (y = x @ W)."""
+    L, d = s.n_layers, s.d_model
+    return {"w_qkv": (L, d, s.qkv_dim), "w_o": (L, s.n_q_heads * s.head_dim, d),
+            "w_up": (L, d, s.d_mlp), "w_down": (L, s.d_mlp, d)}
+
+
+def make_vlm_weights(shape: VlmShape, dtype: str = "bf16", seed: int = 1, std: float = 0.02
+                     ) -> Dict[str, np.ndarray]:
+    """Backbone weights N(0, std^2), drawn in VLM_WEIGHT_ORDER from the
+    weights child of SeedSequence(seed); bf16-representable in bf16 mode."""
+    wss, _, _ = _children(seed, 0)
+    rng = np.random.Generator(np.random.PCG64(wss))
+    out = {}
+    for name in VLM_WEIGHT_ORDER:
+        w = rng.standard_normal(vlm_weight_shapes(shape)[name], dtype=np.float32)
+        w *= np.float32(std)
+        out[name] = bf16_round(w) if dtype == "bf16" else w
+    return out
+
+
+def make_prefix_embeddings(shape: VlmShape, prefix_len: int, dtype: str, seed: int) -> np.ndarray:
+    """Input embeddings of one request's prefix tokens (image patches and text,
+    already embedded), [P][d] N(0, 1), bf16-representable float32 in bf16 mode."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
+    x = rng.standard_normal((prefix_len, shape.d_model), dtype=np.float32)
+    return bf16_round(x) if dtype == "bf16" else x

@@ -1,0 +1,87 @@
+"""Pins of the prefix-producer oracle (Sec. 2.2.1: the VLM backbone's per-layer
+keys and values are the action head's prefix cache).  No GPU needed."""
+import math
+
+import numpy as np
+
+from oracle import prefill
+from synthetic import TINY_VLM, VlmShape, make_prefix_embeddings, make_vlm_weights
+
+SMALL = VlmShape(n_layers=2, d_model=8, n_q_heads=4, n_kv_heads=2, head_dim=4, d_mlp=12)
+
+
+def _brute_prefill(x, w, s):
+    """Scalar brute force on nested Python lists."""
+    L, d, nq, nkv, hd, dff = s.n_layers, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_mlp
+    G = nq // nkv
+    P = len(x)
+    h = [[float(v) for v in row] for row in x]
+
+    def norm(row):
+        ms = sum(v * v for v in row) / len(row)
+        return [v / math.sqrt(ms + s.rms_eps) for v in row]
+
+    def matvec(row, W):
+        return [sum(row[i] * float(W[i][j]) for i in range(len(row))) for j in range(len(W[0]))]
+
+    Ks, Vs = [], []
+    for l in range(L):
+        qkv = [matvec(norm(row), w["w_qkv"][l]) for row in h]
+        q = [[r[g * hd:(g + 1) * hd] for g in range(nq)] for r in qkv]
+        k = [[r[(nq + j) * hd:(nq + j + 1) * hd] for j in range(nkv)] for r in qkv]
+        v = [[r[(nq + nkv + j) * hd:(nq + nkv + j + 1) * hd] for j in range(nkv)] for r in qkv]
+        Ks.append(k)
+        Vs.append(v)
+        o = []
+        for t in range(P):
+            row = []
+            for g in range(nq):
+                j = g // G
+                sc = [sum(q[t][g][e] * k[u][j][e] for e in range(hd)) / math.sqrt(hd) for u in range(P)]
+                m = max(sc)
+                ex = [math.exp(z - m) for z in sc]
+                tot = sum(ex)
+                row += [sum(ex[u] * v[u][j][e] for u in range(P)) / tot for e in range(hd)]
+            o.append(row)
+        h = [[a + b for a, b in zip(hr, matvec(orow, w["w_o"][l]))] for hr, orow in zip(h, o)]
+        new = []
+        for hr in h:
+            up = matvec(norm(hr), w["w_up"][l])
+            gl = [0.5 * z * (1.0 + math.tanh(math.sqrt(2.0 / math.pi) * (z + 0.044715 * z ** 3))) for z in up]
+            new.append([a + b for a, b in zip(hr, matvec(gl, w["w_down"][l]))])
+        h = new
+    return np.array(Ks), np.array(Vs)
+
+
+def test_prefill_matches_scalar_bruteforce():
+    rng = np.random.default_rng(0)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL, "fp32").items()}
+    x = rng.standard_normal((5, SMALL.d_model))
+    K, V = prefill(x, w, SMALL)
+    Kb, Vb = _brute_prefill(x, w, SMALL)
+    np.testing.assert_allclose(K, Kb, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(V, Vb, rtol=0, atol=1e-11)
+
+
+def test_zero_residual_branches_give_per_layer_closed_form():
+    w = make_vlm_weights(TINY_VLM, "fp32", seed=4)
+    w["w_o"][:] = 0.0
+    w["w_down"][:] = 0.0
+    x = make_prefix_embeddings(TINY_VLM, 9, "fp32", seed=5).astype(np.float64)
+    K, V = prefill(x, w, TINY_VLM)
+    nq, nkv, hd = TINY_VLM.n_q_heads, TINY_VLM.n_kv_heads, TINY_VLM.head_dim
+    u = x / np.sqrt((x * x).mean(axis=1, keepdims=True) + TINY_VLM.rms_eps)
+    for l in range(TINY_VLM.n_layers):
+        qkv = u @ w["w_qkv"][l].astype(np.float64)
+        np.testing.assert_allclose(K[l], qkv[:, nq * hd:(nq + nkv) * hd].reshape(9, nkv, hd), rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(V[l], qkv[:, (nq + nkv) * hd:].reshape(9, nkv, hd), rtol=1e-12, atol=1e-13)
+
+
+def test_token_permutation_permutes_the_cache():
+    w = make_vlm_weights(TINY_VLM, "fp32", seed=6)
+    x = make_prefix_embeddings(TINY_VLM, 12, "fp32", seed=7).astype(np.float64)
+    perm = np.random.default_rng(8).permutation(12)
+    K, V = prefill(x, w, TINY_VLM)
+    Kp, Vp = prefill(x[perm], w, TINY_VLM)
+    np.testing.assert_allclose(Kp, K[:, perm], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Vp, V[:, perm], rtol=1e-12, atol=1e-13)
