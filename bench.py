@@ -362,6 +362,134 @@ def step_batching(torch, rosa, expert, db, reqs, preset, args, n_req=1024, seed=
                       "clock": "virtual: advanced by each call's measured duration"}), flush=True)
 
 
+def prefill_work(shape, lens):
+    """Algorithmic flops of one prefix-producer call by kernel class.  Every
+    layer's QKV projection; the attention, output projection and MLP of all
+    layers but the last (its caches need only its K and V).  Attention:
+    4 * n_q * hd * P^2 per job and layer (QK^T and PV)."""
+    L, d, nq, hd, dff = shape.n_layers, shape.d_model, shape.n_q_heads, shape.head_dim, shape.d_mlp
+    M = float(sum(lens))
+    return {
+        "gemm_qkv": 2.0 * M * d * shape.qkv_dim * L,
+        "gemm_o": 2.0 * M * nq * hd * d * (L - 1),
+        "gemm_up": 2.0 * M * d * dff * (L - 1),
+        "gemm_down": 2.0 * M * dff * d * (L - 1),
+        "attention": 4.0 * nq * hd * sum(float(P) * P for P in lens) * (L - 1),
+    }
+
+
+def prefill_cpu_baseline(shape, weights, x, lens, budget_layers: int = 2):
+    """The oracle backbone on a bounded sample: the first `budget_layers`
+    layers of the shortest job, scaled to the whole batch and all layers by
+    algorithmic flops."""
+    import dataclasses
+    from oracle import prefill
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    sub = dataclasses.replace(shape, n_layers=budget_layers)
+    w = {k: v[:budget_layers] for k, v in weights.items()}
+    t0 = time.perf_counter()
+    prefill(x, w, sub)
+    t = time.perf_counter() - t0
+    # the oracle runs every layer in full: 2 * (qkv + o + up + down) per token and layer, plus attention
+    per_tok = 2.0 * (shape.d_model * shape.qkv_dim + shape.n_q_heads * shape.head_dim * shape.d_model
+                     + 2 * shape.d_model * shape.d_mlp)
+    att = lambda P: 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P
+    f_sample = budget_layers * (per_tok * x.shape[0] + att(x.shape[0]))
+    f_total = shape.n_layers * sum(per_tok * P + att(P) for P in lens)
+    batch_s = t * f_total / f_sample
+    return {"value": sum(lens) / batch_s, "unit": "prefix tokens/s", "cores": int(blas_threads),
+            "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
+            "sample": (f"first {budget_layers} of {shape.n_layers} layers of one {x.shape[0]}-token job, "
+                       f"{t:.1f} s measured, scaled to {len(lens)} jobs x {shape.n_layers} layers by "
+                       f"algorithmic flops (extrapolated batch time {batch_s:.1f} s); NumPy float64")}
+
+
+def prefill_bench(torch, rosa, args):
+    """The prefix producer (a PaliGemma-sized VLM backbone, bf16) over one
+    batch of robots' embedded prefixes; value = prefix tokens/s."""
+    from synthetic import PI0_VLM, make_prefix_embeddings, make_vlm_weights, prefill_lengths
+    shape = PI0_VLM
+    lens = prefill_lengths()
+    t0 = time.time()
+    weights = make_vlm_weights(shape, "bf16")
+    xs = [make_prefix_embeddings(shape, P, "bf16", 4000 + i) for i, P in enumerate(lens)]
+    print(f"[bench] generated backbone weights and {len(lens)} prefixes in {time.time() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+    emb = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in xs]
+    kc = [torch.empty((shape.n_layers, P, shape.n_kv_heads, shape.head_dim), dtype=torch.bfloat16,
+                      device="cuda") for P in lens]
+    vc = [torch.empty_like(k) for k in kc]
+    jobs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(emb, kc, vc, lens)]
+    pp = rosa.PrefixProducer(shape, "bf16", weights, len(lens), sum(lens))
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        pp.run(jobs)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = time.perf_counter()
+    for a, b in evs:
+        a.record(stream)
+        pp.run(jobs)
+        b.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    lat = np.array([a.elapsed_time(b) for a, b in evs])
+    print(f"[bench] timed {args.steps} prefill calls: {elapsed:.3f} s", file=sys.stderr, flush=True)
+
+    pp.set_profiling(True)
+    n_prof = 2
+    for _ in range(n_prof):
+        pp.run(jobs)
+    prof = pp.profile()
+    pp.set_profiling(False)
+    work = prefill_work(shape, lens)
+    kernels = {}
+    for name, (launches, ms) in prof.items():
+        if launches == 0:
+            continue
+        per_call = launches / n_prof
+        avg_ms = ms / launches
+        entry = {"launches_per_call": per_call, "avg_launch_ms": avg_ms, "ms_per_call": ms / n_prof}
+        if name in work:
+            ach = work[name] / per_call / (avg_ms * 1e-3) / 1e12
+            entry.update({"bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                          "frac": ach / MFMA_BF16_PEAK_TFS})
+        kernels[name] = entry
+    dom = max((k for k in kernels if "bound" in kernels[k]), key=lambda k: kernels[k]["ms_per_call"])
+    d = kernels[dom]
+    total_flops = sum(work.values())
+    ms_per_step = elapsed / args.steps * 1e3
+    out = {
+        "metric": "prefix tokens/s of the VLM prefix producer (per-layer K/V caches for the action expert)",
+        "value": round(sum(lens) * args.steps / elapsed, 1),
+        "unit": "prefix tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "vlm_prefill_b32", "jobs": len(lens), "prefix_tokens": int(sum(lens)),
+                   "backbone": "18 layers, width 2048, 8 query heads / 1 KV head of 256, MLP 16384"},
+        "jobs_per_s": round(len(lens) * args.steps / elapsed, 2),
+        "p50_ms": round(float(np.percentile(lat, 50)), 3),
+        "p99_ms": round(float(np.percentile(lat, 99)), 3),
+        "roofline": {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 2), "peak": d["peak"],
+                     "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None},
+        "all_mfma": {"achieved": round(total_flops / (ms_per_step * 1e-3) / 1e12, 1), "peak": MFMA_BF16_PEAK_TFS,
+                     "unit": "TFLOP/s", "frac": round(total_flops / (ms_per_step * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
+        "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                    for k, v in kernels.items()},
+    }
+    pp.close()
+    if not args.no_cpu_baseline:
+        i = int(np.argmin(lens))
+        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs[i], lens)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -381,6 +509,9 @@ def main():
                     help="open-loop request arrivals served by one worker with whole-chunk batches vs "
                          "step-level batches (rosa_generate_steps); prints its own JSON line")
     ap.add_argument("--arrival-rate", type=float, default=2000.0, help="requests per second for --step-batching")
+    ap.add_argument("--prefill", action="store_true",
+                    help="the prefix producer instead: a VLM backbone over 32 robots' prefixes "
+                         "(prints its own JSON line)")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="write the profiles/ summaries from rocprofv3 outputs under DIR and exit (no GPU)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -399,6 +530,9 @@ def main():
         copy_probe(torch)
         return
     from paper_2607_01088_amd import rosa
+    if args.prefill:
+        prefill_bench(torch, rosa, args)
+        return
     from synthetic import PRESETS, make_metadata, make_requests, make_weights
 
     preset = PRESETS[args.workload]

@@ -7,6 +7,7 @@
 #define ROSA_DEBUG_H_
 
 #include "rosa.h"
+#include "rosa_prefill.h"
 
 #ifdef __cplusplus
 extern "C" {
@@ -77,6 +78,13 @@ rosa_status rosa_debug_set_lanes(rosa_batch *b, int32_t n);
 rosa_status rosa_debug_set_profiling(rosa_batch *b, int32_t enable);
 rosa_status rosa_debug_get_profile(rosa_batch *b, const char **names, int64_t *launches,
                                    double *total_ms, int32_t max, int32_t *n_out);
+
+/* The same per-kernel timing for a prefix producer handle (rosa_prefill.h):
+ * classes load, norm, gemm_qkv, kv_scatter, attention, attn_merge, gemm_o,
+ * gemm_up, gemm_down. */
+rosa_status rosa_debug_prefill_set_profiling(rosa_prefill *h, int32_t enable);
+rosa_status rosa_debug_prefill_get_profile(rosa_prefill *h, const char **names, int64_t *launches,
+                                           double *total_ms, int32_t max, int32_t *n_out);
 
 #ifdef __cplusplus
 }

@@ -14,7 +14,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librosa.so")
-SOURCES = ["k_time.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "rosa_api.cpp", "rosa_sched.cpp"]
+SOURCES = ["k_time.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_prefill.hip", "rosa_api.cpp",
+           "rosa_prefill.cpp", "rosa_sched.cpp"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-result",
          # packed fp32 VALU ops stay disabled (compiler-formed v_pk_* fp32 ops)

@@ -16,16 +16,87 @@
 
 using namespace rosa;
 
+// Attention launch order.  Blocks reach the 8 XCDs round-robin (block b on
+// XCD b % 8) and each XCD starts its blocks in order as CUs free up, so:
+// requests (each a contiguous range of items) go whole to an XCD (their query
+// blocks share its L2), longest first to the least-loaded XCD, and each XCD's
+// items run longest first.  Item cost = 32-key steps + a fixed overhead.
+// Appends the block -> item table (block b = x + 8 q runs XCD x's q-th item,
+// -1: the block exits) and returns the block count.  The order never changes
+// what an item computes.
+namespace rosa {
+int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std::pair<int, int>> &ranges,
+                      std::vector<int32_t> &out) {
+  constexpr int kItemOverheadSteps = 12;   // measured fixed cost of an item, in 32-key steps
+  auto icost = [&](int it) -> int64_t { return (items[it].kend - items[it].kbeg + 31) / 32 + kItemOverheadSteps; };
+  struct RC { int lo, hi; int64_t cost; };
+  std::vector<RC> rc;
+  for (const auto &r : ranges) {
+    int64_t c = 0;
+    for (int j = r.first; j < r.second; ++j) c += icost(j);
+    rc.push_back({r.first, r.second, c});
+  }
+  std::stable_sort(rc.begin(), rc.end(), [](const RC &a, const RC &b2) { return a.cost > b2.cost; });
+  int64_t xload[8] = {};
+  std::vector<std::vector<int>> xitems(8);
+  for (const RC &r : rc) {
+    int best = 0;
+    for (int x = 1; x < 8; ++x)
+      if (xload[x] < xload[best]) best = x;
+    xload[best] += r.cost;
+    for (int it = r.lo; it < r.hi; ++it) xitems[best].push_back(it);
+  }
+  size_t most = 0;
+  for (int x = 0; x < 8; ++x) {
+    std::stable_sort(xitems[x].begin(), xitems[x].end(), [&](int a, int b2) { return icost(a) > icost(b2); });
+    most = std::max(most, xitems[x].size());
+  }
+  const size_t at = out.size();
+  out.resize(at + 8 * most, -1);
+  for (int x = 0; x < 8; ++x)
+    for (size_t q = 0; q < xitems[x].size(); ++q) out[at + x + 8 * q] = xitems[x][q];
+  return (int)(8 * most);
+}
+
+uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16) {
+  const size_t per = (size_t)K * N;
+  std::vector<uint8_t> tmp(per * L * (bf16 ? 2 : 4));
+  auto work = [&](int l) {
+    const float *s = src + per * l;
+    for (int k0 = 0; k0 < K; k0 += 64)
+      for (int n0 = 0; n0 < N; n0 += 64)
+        for (int n = n0; n < std::min(N, n0 + 64); ++n)
+          for (int k = k0; k < std::min(K, k0 + 64); ++k) {
+            const float v = s[(size_t)k * N + n];
+            const size_t di = per * l + (size_t)n * K + k;
+            if (bf16) reinterpret_cast<uint16_t *>(tmp.data())[di] = f32_to_bf16_rne(v);
+            else reinterpret_cast<float *>(tmp.data())[di] = v;
+          }
+  };
+  std::vector<std::thread> th;
+  const int nt = std::max(1, std::min(L, 8));
+  for (int t = 0; t < nt; ++t)
+    th.emplace_back([&, t] { for (int l = t; l < L; l += nt) work(l); });
+  for (auto &x : th) x.join();
+  return hipMemcpy(dst, tmp.data(), tmp.size(), hipMemcpyHostToDevice);
+}
+}  // namespace rosa
+
 namespace {
 
-constexpr int kSplitTarget = 256;   // attention work items wanted per call before keys are split
-constexpr int kMinSplitKeys = 256;  // smallest key range worth a separate work item
-constexpr int kMaxSlots = 2 * kSplitTarget;
+constexpr int kSplitTarget = kAttnSplitTarget;
+constexpr int kMinSplitKeys = kAttnMinSplitKeys;
+constexpr int kMaxSlots = kAttnMaxSlots;
 constexpr int kMaxLanes = 4;
 constexpr int kMinLaneRequests = 64;  // a batch splits into lanes only with at least this many requests per lane
-// Fixed cost of one attention work item (query loads, first copies, output
-// write, dispatch), in units of one 32-key step; measured on MI355X.
-constexpr int kItemOverheadSteps = 12;
 
 enum KernelClass {
   kcTime = 0, kcSetup, kcInProj, kcModNorm, kcGemmQKV, kcAttention, kcMerge, kcGemmO, kcGemmUp,
@@ -36,14 +107,6 @@ const char *kClassNames[kcCount] = {"time_conditioning", "setup_rows", "in_proj"
                                     "final_euler"};
 
 thread_local std::string g_create_error;
-
-uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u;
-  std::memcpy(&u, &f, 4);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);  // quiet NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 struct Plan {
   std::vector<int32_t> order;        // plan position -> caller index
@@ -349,13 +412,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   }
   if (slots > kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
 
-  // Attention launch orders.  Blocks reach the 8 XCDs round-robin (block b
-  // on XCD b % 8) and each XCD starts its blocks in order as CUs free up, so
-  // per set of active requests of a lane: requests go whole to an XCD (their
-  // query blocks share its L2), longest first to the least-loaded XCD, and
-  // each XCD's items run longest first.  Item cost = 32-key steps + a fixed
-  // overhead.  The order never changes what an item computes.
-  auto icost = [&](int it) -> int64_t { return (p.items[it].kend - p.items[it].kbeg + 31) / 32 + kItemOverheadSteps; };
+  // Attention launch orders, one per distinct set of active requests of a lane.
   for (Plan::Lane &ln : p.lanes) {
     ln.list_at.assign(p.Kmax, -1);
     ln.list_blocks.assign(p.Kmax, 0);
@@ -365,37 +422,11 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
       if (na == 0) continue;
       if (na == prev_n) { ln.list_at[k] = ln.list_at[k - 1]; ln.list_blocks[k] = ln.list_blocks[k - 1]; continue; }
       prev_n = na;
-      struct RC { int lo, hi; int64_t cost; };
-      std::vector<RC> rc;
-      for (int i = ln.req_lo; i < ln.req_lo + na; ++i) {
-        const int lo = i > 0 ? p.items_upto[i - 1] : 0, hi = p.items_upto[i];
-        int64_t c = 0;
-        for (int j = lo; j < hi; ++j) c += icost(j);
-        rc.push_back({lo, hi, c});
-      }
-      std::stable_sort(rc.begin(), rc.end(), [](const RC &a, const RC &b2) { return a.cost > b2.cost; });
-      int64_t xload[8] = {};
-      std::vector<std::vector<int>> xitems(8);
-      for (const RC &r : rc) {
-        int best = 0;
-        for (int x = 1; x < 8; ++x)
-          if (xload[x] < xload[best]) best = x;
-        xload[best] += r.cost;
-        for (int it = r.lo; it < r.hi; ++it) xitems[best].push_back(it);
-      }
-      size_t most = 0;
-      for (int x = 0; x < 8; ++x) {
-        std::vector<int> &its = xitems[x];
-        std::stable_sort(its.begin(), its.end(), [&](int a, int b2) { return icost(a) > icost(b2); });
-        most = std::max(most, its.size());
-      }
-      // Block b = x + 8 q runs XCD x's q-th item (or exits).
-      const int at = (int)p.attn_lists.size();
-      p.attn_lists.resize(at + 8 * most, -1);
-      for (int x = 0; x < 8; ++x)
-        for (size_t q = 0; q < xitems[x].size(); ++q) p.attn_lists[at + x + 8 * q] = xitems[x][q];
-      ln.list_at[k] = at;
-      ln.list_blocks[k] = (int)(8 * most);
+      std::vector<std::pair<int, int>> ranges;
+      for (int i = ln.req_lo; i < ln.req_lo + na; ++i)
+        ranges.push_back({i > 0 ? p.items_upto[i - 1] : 0, p.items_upto[i]});
+      ln.list_at[k] = (int)p.attn_lists.size();
+      ln.list_blocks[k] = attn_launch_order(p.items, ranges, p.attn_lists);
     }
   }
   return ROSA_OK;
@@ -420,26 +451,7 @@ hipError_t upload_act(rosa_batch *b, void *dst, const float *src, size_t n) {
 
 // Upload L stacked [K][N] matrices as [L][N][K] (transposed), activation dtype.
 hipError_t upload_transposed(rosa_batch *b, void *dst, const float *src, int L, int K, int N) {
-  const size_t per = (size_t)K * N;
-  std::vector<uint8_t> tmp(per * L * b->esz);
-  auto work = [&](int l) {
-    const float *s = src + per * l;
-    for (int k0 = 0; k0 < K; k0 += 64)
-      for (int n0 = 0; n0 < N; n0 += 64)
-        for (int n = n0; n < std::min(N, n0 + 64); ++n)
-          for (int k = k0; k < std::min(K, k0 + 64); ++k) {
-            const float v = s[(size_t)k * N + n];
-            const size_t di = per * l + (size_t)n * K + k;
-            if (b->bf16) reinterpret_cast<uint16_t *>(tmp.data())[di] = f32_to_bf16_rne(v);
-            else reinterpret_cast<float *>(tmp.data())[di] = v;
-          }
-  };
-  std::vector<std::thread> th;
-  const int nt = std::max(1, std::min(L, 8));
-  for (int t = 0; t < nt; ++t)
-    th.emplace_back([&, t] { for (int l = t; l < L; l += nt) work(l); });
-  for (auto &x : th) x.join();
-  return hipMemcpy(dst, tmp.data(), tmp.size(), hipMemcpyHostToDevice);
+  return upload_weights_transposed(dst, src, L, K, N, b->bf16);
 }
 
 // Profiling helpers.

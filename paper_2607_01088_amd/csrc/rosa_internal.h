@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+#include <vector>
+
 namespace rosa {
 
 // Per-request descriptor on the device (64 bytes), in plan order (K descending).
@@ -46,6 +49,12 @@ constexpr int kAttnQB = 256;       // most query rows per attention work item (4
 // 32-row query groups per wave of the bf16 attention kernel: two where Q^T and
 // O^T of both fit the register file.  Work items hold at most 128 x this rows.
 constexpr int attn_groups_per_wave(int hd) { return hd <= 128 ? 2 : 1; }
+// Keys of a query block are split over several work items only while a
+// launch has fewer than kAttnSplitTarget items; a split item holds at least
+// kAttnMinSplitKeys keys; at most kAttnMaxSlots partial-result slots per launch.
+constexpr int kAttnSplitTarget = 256;
+constexpr int kAttnMinSplitKeys = 256;
+constexpr int kAttnMaxSlots = 2 * kAttnSplitTarget;
 constexpr int kMaxTau = 128;       // distinct flow times per call
 constexpr int kMaxSteps = 64;
 
@@ -60,6 +69,16 @@ enum Epilogue : int {
   kEpiGelu = 1,           // out = gelu_tanh(acc)           (activation dtype)
   kEpiGatedResidual = 2,  // h += gate[rowmod[m]][n] * acc  (fp32)
 };
+
+// One job of the prefix producer on the device (32 bytes): its embedded
+// tokens [P][d], its caches [L][P][n_kv][hd] (activation dtype) and its first
+// stacked row.
+struct PrefillJob {
+  const void *emb;
+  void *k, *v;
+  int32_t P, tok_off;
+};
+static_assert(sizeof(PrefillJob) == 32, "PrefillJob is 32 bytes");
 
 // ---------------------------------------------------------------- launchers
 // All return hipGetLastError() of the launch.  `bf16` selects the activation
@@ -111,6 +130,15 @@ constexpr int kGemmConfigs = 11;
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s);
 int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 
+// Prefix producer rows.  row_job[row]: the job of stacked row `row`.
+// h[row] = the job's embedding row (bf16 or fp32 in, fp32 out), d % 4 == 0.
+hipError_t launch_prefill_load(const PrefillJob *jobs, const int32_t *row_job, int64_t M, int d, bool bf16_in,
+                               float *h, hipStream_t s);
+// Layer `layer`'s K and V column blocks of the stacked QKV rows into each job's
+// caches; esz: bytes per element.
+hipError_t launch_prefill_kv_scatter(const PrefillJob *jobs, const int32_t *row_job, int64_t M, const void *qkv,
+                                     int ldqkv, int nq, int nkv, int hd, size_t esz, int layer, hipStream_t s);
+
 // Attention of one layer.
 struct AttnArgs {
   const AttnItem *items; int n_items;
@@ -126,6 +154,15 @@ struct AttnArgs {
   float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
 };
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
+// Host: XCD-balanced, longest-first block -> item table for the items of the
+// given requests (contiguous item ranges); appended to out; returns the block count.
+int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std::pair<int, int>> &ranges,
+                      std::vector<int32_t> &out);
+// Host: round-to-nearest-even fp32 -> bf16 bits (NaN stays a quiet NaN).
+uint16_t f32_to_bf16_rne(float f);
+// Host: upload L stacked [K][N] fp32 matrices as [L][N][K] (K contiguous), in
+// bf16 or fp32; synchronous.
+hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16);
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16, hipStream_t s);

@@ -1,4 +1,5 @@
-"""Python binding of the rosa C ABI (include/rosa.h, include/rosa_debug.h).
+"""Python binding of the rosa C ABI (include/rosa.h, rosa_prefill.h, rosa_sched.h,
+rosa_debug.h).
 
 Argument marshalling only: every step of the computation runs in the HIP
 library.  PyTorch supplies device memory and the stream.  The library must be
@@ -53,6 +54,24 @@ class S1Outcome(C.Structure):
 
     def as_dict(self) -> Dict[str, float]:
         return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class VlmConfig(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
+                ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_mlp", C.c_int32),
+                ("rms_eps", C.c_float), ("dtype", C.c_int32)]
+
+
+_VLM_WEIGHT_FIELDS = ["w_qkv", "w_o", "w_up", "w_down"]
+
+
+class VlmWeights(C.Structure):
+    _fields_ = [(n, C.POINTER(C.c_float)) for n in _VLM_WEIGHT_FIELDS]
+
+
+class PrefixJob(C.Structure):
+    _fields_ = [("embeddings", C.c_void_p), ("prefix_k", C.c_void_p), ("prefix_v", C.c_void_p),
+                ("prefix_len", C.c_int32), ("reserved", C.c_int32)]
 
 
 class RosaError(RuntimeError):
@@ -111,6 +130,19 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_s1_select_batch.argtypes = [C.POINTER(i32), C.POINTER(C.c_double), i32, i32, C.c_double, C.c_double,
                                          i32, C.POINTER(i32), C.POINTER(S1Outcome)]
     lib.rosa_s1_select_batch.restype = C.c_int
+    lib.rosa_prefill_create.argtypes = [C.POINTER(VlmConfig), C.POINTER(VlmWeights), i32, i64, vp, C.POINTER(vp)]
+    lib.rosa_prefill_create.restype = C.c_int
+    lib.rosa_prefill_run.argtypes = [vp, C.POINTER(PrefixJob), i32]
+    lib.rosa_prefill_run.restype = C.c_int
+    lib.rosa_prefill_destroy.argtypes = [vp]
+    lib.rosa_prefill_destroy.restype = None
+    lib.rosa_prefill_last_error.argtypes = [vp]
+    lib.rosa_prefill_last_error.restype = C.c_char_p
+    lib.rosa_debug_prefill_set_profiling.argtypes = [vp, i32]
+    lib.rosa_debug_prefill_set_profiling.restype = C.c_int
+    lib.rosa_debug_prefill_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64),
+                                                   C.POINTER(C.c_double), i32, C.POINTER(i32)]
+    lib.rosa_debug_prefill_get_profile.restype = C.c_int
     _lib = lib
     return lib
 
@@ -271,6 +303,76 @@ class ActionExpert:
     def close(self) -> None:
         if getattr(self, "handle", None):
             self.lib.rosa_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def vlm_config(shape, dtype: str) -> VlmConfig:
+    return VlmConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                     shape.d_mlp, shape.rms_eps, ROSA_BF16 if dtype == "bf16" else ROSA_FP32)
+
+
+def prefix_job(embeddings, prefix_k, prefix_v, P: int) -> PrefixJob:
+    """A prefix-producer job from torch device tensors (or raw integer device pointers)."""
+    def ptr(t):
+        return t if isinstance(t, int) else t.data_ptr()
+    return PrefixJob(ptr(embeddings), ptr(prefix_k), ptr(prefix_v), P, 0)
+
+
+class PrefixProducer:
+    """A rosa_prefill handle: the VLM backbone's weights on the GPU plus workspaces."""
+
+    def __init__(self, shape, dtype: str, weights: Dict[str, np.ndarray], max_jobs: int, max_tokens: int,
+                 stream: Optional[int] = None):
+        import torch
+        self.lib = load()
+        self.shape, self.dtype = shape, dtype
+        self._cfg = vlm_config(shape, dtype)
+        host = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in _VLM_WEIGHT_FIELDS}
+        w = VlmWeights(*[_f32_ptr(host[k]) for k in _VLM_WEIGHT_FIELDS])
+        if stream is None:
+            stream = torch.cuda.current_stream().cuda_stream
+        self.stream = stream
+        h = C.c_void_p()
+        st = self.lib.rosa_prefill_create(C.byref(self._cfg), C.byref(w), max_jobs, max_tokens, C.c_void_p(stream),
+                                          C.byref(h))
+        del host   # the library copied what it needs
+        if st != ROSA_OK:
+            raise RosaError(st, self.lib.rosa_prefill_last_error(None).decode())
+        self.handle = h
+
+    def _check(self, st: int):
+        if st != ROSA_OK:
+            raise RosaError(st, self.lib.rosa_prefill_last_error(self.handle).decode())
+
+    def run_status(self, jobs: Sequence[PrefixJob]) -> int:
+        arr = (PrefixJob * max(1, len(jobs)))(*jobs)
+        return self.lib.rosa_prefill_run(self.handle, arr, len(jobs))
+
+    def run(self, jobs: Sequence[PrefixJob]) -> None:
+        """Enqueue rosa_prefill_run; raises on error."""
+        self._check(self.run_status(jobs))
+
+    def set_profiling(self, enable: bool) -> None:
+        self._check(self.lib.rosa_debug_prefill_set_profiling(self.handle, 1 if enable else 0))
+
+    def profile(self) -> Dict[str, tuple]:
+        n = 16
+        names = (C.c_char_p * n)()
+        launches = (C.c_int64 * n)()
+        ms = (C.c_double * n)()
+        cnt = C.c_int32()
+        self._check(self.lib.rosa_debug_prefill_get_profile(self.handle, names, launches, ms, n, C.byref(cnt)))
+        return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(cnt.value)}
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            self.lib.rosa_prefill_destroy(self.handle)
             self.handle = None
 
     def __del__(self):

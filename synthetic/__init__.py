@@ -40,7 +40,7 @@ __all__ = [
     "TINY_SHAPE", "PI0_SHAPE", "bf16_round", "bf16_bits", "bits_to_f32",
     "make_weights", "make_metadata", "make_request", "make_requests",
     "weight_shapes", "VlmShape", "TINY_VLM", "PI0_VLM", "VLM_WEIGHT_ORDER", "vlm_weight_shapes",
-    "make_vlm_weights", "make_prefix_embeddings",
+    "make_vlm_weights", "make_prefix_embeddings", "prefill_lengths",
 ]
 
 
@@ -277,17 +277,28 @@ def vlm_weight_shapes(s: VlmShape) -> Dict[str, tuple]:
             "w_up": (L, d, s.d_mlp), "w_down": (L, s.d_mlp, d)}
 
 
-def make_vlm_weights(shape: VlmShape, dtype: str = "bf16", seed: int = 1, std: float = 0.02
-                     ) -> Dict[str, np.ndarray]:
-    """Backbone weights N(0, std^2), drawn in VLM_WEIGHT_ORDER from the
-    weights child of SeedSequence(seed); bf16-representable in bf16 mode."""
+def make_vlm_weights(shape: VlmShape, dtype: str = "bf16", seed: int = 1, std: float = 0.02,
+                     threads: int = 16) -> Dict[str, np.ndarray]:
+    """Backbone weights N(0, std^2); bf16-representable in bf16 mode.  The
+    weights child of SeedSequence(seed) is spawned into one child per (tensor,
+    layer), tensor-major in VLM_WEIGHT_ORDER, and each layer's matrix is drawn
+    from its own child, so layers are drawn in parallel with the same values."""
     wss, _, _ = _children(seed, 0)
-    rng = np.random.Generator(np.random.PCG64(wss))
-    out = {}
-    for name in VLM_WEIGHT_ORDER:
-        w = rng.standard_normal(vlm_weight_shapes(shape)[name], dtype=np.float32)
+    L = shape.n_layers
+    kids = wss.spawn(len(VLM_WEIGHT_ORDER) * L)
+    shapes = vlm_weight_shapes(shape)
+    out = {n: np.empty(shapes[n], dtype=np.float32) for n in VLM_WEIGHT_ORDER}
+
+    def draw(job):
+        ti, l = divmod(job, L)
+        name = VLM_WEIGHT_ORDER[ti]
+        rng = np.random.Generator(np.random.PCG64(kids[job]))
+        w = rng.standard_normal(shapes[name][1:], dtype=np.float32)
         w *= np.float32(std)
-        out[name] = bf16_round(w) if dtype == "bf16" else w
+        out[name][l] = bf16_round(w) if dtype == "bf16" else w
+
+    with ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+        list(ex.map(draw, range(len(VLM_WEIGHT_ORDER) * L)))
     return out
 
 
@@ -297,3 +308,12 @@ def make_prefix_embeddings(shape: VlmShape, prefix_len: int, dtype: str, seed: i
     rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed)))
     x = rng.standard_normal((prefix_len, shape.d_model), dtype=np.float32)
     return bf16_round(x) if dtype == "bf16" else x
+
+
+def prefill_lengths(n_jobs: int = 32, lo: int = 600, hi: int = 1024, seed: int = 11) -> List[int]:
+    """Prefix lengths of a prefill batch: n_jobs draws, uniform on [lo, hi]
+    inclusive, from numpy.random.default_rng(seed).  The default is the
+    benchmarked batch: 32 robots' prefixes of a few camera images plus an
+    instruction (600..1024 tokens, as the pi0_b32 preset)."""
+    rng = np.random.default_rng(seed)
+    return [int(p) for p in rng.integers(lo, hi + 1, size=n_jobs)]

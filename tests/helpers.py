@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions() -> List[str]:
     """Every function the public headers declare."""
     names = []
-    for h in ["rosa.h", "rosa_debug.h", "rosa_sched.h"]:
+    for h in ["rosa.h", "rosa_debug.h", "rosa_sched.h", "rosa_prefill.h"]:
         src = open(os.path.join(ROOT, "include", h)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
         names += re.findall(r"\b(rosa_[a-z0-9_]+)\s*\(", src)

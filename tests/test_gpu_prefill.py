@@ -1,0 +1,176 @@
+"""Prefix producer on the GPU (include/rosa_prefill.h) against the oracle's
+backbone (Sec. 2.2.1: the VLM's per-layer keys and values are the action
+head's prefix cache): every layer's K and V caches of a ragged batch of jobs,
+element by element, in fp32 and bf16; the caches feeding the action expert
+end to end; the full-size backbone on a sampled job; argument validation."""
+import numpy as np
+import pytest
+
+from oracle import OracleModel, prefill
+from synthetic import (PI0_VLM, TINY_SHAPE, TINY_VLM, VlmShape, custom_request, make_prefix_embeddings,
+                       make_vlm_weights, prefill_lengths)
+from tests.helpers import cached_weights, rel_l2
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+# fp32: only the summation order differs from the float64 oracle.  bf16: the
+# normalised rows, projections, attention output, MLP activations and the
+# caches themselves are rounded to bf16 (relative 2^-9 each), accumulated in
+# fp32; a few such roundings per layer stay well inside 1e-2.
+TOL = {"fp32": 1e-5, "bf16": 1e-2}
+# Same backbone width and heads as PI0_VLM with two layers: the hd-256 tiles
+# and the 16384-wide MLP at a size the oracle finishes in seconds.
+PI0_VLM_2L = VlmShape(n_layers=2, d_model=2048, n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384)
+
+
+def _rosa():
+    from paper_2607_01088_amd import rosa
+    return rosa
+
+
+_W = {}
+
+
+def _weights(shape, dtype):
+    key = (shape, dtype)
+    if key not in _W:
+        _W.clear()
+        _W[key] = make_vlm_weights(shape, dtype)
+    return _W[key]
+
+
+def _tdtype(dtype):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+class _Jobs:
+    """Embeddings on the device and NaN-filled cache buffers."""
+
+    def __init__(self, shape, dtype, lens, seed):
+        rosa = _rosa()
+        self.lens = list(lens)
+        self.x = [make_prefix_embeddings(shape, P, dtype, seed * 1000 + i) for i, P in enumerate(lens)]
+        td = _tdtype(dtype)
+        self.emb = [torch.from_numpy(x).to(td).cuda() for x in self.x]
+        cache = lambda P: torch.full((shape.n_layers, P, shape.n_kv_heads, shape.head_dim), float("nan"),
+                                     dtype=td, device="cuda")
+        self.k = [cache(P) for P in lens]
+        self.v = [cache(P) for P in lens]
+        self.structs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(self.emb, self.k, self.v, lens)]
+
+    def caches(self, i):
+        return self.k[i].float().cpu().numpy(), self.v[i].float().cpu().numpy()
+
+
+def _run(shape, dtype, lens, seed=1, max_jobs=None, max_tokens=None):
+    rosa = _rosa()
+    w = _weights(shape, dtype)
+    jobs = _Jobs(shape, dtype, lens, seed)
+    pp = rosa.PrefixProducer(shape, dtype, w, max_jobs or len(lens), max_tokens or sum(lens))
+    pp.run(jobs.structs)
+    torch.cuda.synchronize()
+    pp.close()
+    return w, jobs
+
+
+def _check_layers(shape, dtype, w, jobs, idx):
+    for i in idx:
+        K, V = prefill(jobs.x[i], w, shape)
+        gk, gv = jobs.caches(i)
+        assert np.isfinite(gk).all() and np.isfinite(gv).all(), i
+        for l in range(shape.n_layers):
+            ek, ev = rel_l2(gk[l], K[l]), rel_l2(gv[l], V[l])
+            print(f"job {i} P={jobs.lens[i]} layer {l}: K {ek:.2e} V {ev:.2e}", flush=True)
+            assert ek <= TOL[dtype] and ev <= TOL[dtype], (i, l, ek, ev)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_tiny_ragged_batch_matches_oracle(dtype):
+    # P = 1 (a single token), several 32-row groups, ragged tails, and jobs
+    # long enough for the bf16 launch to split their keys over work items.
+    lens = [1, 5, 37, 130, 300, 64]
+    w, jobs = _run(TINY_VLM, dtype, lens)
+    _check_layers(TINY_VLM, dtype, w, jobs, range(len(lens)))
+
+
+def test_bf16_many_jobs_no_key_split():
+    # Enough query blocks that no job's keys are split (one item per block).
+    rng = np.random.default_rng(7)
+    lens = [int(p) for p in rng.integers(1, 65, size=260)]
+    w, jobs = _run(TINY_VLM, "bf16", lens, seed=2)
+    _check_layers(TINY_VLM, "bf16", w, jobs, [0, 1, 2, 100, 259])
+
+
+def test_bf16_pi0_width_matches_oracle():
+    lens = [816, 300, 17]
+    w, jobs = _run(PI0_VLM_2L, "bf16", lens, seed=3)
+    _check_layers(PI0_VLM_2L, "bf16", w, jobs, range(len(lens)))
+
+
+def test_bf16_full_backbone_sampled_job():
+    # The benchmarked backbone (18 layers) and batch: 32 jobs of 600..1024
+    # prefix tokens; the shortest job is checked against the oracle.
+    lens = prefill_lengths()
+    w, jobs = _run(PI0_VLM, "bf16", lens, seed=4)
+    i = int(np.argmin(lens))
+    _check_layers(PI0_VLM, "bf16", w, jobs, [i])
+    for j in range(len(lens)):
+        gk, gv = jobs.caches(j)
+        assert np.isfinite(gk).all() and np.isfinite(gv).all(), j
+    _W.clear()
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_prefill_feeds_action_expert(dtype):
+    rosa = _rosa()
+    lens = [40, 3, 200]
+    w, jobs = _run(TINY_VLM, dtype, lens, seed=5)
+    ew = cached_weights(TINY_SHAPE, dtype)
+    reqs = [custom_request(TINY_SHAPE, dtype, 0, 8, 4, 50 + i) for i in range(len(lens))]
+    noise = [torch.from_numpy(np.ascontiguousarray(r.noise, dtype=np.float32)).cuda() for r in reqs]
+    out = [torch.full_like(n, float("nan")) for n in noise]
+    structs = [rosa.request_struct(jobs.k[i], jobs.v[i], noise[i], out[i], lens[i], r.horizon, r.steps)
+               for i, r in enumerate(reqs)]
+    cap = rosa.capacity(len(reqs), 8, 8 * len(reqs), 4, sum(lens))
+    e = rosa.ActionExpert(TINY_SHAPE, dtype, ew, cap)
+    e.generate(structs)
+    torch.cuda.synchronize()
+    e.close()
+    om = OracleModel(ew, TINY_SHAPE)
+    for i, r in enumerate(reqs):
+        K, V = prefill(jobs.x[i], w, TINY_VLM)
+        ref = om.generate_chunk(r.noise, r.steps, K, V)
+        err = rel_l2(out[i].cpu().numpy(), ref)
+        print(f"request {i} P={lens[i]}: rel-L2 {err:.2e}", flush=True)
+        assert err <= TOL[dtype], (i, err)
+
+
+def test_validation():
+    rosa = _rosa()
+    w = _weights(TINY_VLM, "fp32")
+    pp = rosa.PrefixProducer(TINY_VLM, "fp32", w, 2, 64)
+    jobs = _Jobs(TINY_VLM, "fp32", [8, 8], 9)
+    assert pp.run_status([]) == rosa.ROSA_OK
+    bad = rosa.prefix_job(jobs.emb[0], jobs.k[0], jobs.v[0], 0)
+    assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
+    bad = rosa.prefix_job(jobs.emb[0], jobs.k[0], jobs.v[0], 8)
+    bad.reserved = 1
+    assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
+    bad = rosa.prefix_job(0, jobs.k[0], jobs.v[0], 8)
+    assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
+    bad = rosa.prefix_job(jobs.emb[0].data_ptr() + 4, jobs.k[0], jobs.v[0], 7)
+    assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
+    assert pp.run_status(jobs.structs * 2) == rosa.ROSA_E_CAPACITY          # 4 jobs > max_jobs
+    big = _Jobs(TINY_VLM, "fp32", [40, 40], 10)
+    assert pp.run_status(big.structs) == rosa.ROSA_E_CAPACITY               # 80 tokens > 64
+    # A rejected call wrote nothing; a valid one still runs.
+    assert np.isnan(jobs.caches(0)[0]).all()
+    pp.run(jobs.structs)
+    torch.cuda.synchronize()
+    assert np.isfinite(jobs.caches(1)[1]).all()
+    pp.close()
+    with pytest.raises(rosa.RosaError):
+        rosa.PrefixProducer(VlmShape(1, 256, 4, 1, 48, 512), "fp32",
+                            make_vlm_weights(VlmShape(1, 256, 4, 1, 48, 512), "fp32"), 1, 8)
