@@ -138,6 +138,29 @@ def _counter_avg(rs, kernel_prefix):
     return sum(v) / len(v), len(v)
 
 
+def _summarize_prefill(out):
+    """Kernel-time table of the prefix producer from a --kernel-trace --stats
+    run of `bench.py --prefill` (prof_prefill/)."""
+    stats = _csv_rows(f"{out}/prof_prefill/**/*kernel_stats.csv")
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["# Kernel-time summary: vlm_prefill_b32 workload (32 robots' prefixes, 26,173 tokens, "
+             "18-layer width-2048 VLM backbone, bf16)", "",
+             "Command (one MI355X, repository root, library built in-tree):", "", "```",
+             "export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_prefill "
+             "-o prefill -- python3 -u bench.py --prefill --steps 3 --warmup 1 --no-cpu-baseline",
+             "python bench.py --summarize-profiles gpurun_out", "```", "",
+             "The profiled process runs 1 warm-up + 3 timed + 2 per-kernel-timing prefill calls (6 calls); each "
+             "call is 18 QKV projections and K/V scatters and 17 attention, output-projection and MLP layers "
+             "(the last layer's caches need only its K and V).",
+             "Table from `prefill_kernel_stats.csv`, sorted by total time.", "",
+             "| Kernel | Calls | Avg (us) | Total (ms) | % |", "|---|---:|---:|---:|---:|"]
+    for r in stats:
+        name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
+    open(os.path.join(PROFILES, "kernel_stats_vlm_prefill_b32.md"), "w").write("\n".join(lines) + "\n")
+
+
 def summarize_profiles(out):
     """Turn rocprofv3 outputs of this script into the summaries under
     profiles/ (kernel-time table, calibrated HBM traffic of the attention
@@ -145,8 +168,11 @@ def summarize_profiles(out):
     FETCH_SIZE and WRITE_SIZE --pmc runs (pmc_fetch/, pmc_write/) and the same
     counters for --copy-probe (pmc_cfetch/, pmc_cwrite/); the commands are
     written into the summaries."""
-    import csv
     import glob
+    if glob.glob(f"{out}/prof_prefill/**/*kernel_stats.csv", recursive=True):
+        _summarize_prefill(out)
+    if not glob.glob(f"{out}/prof_factory/**/*kernel_stats.csv", recursive=True):
+        return
     stats = _csv_rows(f"{out}/prof_factory/**/*kernel_stats.csv")
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
     lines = ["# Kernel-time summary: factory_b256 workload (256 ragged requests, pi0-shaped expert, bf16)", "",
@@ -158,7 +184,7 @@ def summarize_profiles(out):
              "Table from `factory_kernel_stats.csv`, sorted by total time.", "",
              "| Kernel | Calls | Avg (us) | Total (ms) | % |", "|---|---:|---:|---:|---:|"]
     for r in stats:
-        name = r["Name"].split("(")[0]
+        name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0]
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                      f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f} |")
     open(os.path.join(PROFILES, "kernel_stats_factory_b256.md"), "w").write("\n".join(lines) + "\n")
@@ -378,34 +404,34 @@ def prefill_work(shape, lens):
     }
 
 
-def prefill_cpu_baseline(shape, weights, x, lens, budget_layers: int = 2):
-    """The oracle backbone on a bounded sample: the first `budget_layers`
-    layers of the shortest job, scaled to the whole batch and all layers by
-    algorithmic flops."""
-    import dataclasses
+def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float):
+    """The oracle backbone on a bounded sample: whole jobs of the batch, in
+    order, until budget_s seconds have been spent; scaled to the whole batch by
+    algorithmic flops (the oracle's cost is additive over jobs)."""
     from oracle import prefill
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         blas_threads = 1
-    sub = dataclasses.replace(shape, n_layers=budget_layers)
-    w = {k: v[:budget_layers] for k, v in weights.items()}
-    t0 = time.perf_counter()
-    prefill(x, w, sub)
-    t = time.perf_counter() - t0
     # the oracle runs every layer in full: 2 * (qkv + o + up + down) per token and layer, plus attention
     per_tok = 2.0 * (shape.d_model * shape.qkv_dim + shape.n_q_heads * shape.head_dim * shape.d_model
                      + 2 * shape.d_model * shape.d_mlp)
-    att = lambda P: 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P
-    f_sample = budget_layers * (per_tok * x.shape[0] + att(x.shape[0]))
-    f_total = shape.n_layers * sum(per_tok * P + att(P) for P in lens)
-    batch_s = t * f_total / f_sample
+    flops = lambda P: shape.n_layers * (per_tok * P + 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P)
+    t_used, done = 0.0, 0
+    for x in xs:
+        t0 = time.perf_counter()
+        prefill(x, weights, shape)
+        t_used += time.perf_counter() - t0
+        done += 1
+        if t_used >= budget_s:
+            break
+    batch_s = t_used * sum(flops(P) for P in lens) / sum(flops(P) for P in lens[:done])
     return {"value": sum(lens) / batch_s, "unit": "prefix tokens/s", "cores": int(blas_threads),
             "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": (f"first {budget_layers} of {shape.n_layers} layers of one {x.shape[0]}-token job, "
-                       f"{t:.1f} s measured, scaled to {len(lens)} jobs x {shape.n_layers} layers by "
-                       f"algorithmic flops (extrapolated batch time {batch_s:.1f} s); NumPy float64")}
+            "sample": (f"{done} of {len(lens)} jobs ({sum(lens[:done])} tokens, all {shape.n_layers} layers), "
+                       f"{t_used:.1f} s measured, scaled to the whole batch by algorithmic flops "
+                       f"(extrapolated batch time {batch_s:.1f} s); NumPy float64")}
 
 
 def prefill_bench(torch, rosa, args):
@@ -485,8 +511,7 @@ def prefill_bench(torch, rosa, args):
     }
     pp.close()
     if not args.no_cpu_baseline:
-        i = int(np.argmin(lens))
-        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs[i], lens)
+        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs, lens, args.cpu_budget)
     print(json.dumps(out), flush=True)
 
 

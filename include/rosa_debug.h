@@ -83,6 +83,9 @@ rosa_status rosa_debug_get_profile(rosa_batch *b, const char **names, int64_t *l
  * classes load, norm, gemm_qkv, kv_scatter, attention, attn_merge, gemm_o,
  * gemm_up, gemm_down. */
 rosa_status rosa_debug_prefill_set_profiling(rosa_prefill *h, int32_t enable);
+/* Force the prefix producer's projection block configuration (as
+ * rosa_debug_gemm_config). */
+rosa_status rosa_debug_prefill_gemm_config(rosa_prefill *h, int32_t cfg, int32_t *n_configs);
 rosa_status rosa_debug_prefill_get_profile(rosa_prefill *h, const char **names, int64_t *launches,
                                            double *total_ms, int32_t max, int32_t *n_out);
 

@@ -291,20 +291,23 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
 // Block configurations and their measured cost on MI355X (one round of
 // blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
 // (store, GELU, gated residual); least-squares fits to the projection shapes
-// of the batch workloads at 1060, 2113, 4241 and 8482 rows.
-struct GemmCfg { int bm, bn, bk; float a, b[3]; };
+// of the batch workloads at 1060, 2113, 4241 and 8482 rows.  Past K = 4096 a
+// round costs a2 more per 1024 of K, from the 16384-deep MLP-down projection
+// of a 26173-row VLM backbone batch (long sustained launches run each tile
+// more slowly, by an amount that differs between tiles).
+struct GemmCfg { int bm, bn, bk; float a, a2, b[3]; };
 static constexpr GemmCfg kCfgs[kGemmConfigs] = {
-    {384, 128, 32, 15.5f, {9.7f, 13.1f, 19.8f}},  // 0: 8 waves, 96 x 64 each
-    {256, 256, 32, 20.1f, {8.8f, 12.5f, 16.0f}},  // 1: 16 waves, 64 x 64 each
-    {128, 256, 32, 12.5f, {7.5f, 7.9f, 13.8f}},   // 2: 8 waves, 64 x 64 each
-    {192, 128, 32, 12.3f, {5.3f, 4.2f, 9.1f}},    // 3: 8 waves, 96 x 32 each
-    {288, 128, 32, 17.1f, {7.5f, 9.9f, 13.6f}},   // 4: 12 waves, 96 x 32 each
-    {128, 64, 64, 4.6f, {3.0f, 3.2f, 6.9f}},      // 5: 4 waves, 64 x 32 each
-    {192, 128, 64, 8.9f, {6.8f, 8.4f, 13.1f}},    // 6: 8 waves, 96 x 32 each
-    {128, 128, 64, 6.8f, {4.5f, 6.2f, 11.5f}},    // 7: 4 waves, 64 x 64 each
-    {160, 128, 64, 9.5f, {4.6f, 6.5f, 15.1f}},    // 8: 4 waves, 160 x 32 each
-    {96, 128, 64, 6.5f, {3.5f, 4.8f, 9.0f}},      // 9: 4 waves, 96 x 32 each
-    {256, 64, 64, 7.1f, {4.0f, 5.0f, 9.2f}},      // 10: 8 waves, 64 x 32 each
+    {384, 128, 32, 15.5f, 19.2f, {9.7f, 13.1f, 19.8f}},  // 0: 8 waves, 96 x 64 each
+    {256, 256, 32, 20.1f, 13.8f, {8.8f, 12.5f, 16.0f}},  // 1: 16 waves, 64 x 64 each
+    {128, 256, 32, 12.5f, 13.0f, {7.5f, 7.9f, 13.8f}},   // 2: 8 waves, 64 x 64 each
+    {192, 128, 32, 12.3f, 3.2f, {5.3f, 4.2f, 9.1f}},     // 3: 8 waves, 96 x 32 each
+    {288, 128, 32, 17.1f, 15.3f, {7.5f, 9.9f, 13.6f}},   // 4: 12 waves, 96 x 32 each
+    {128, 64, 64, 4.6f, 5.0f, {3.0f, 3.2f, 6.9f}},       // 5: 4 waves, 64 x 32 each
+    {192, 128, 64, 8.9f, 6.8f, {6.8f, 8.4f, 13.1f}},     // 6: 8 waves, 96 x 32 each
+    {128, 128, 64, 6.8f, 6.0f, {4.5f, 6.2f, 11.5f}},     // 7: 4 waves, 64 x 64 each
+    {160, 128, 64, 9.5f, 3.4f, {4.6f, 6.5f, 15.1f}},     // 8: 4 waves, 160 x 32 each
+    {96, 128, 64, 6.5f, 4.2f, {3.5f, 4.8f, 9.0f}},       // 9: 4 waves, 96 x 32 each
+    {256, 64, 64, 7.1f, 7.4f, {4.0f, 5.0f, 9.2f}},       // 10: 8 waves, 64 x 32 each
 };
 using Cfg0 = GemmTile<12, 2, 4, 2>;
 using Cfg1 = GemmTile<8, 2, 4, 4>;
@@ -363,7 +366,8 @@ int gemm_pick_config(int M, int N, int K, int epi, int n_cu) {
   for (int c = 0; c < kGemmConfigs; ++c) {
     const long tiles = (long)((M + kCfgs[c].bm - 1) / kCfgs[c].bm) * ((N + kCfgs[c].bn - 1) / kCfgs[c].bn);
     const long rounds = (tiles + n_cu - 1) / n_cu;
-    const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].b[e]);
+    const float t = rounds * (kCfgs[c].a * (K / 1024.0f) + kCfgs[c].a2 * (std::max(K - 4096, 0) / 1024.0f) +
+                              kCfgs[c].b[e]);
     if (best_t == 0.f || t < best_t) { best = c; best_t = t; }
   }
   return best;

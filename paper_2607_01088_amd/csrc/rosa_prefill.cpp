@@ -51,6 +51,7 @@ struct rosa_prefill {
   int device = 0;
   hipStream_t stream = nullptr;
   bool poisoned = false;
+  int gemm_cfg = -1;                         // forced projection block configuration, -1: cost model
   std::string last_error;
   int32_t max_jobs = 0;
   int64_t max_tokens = 0;
@@ -60,6 +61,7 @@ struct rosa_prefill {
   void *wt_qkv = nullptr, *wt_o = nullptr, *wt_up = nullptr, *wt_down = nullptr;  // [L][N][K]
   float *h = nullptr;
   void *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr;
+  int ldg = 0;                               // row stride of g: d_mlp + 64, off a power of two
   float *zeros = nullptr, *ones = nullptr;   // [d]: zero shift and scale, unit gate
   int32_t *rowmod = nullptr;                 // [max_tokens] zeros
   float *part_o = nullptr, *part_ml = nullptr;
@@ -328,7 +330,8 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     h->u = palloc<uint8_t>(h, T * d * es, e);
     h->qkv = palloc<uint8_t>(h, T * h->qkv_dim * es, e);
     h->o = palloc<uint8_t>(h, T * h->o_dim * es, e);
-    h->g = palloc<uint8_t>(h, T * h->dff * es, e);
+    h->ldg = h->dff + 64;
+    h->g = palloc<uint8_t>(h, T * h->ldg * es, e);
     h->zeros = palloc<float>(h, d, e);
     h->ones = palloc<float>(h, d, e);
     h->rowmod = palloc<int32_t>(h, T, e);
@@ -414,7 +417,7 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       GemmArgs gq{};
       gq.a = h->u; gq.lda = h->d; gq.wt = (uint8_t *)h->wt_qkv + (size_t)l * h->qkv_dim * h->d * es;
       gq.M = M; gq.N = h->qkv_dim; gq.K = h->d; gq.epi = kEpiStore; gq.out = h->qkv; gq.ldo = h->qkv_dim;
-      e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gq, h->bf16, s); });
+      e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gq, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
       e = ptimed(h, pcScatter, [&] {
         return launch_prefill_kv_scatter(d_jobs, d_rows, M, h->qkv, h->qkv_dim, h->nq, h->nkv, h->hd, es, l, s);
@@ -440,7 +443,7 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       go.a = h->o; go.lda = h->o_dim; go.wt = (uint8_t *)h->wt_o + (size_t)l * h->d * h->o_dim * es;
       go.M = M; go.N = h->d; go.K = h->o_dim; go.epi = kEpiGatedResidual; go.out = h->h; go.ldo = h->d;
       go.gate = h->ones; go.gate_stride = 0; go.rowmod = h->rowmod;
-      e = ptimed(h, pcGemmO, [&] { return launch_gemm(go, h->bf16, s); });
+      e = ptimed(h, pcGemmO, [&] { return launch_gemm(go, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
       e = ptimed(h, pcNorm, [&] {
         return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s);
@@ -448,14 +451,14 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       if (e != hipSuccess) break;
       GemmArgs gu{};
       gu.a = h->u; gu.lda = h->d; gu.wt = (uint8_t *)h->wt_up + (size_t)l * h->dff * h->d * es;
-      gu.M = M; gu.N = h->dff; gu.K = h->d; gu.epi = kEpiGelu; gu.out = h->g; gu.ldo = h->dff;
-      e = ptimed(h, pcGemmUp, [&] { return launch_gemm(gu, h->bf16, s); });
+      gu.M = M; gu.N = h->dff; gu.K = h->d; gu.epi = kEpiGelu; gu.out = h->g; gu.ldo = h->ldg;
+      e = ptimed(h, pcGemmUp, [&] { return launch_gemm(gu, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
       GemmArgs gd{};
-      gd.a = h->g; gd.lda = h->dff; gd.wt = (uint8_t *)h->wt_down + (size_t)l * h->d * h->dff * es;
+      gd.a = h->g; gd.lda = h->ldg; gd.wt = (uint8_t *)h->wt_down + (size_t)l * h->d * h->dff * es;
       gd.M = M; gd.N = h->d; gd.K = h->dff; gd.epi = kEpiGatedResidual; gd.out = h->h; gd.ldo = h->d;
       gd.gate = h->ones; gd.gate_stride = 0; gd.rowmod = h->rowmod;
-      e = ptimed(h, pcGemmDown, [&] { return launch_gemm(gd, h->bf16, s); });
+      e = ptimed(h, pcGemmDown, [&] { return launch_gemm(gd, h->bf16, s, h->gemm_cfg); });
     }
     if (e != hipSuccess) return pdevice_fail(h, e, "kernel launch");
     return ROSA_OK;
@@ -489,6 +492,14 @@ rosa_status rosa_debug_prefill_set_profiling(rosa_prefill *h, int32_t enable) {
   } catch (...) {
     return pfail(h, ROSA_E_DEVICE, "unexpected exception");
   }
+}
+
+rosa_status rosa_debug_prefill_gemm_config(rosa_prefill *h, int32_t cfg, int32_t *n_configs) {
+  if (!h) return ROSA_E_INVALID;
+  if (n_configs) *n_configs = kGemmConfigs;
+  if (cfg < -1 || cfg >= kGemmConfigs) return pfail(h, ROSA_E_INVALID, "gemm configuration out of range");
+  h->gemm_cfg = cfg;
+  return ROSA_OK;
 }
 
 rosa_status rosa_debug_prefill_get_profile(rosa_prefill *h, const char **names, int64_t *launches,

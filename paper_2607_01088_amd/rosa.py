@@ -140,6 +140,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_prefill_last_error.restype = C.c_char_p
     lib.rosa_debug_prefill_set_profiling.argtypes = [vp, i32]
     lib.rosa_debug_prefill_set_profiling.restype = C.c_int
+    lib.rosa_debug_prefill_gemm_config.argtypes = [vp, i32, C.POINTER(i32)]
+    lib.rosa_debug_prefill_gemm_config.restype = C.c_int
     lib.rosa_debug_prefill_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64),
                                                    C.POINTER(C.c_double), i32, C.POINTER(i32)]
     lib.rosa_debug_prefill_get_profile.restype = C.c_int
@@ -360,6 +362,13 @@ class PrefixProducer:
 
     def set_profiling(self, enable: bool) -> None:
         self._check(self.lib.rosa_debug_prefill_set_profiling(self.handle, 1 if enable else 0))
+
+    def gemm_config(self, cfg: int) -> int:
+        """Force the projection block configuration (-1: cost model); returns
+        the number of configurations."""
+        n = C.c_int32()
+        self._check(self.lib.rosa_debug_prefill_gemm_config(self.handle, cfg, C.byref(n)))
+        return n.value
 
     def profile(self) -> Dict[str, tuple]:
         n = 16
