@@ -290,8 +290,37 @@ def batch_profile(torch, rosa, expert, db, reqs, preset, args):
                                   "gain_vs_batch1": round(o["throughput_hz"] / one["throughput_hz"], 2)
                                   if one["feasible"] else None})
                 choices.append(entry)
+    # Homogeneous fleet schedules on a node of 8 such GPUs: System-1 latency
+    # profiles L(b, rate) simulated from the measured call times, then the
+    # binary search on the shared action rate (System 1 only: no System-2 or
+    # obligation models are served here).
+    profile = [(b, rosa.rate_profile(b, t, n_rates=10, n_requests=max(4000, 40 * b), seed=1))
+               for b, t in zip(sizes, ms)]
+    schedules = []
+    for robots in [16, 64, 256, 1024]:
+        for t_act in [50.0, 200.0]:
+            s1 = {"role": rosa.ROSA_ROLE_S1, "deadline_ms": 200.0, "profile": profile}
+            t0 = time.perf_counter()
+            out = rosa.schedule_homogeneous({"robots": robots, "servers": 8, "t_act_ms": t_act, "horizon": 1,
+                                             "eps_hz": 1e-2}, [s1])
+            solve_s = time.perf_counter() - t0
+            servers = {}
+            for _, (b, k, mean, slo) in out["assignment"]:
+                servers.setdefault((b, k), [0, mean, slo])[0] += 1
+            schedules.append({"robots": robots, "t_act_ms": t_act, "feasible": out["feasible"],
+                              "f_hz": round(out["f_hz"], 3), "l_s1_ms": round(out["l_s1_ms"], 2),
+                              "fleet_chunks_per_s": round(out["f_hz"] * robots, 1),
+                              "bound_zero_latency_hz": round(1000.0 / t_act, 3),
+                              "servers": [{"batch": b, "streams": k, "count": c, "mean_ms": round(mn, 2),
+                                           "p99_ms": round(sl, 2)} for (b, k), (c, mn, sl) in sorted(servers.items())],
+                              "solve_s": round(solve_s, 3)})
+            print(f"[bench] schedule robots={robots} t_act={t_act}: f={out['f_hz']:.2f} Hz "
+                  f"({solve_s:.2f} s)", file=sys.stderr, flush=True)
     print(json.dumps({"kind": "s1_batch_profile", "workload": preset.name, "dtype": preset.dtype,
-                      "profile": rows, "choices": choices,
+                      "profile": rows, "choices": choices, "homogeneous_schedules": schedules,
+                      "schedule_model": "8 servers (GPUs) like this one, System 1 only, p99 deadline 200 ms; "
+                                        "L(b, rate) simulated from the measured p50 call times (Poisson arrivals, "
+                                        "a batch waits for b requests), ten rates per batch size",
                       "server_model": "closed loop, FIFO, a batch starts when the worker is idle and B "
                                       "requests wait; batch latency = measured p50"}), flush=True)
 

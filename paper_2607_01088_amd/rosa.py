@@ -74,6 +74,39 @@ class PrefixJob(C.Structure):
                 ("prefix_len", C.c_int32), ("reserved", C.c_int32)]
 
 
+class RatePoint(C.Structure):
+    _fields_ = [("rate_hz", C.c_double), ("mean_ms", C.c_double), ("slo_ms", C.c_double)]
+
+
+class ConfigProfile(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("n_points", C.c_int32), ("points", C.POINTER(RatePoint))]
+
+
+class ModelProfile(C.Structure):
+    _fields_ = [("role", C.c_int32), ("max_streams", C.c_int32), ("deadline_ms", C.c_double),
+                ("rate_per_robot_hz", C.c_double), ("n_configs", C.c_int32), ("reserved", C.c_int32),
+                ("configs", C.POINTER(ConfigProfile))]
+
+
+class Fleet(C.Structure):
+    _fields_ = [("robots", C.c_int32), ("servers", C.c_int32), ("t_act_ms", C.c_double), ("horizon", C.c_int32),
+                ("reserved", C.c_int32), ("eps_hz", C.c_double)]
+
+
+class ServerPlan(C.Structure):
+    _fields_ = [("model", C.c_int32), ("batch", C.c_int32), ("streams", C.c_int32), ("reserved", C.c_int32),
+                ("mean_ms", C.c_double), ("slo_ms", C.c_double)]
+
+
+class FleetSchedule(C.Structure):
+    _fields_ = [("feasible", C.c_int32), ("obligation_servers", C.c_int32), ("goal_servers", C.c_int32),
+                ("steps", C.c_int32), ("f_hz", C.c_double), ("l_s1_ms", C.c_double), ("l_s2_ms", C.c_double),
+                ("f_loop_hz", C.c_double)]
+
+
+ROSA_ROLE_S1, ROSA_ROLE_S2, ROSA_ROLE_OBLIGATION = 0, 1, 2
+
+
 class RosaError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"rosa status {status}: {msg}")
@@ -145,6 +178,11 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_prefill_get_profile.argtypes = [vp, C.POINTER(C.c_char_p), C.POINTER(i64),
                                                    C.POINTER(C.c_double), i32, C.POINTER(i32)]
     lib.rosa_debug_prefill_get_profile.restype = C.c_int
+    lib.rosa_rate_profile.argtypes = [i32, C.c_double, i32, i32, C.c_uint64, C.c_double, C.POINTER(RatePoint)]
+    lib.rosa_rate_profile.restype = C.c_int
+    lib.rosa_schedule_homogeneous.argtypes = [C.POINTER(Fleet), C.POINTER(ModelProfile), i32,
+                                              C.POINTER(FleetSchedule), C.POINTER(ServerPlan)]
+    lib.rosa_schedule_homogeneous.restype = C.c_int
     _lib = lib
     return lib
 
@@ -218,6 +256,49 @@ def s1_select_batch(batch_sizes: Sequence[int], batch_ms: Sequence[float], robot
     if st != ROSA_OK:
         raise RosaError(st, "rosa_s1_select_batch: invalid arguments")
     return (None if best.value < 0 else best.value), [outs[i].as_dict() for i in range(n)]
+
+
+def rate_profile(batch: int, batch_ms: float, n_rates: int = 10, n_requests: int = 4000, seed: int = 1,
+                 pct: float = 0.99) -> List[tuple]:
+    """rosa_rate_profile: [(rate_hz, mean_ms, slo_ms)] of one batch size."""
+    lib = load()
+    out = (RatePoint * n_rates)()
+    st = lib.rosa_rate_profile(batch, batch_ms, n_rates, n_requests, seed, pct, out)
+    if st != ROSA_OK:
+        raise RosaError(st, "rosa_rate_profile: invalid arguments")
+    return [(p.rate_hz, p.mean_ms, p.slo_ms) for p in out]
+
+
+def schedule_homogeneous(fleet: Dict, models: Sequence[Dict]) -> Dict:
+    """rosa_schedule_homogeneous.  fleet: robots, servers, t_act_ms, horizon,
+    eps_hz.  models: dicts with role (ROSA_ROLE_*), deadline_ms, profile
+    [(batch, [(rate, mean, slo), ...])], optional max_streams and
+    rate_per_robot_hz.  Returns the schedule with assignment
+    [(model, (batch, streams, mean_ms, slo_ms))]."""
+    lib = load()
+    keep = []
+    mp = (ModelProfile * len(models))()
+    for i, m in enumerate(models):
+        cps = (ConfigProfile * len(m["profile"]))()
+        for j, (batch, pts) in enumerate(m["profile"]):
+            arr = (RatePoint * len(pts))(*[RatePoint(*p) for p in pts])
+            keep.append(arr)
+            cps[j] = ConfigProfile(batch, len(pts), arr)
+        keep.append(cps)
+        mp[i] = ModelProfile(m["role"], m.get("max_streams", 0), m["deadline_ms"], m.get("rate_per_robot_hz", 0.0),
+                             len(m["profile"]), 0, cps)
+    fl = Fleet(fleet["robots"], fleet["servers"], fleet["t_act_ms"], fleet.get("horizon", 1), 0, fleet["eps_hz"])
+    out = FleetSchedule()
+    plans = (ServerPlan * fleet["servers"])()
+    st = lib.rosa_schedule_homogeneous(C.byref(fl), mp, len(models), C.byref(out), plans)
+    if st != ROSA_OK:
+        raise RosaError(st, "rosa_schedule_homogeneous: invalid arguments")
+    n = out.obligation_servers + out.goal_servers if out.feasible else 0
+    return {"feasible": bool(out.feasible), "f_hz": out.f_hz, "l_s1_ms": out.l_s1_ms, "l_s2_ms": out.l_s2_ms,
+            "f_loop_hz": out.f_loop_hz, "obligation_servers": out.obligation_servers,
+            "goal_servers": out.goal_servers, "steps": out.steps,
+            "assignment": [(plans[i].model, (plans[i].batch, plans[i].streams, plans[i].mean_ms, plans[i].slo_ms))
+                           for i in range(n)]}
 
 
 class ActionExpert:

@@ -1,0 +1,125 @@
+"""The library's homogeneous scheduler (include/rosa_sched.h; Sec. 3.4.2)
+against the oracle: simulated rate profiles bitwise, and schedules on the
+pinned cases and on random tiny fleets (the library packs with a dynamic
+program, the oracle by exhaustive enumeration).  Host code only, no GPU."""
+import numpy as np
+import pytest
+
+from oracle.homogeneous import ROLE_OBLIGATION, ROLE_S1, ROLE_S2, lookup, rate_profile, schedule_homogeneous
+
+
+def _rosa():
+    from paper_2607_01088_amd import rosa
+    rosa.load()
+    return rosa
+
+
+@pytest.mark.parametrize("b,T", [(1, 16.8), (4, 20.0), (16, 19.4), (64, 31.0)])
+def test_rate_profile_bitwise(b, T):
+    rosa = _rosa()
+    got = rosa.rate_profile(b, T, n_rates=10, n_requests=max(2000, 40 * b), seed=3)
+    want = rate_profile(b, T, n_rates=10, n_requests=max(2000, 40 * b), seed=3)
+    assert got == want
+
+
+def _random_profile(rng, batch, base_ms):
+    peak = batch * 1000.0 / base_ms
+    pts, mean = [], base_ms * (1.0 + rng.random())
+    for j in range(1, 11):
+        mean += rng.random() * base_ms * 0.3
+        pts.append((peak * j / 10, mean, mean * (1.2 + 0.5 * rng.random())))
+    return (batch, pts)
+
+
+def _random_case(rng):
+    R = int(rng.integers(1, 7))
+    S = int(rng.integers(1, 5))
+    models = []
+    bs = sorted(rng.choice([1, 2, 4], size=int(rng.integers(1, 4)), replace=False).tolist())
+    models.append({"role": ROLE_S1, "deadline_ms": float(rng.uniform(20, 120)),
+                   "profile": [_random_profile(rng, b, float(rng.uniform(5, 30))) for b in bs],
+                   "max_streams": int(rng.integers(0, 5))})
+    if rng.random() < 0.4:
+        models.append({"role": ROLE_S2, "deadline_ms": float(rng.uniform(150, 600)),
+                       "profile": [_random_profile(rng, 1, float(rng.uniform(50, 200)))]})
+    if rng.random() < 0.3:
+        models.append({"role": ROLE_OBLIGATION, "deadline_ms": float(rng.uniform(10, 60)),
+                       "profile": [_random_profile(rng, 1, float(rng.uniform(2, 8)))],
+                       "rate_per_robot_hz": float(rng.uniform(1, 20))})
+    fleet = {"robots": R, "servers": S, "t_act_ms": float(rng.uniform(10, 200)),
+             "horizon": int(rng.integers(1, 20)), "eps_hz": 1e-3}
+    return fleet, models
+
+
+def _check_valid(fleet, models, out):
+    per_model = {}
+    for mi, (batch, k, mean, slo) in out["assignment"]:
+        per_model[mi] = per_model.get(mi, 0) + k
+        m = models[mi]
+        assert slo <= m["deadline_ms"]
+        assert not m.get("max_streams") or k <= m["max_streams"]
+        prof = dict(m["profile"])[batch]
+        rate = (m["rate_per_robot_hz"] if m["role"] == ROLE_OBLIGATION else
+                out["f_hz"] if m["role"] == ROLE_S1 else out["f_hz"] / fleet["horizon"])
+        got = lookup(prof, batch, k * rate)
+        assert got is not None and abs(got[0] - mean) <= 1e-9 * max(1.0, mean)
+    for mi in range(len(models)):
+        assert per_model.get(mi, 0) == fleet["robots"], mi
+    assert len(out["assignment"]) <= fleet["servers"]
+
+
+def test_random_fleets_match_oracle():
+    rosa = _rosa()
+    rng = np.random.default_rng(2024)
+    n_feasible = 0
+    for case in range(150):
+        fleet, models = _random_case(rng)
+        want = schedule_homogeneous(fleet, models)
+        got = rosa.schedule_homogeneous(fleet, models)
+        assert got["feasible"] == want["feasible"], case
+        assert got["obligation_servers"] == want["obligation_servers"], case
+        if not want["feasible"]:
+            continue
+        n_feasible += 1
+        assert abs(got["f_hz"] - want["f_hz"]) <= 2 * fleet["eps_hz"], (case, got["f_hz"], want["f_hz"])
+        if got["f_hz"] == want["f_hz"]:
+            assert abs(got["l_s1_ms"] - want["l_s1_ms"]) <= 1e-9 * max(1.0, want["l_s1_ms"]), case
+            assert abs(got["l_s2_ms"] - want["l_s2_ms"]) <= 1e-9 * max(1.0, want["l_s2_ms"]), case
+            assert got["goal_servers"] == want["goal_servers"], case
+        _check_valid(fleet, models, got)
+    assert n_feasible >= 40
+
+
+def _const(batch, lat, max_rate):
+    return [(batch, [(max_rate * j / 10, lat, lat) for j in range(1, 11)])]
+
+
+def test_closed_form_cases():
+    rosa = _rosa()
+    s1 = {"role": ROLE_S1, "deadline_ms": 20.0, "profile": _const(1, 10.0, 60.0)}
+    for R, S, t_act in [(8, 2, 50.0), (8, 8, 50.0), (5, 2, 20.0)]:
+        out = rosa.schedule_homogeneous({"robots": R, "servers": S, "t_act_ms": t_act, "horizon": 1,
+                                         "eps_hz": 1e-4}, [s1])
+        want = min(60.0 / -(-R // S), 1000.0 / (t_act + 10.0))
+        assert want - 2e-4 <= out["f_hz"] <= want + 1e-12
+        assert abs(out["f_loop_hz"] - 1000.0 / (t_act + 10.0)) < 1e-9
+    safe = {"role": ROLE_OBLIGATION, "deadline_ms": 20.0, "profile": _const(1, 2.0, 100.0), "rate_per_robot_hz": 10.0}
+    out = rosa.schedule_homogeneous({"robots": 12, "servers": 4, "t_act_ms": 10.0, "horizon": 1, "eps_hz": 1e-4},
+                                    [s1, safe])
+    assert out["obligation_servers"] == 2 and abs(out["f_hz"] - 10.0) <= 2e-4
+    assert [a[0] for a in out["assignment"]] == [1, 1, 0, 0]     # obligation servers first
+
+
+def test_validation():
+    rosa = _rosa()
+    good = {"role": ROLE_S1, "deadline_ms": 20.0, "profile": _const(1, 10.0, 60.0)}
+    fleet = {"robots": 4, "servers": 2, "t_act_ms": 50.0, "horizon": 1, "eps_hz": 1e-3}
+    bad_sorted = dict(good, profile=[(1, [(20.0, 1.0, 1.0), (10.0, 2.0, 2.0)])])
+    dup = dict(good, profile=_const(1, 10.0, 60.0) * 2)
+    for models, fl in [([bad_sorted], fleet), ([dup], fleet), ([good], dict(fleet, robots=0)),
+                       ([good], dict(fleet, eps_hz=0.0)), ([dict(good, role=7)], fleet),
+                       ([dict(good, role=ROLE_OBLIGATION)], fleet)]:       # obligation without a rate
+        with pytest.raises(rosa.RosaError):
+            rosa.schedule_homogeneous(fl, models)
+    with pytest.raises(rosa.RosaError):
+        rosa.rate_profile(4, 10.0, n_requests=39)                           # fewer than 10 batches
