@@ -25,8 +25,11 @@ readings (each is restated where it is used):
   two-matrix tanh-GELU MLP; no biases in QKV/O/MLP;
 * attention: each action token of request r attends, bidirectionally, to all
   P_r cached prefix keys of request r followed by all H_r action keys of
-  request r; scale 1/sqrt(head_dim); query head g reads KV head
-  g // (n_q / n_kv); no rotary embedding;
+  request r (the joint, pi0-style layout); scale 1/sqrt(head_dim); query head
+  g reads KV head g // (n_q / n_kv); no rotary embedding.  The alternating,
+  GR00T-style layout (a DiT head that interleaves cross-attention to the VLM
+  context with self-attention, Sec. 2.2.1) attends to the prefix keys only in
+  even layers and to the request's own action keys only in odd layers;
 * final modulated RMSNorm (shift, scale) and an output projection with bias
   give the velocity.
 
@@ -134,6 +137,20 @@ class OracleModel:
         return np.split(s @ self.w["w_fmod"] + self.w["b_fmod"], 2)
 
     # ---- one velocity evaluation
+    def attention_keys(self, l: int, prefix_k, prefix_v, ka: np.ndarray, va: np.ndarray):
+        """Keys and values layer l's action tokens attend to.  Joint layout
+        (pi0-style, 0): the request's prefix keys of layer l, then its own
+        action keys.  Alternating layout (GR00T-style DiT, 1): even layers
+        cross-attend to the prefix keys only, odd layers self-attend to the
+        request's own action keys only."""
+        pk = np.asarray(prefix_k[l], dtype=F) if len(prefix_k) else None
+        pv = np.asarray(prefix_v[l], dtype=F) if len(prefix_v) else None
+        if getattr(self.shape, "attention_layout", 0) == 1:
+            return (pk, pv) if l % 2 == 0 else (ka, va)
+        if pk is None or pk.shape[0] == 0:
+            return ka, va
+        return np.concatenate([pk, ka], axis=0), np.concatenate([pv, va], axis=0)
+
     def velocity(self, x: np.ndarray, tau: float, prefix_k: np.ndarray, prefix_v: np.ndarray
                  ) -> np.ndarray:
         """v(x, tau) for one request.  x: [H][A]; prefix_k/v: [L][P][n_kv][hd]."""
@@ -149,8 +166,7 @@ class OracleModel:
             q = qkv[:, : nq * hd].reshape(H, nq, hd)
             ka = qkv[:, nq * hd: (nq + nkv) * hd].reshape(H, nkv, hd)
             va = qkv[:, (nq + nkv) * hd:].reshape(H, nkv, hd)
-            kf = np.concatenate([np.asarray(prefix_k[l], dtype=F), ka], axis=0)
-            vf = np.concatenate([np.asarray(prefix_v[l], dtype=F), va], axis=0)
+            kf, vf = self.attention_keys(l, prefix_k, prefix_v, ka, va)
             o = attention(q, kf, vf).reshape(H, nq * hd)
             h = h + ga * (o @ w["w_o"][l])
             u = modulate(rms_norm(h, sh.rms_eps), sm, cm)

@@ -37,7 +37,7 @@ import numpy as np
 
 __all__ = [
     "ModelShape", "Preset", "RequestData", "PRESETS", "WEIGHT_ORDER",
-    "TINY_SHAPE", "PI0_SHAPE", "bf16_round", "bf16_bits", "bits_to_f32",
+    "TINY_SHAPE", "PI0_SHAPE", "TINY_ALT_SHAPE", "PI0_ALT_SHAPE", "bf16_round", "bf16_bits", "bits_to_f32",
     "make_weights", "make_metadata", "make_request", "make_requests",
     "weight_shapes", "VlmShape", "TINY_VLM", "PI0_VLM", "VLM_WEIGHT_ORDER", "vlm_weight_shapes",
     "make_vlm_weights", "make_prefix_embeddings", "prefill_lengths",
@@ -55,6 +55,10 @@ class ModelShape:
     action_dim: int
     time_emb_dim: int
     rms_eps: float = 1e-6
+    # 0: joint attention over [prefix ; own actions] in every layer (pi0-style);
+    # 1: alternating, even layers cross-attend to the prefix only and odd
+    #    layers self-attend to the request's own actions only (GR00T-style DiT).
+    attention_layout: int = 0
 
     @property
     def qkv_dim(self) -> int:
@@ -65,6 +69,9 @@ TINY_SHAPE = ModelShape(n_layers=2, d_model=128, n_q_heads=4, n_kv_heads=1, head
                         d_mlp=512, action_dim=7, time_emb_dim=128)
 PI0_SHAPE = ModelShape(n_layers=18, d_model=1024, n_q_heads=8, n_kv_heads=1, head_dim=256,
                        d_mlp=4096, action_dim=32, time_emb_dim=1024)
+# The same sizes with the alternating cross-/self-attention layout.
+TINY_ALT_SHAPE = dataclasses.replace(TINY_SHAPE, attention_layout=1)
+PI0_ALT_SHAPE = dataclasses.replace(PI0_SHAPE, attention_layout=1)
 
 
 @dataclasses.dataclass(frozen=True)

@@ -238,8 +238,9 @@ def test_zero_gates_closed_form():
 
 # ------------------------------------------------------------------ whole forward, scalar brute force
 
-def _scalar_forward(w, sh, noise, K, pk, pv):
-    """The whole generate loop on nested Python lists and floats."""
+def _scalar_forward(w, sh, noise, K, pk, pv, layout=0):
+    """The whole generate loop on nested Python lists and floats.  layout 1:
+    even layers see only the prefix keys, odd layers only the action keys."""
     d, nq, nkv, hd, A = sh.d_model, sh.n_q_heads, sh.n_kv_heads, sh.head_dim, sh.action_dim
     H = len(noise)
     W = {k: v.astype(np.float64).tolist() for k, v in w.items()}
@@ -275,11 +276,17 @@ def _scalar_forward(w, sh, noise, K, pk, pv):
                 for g in range(nq):
                     j = g // (nq // nkv)
                     qv = qkv[t][g * hd:(g + 1) * hd]
-                    keys = [list(map(float, pk[l][p][j])) for p in range(len(pk[l]))] + \
-                           [qkv[tt][nq * hd + j * hd: nq * hd + (j + 1) * hd] for tt in range(H)]
-                    vals = [list(map(float, pv[l][p][j])) for p in range(len(pv[l]))] + \
-                           [qkv[tt][(nq + nkv) * hd + j * hd: (nq + nkv) * hd + (j + 1) * hd]
-                            for tt in range(H)]
+                    pre_k = [list(map(float, pk[l][p][j])) for p in range(len(pk[l]))]
+                    act_k = [qkv[tt][nq * hd + j * hd: nq * hd + (j + 1) * hd] for tt in range(H)]
+                    pre_v = [list(map(float, pv[l][p][j])) for p in range(len(pv[l]))]
+                    act_v = [qkv[tt][(nq + nkv) * hd + j * hd: (nq + nkv) * hd + (j + 1) * hd]
+                             for tt in range(H)]
+                    if layout == 1 and l % 2 == 0:
+                        keys, vals = pre_k, pre_v
+                    elif layout == 1:
+                        keys, vals = act_k, act_v
+                    else:
+                        keys, vals = pre_k + act_k, pre_v + act_v
                     lg = [sum(qv[c2] * kk[c2] for c2 in range(hd)) / math.sqrt(hd) for kk in keys]
                     mx = max(lg)
                     ws = [math.exp(z - mx) for z in lg]
@@ -315,6 +322,39 @@ def test_whole_forward_matches_scalar_bruteforce(nkv):
     ref = _scalar_forward(w, sh, req.noise, req.steps, req.prefix_k, req.prefix_v)
     got = OracleModel(w, sh).generate([req])[0]
     np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("P", [1, 3])
+def test_alternating_layout_matches_scalar_bruteforce(P):
+    sh = dataclasses.replace(MICRO, n_layers=4, attention_layout=1)
+    w = make_weights(sh, "fp32", seed=4, std=0.3)
+    rng = np.random.default_rng(8)
+    for k in ["b_in", "b_t1", "b_t2", "b_mod", "b_fmod", "b_out"]:
+        w[k] = (rng.standard_normal(w[k].shape) * 0.2).astype(np.float32)
+    req = custom_request(sh, "fp32", P, 3, 2, seed=16)
+    ref = _scalar_forward(w, sh, req.noise, req.steps, req.prefix_k, req.prefix_v, layout=1)
+    got = OracleModel(w, sh).generate([req])[0]
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-12)
+    joint = OracleModel(w, dataclasses.replace(sh, attention_layout=0)).generate([req])[0]
+    assert np.abs(joint - got).max() > 1e-6          # the layouts differ
+
+
+def test_alternating_layout_reads_prefix_in_even_layers_only():
+    sh = dataclasses.replace(TINY_SHAPE, attention_layout=1)
+    w = make_weights(sh, "fp32", seed=0)
+    d = sh.d_model
+    w["w_down"][:] = 0.0
+    w["b_mod"][:, 2 * d:3 * d] = 1.0                 # attention-isolating variant
+    r = custom_request(sh, "fp32", 40, 8, 4, seed=40)
+    m = OracleModel(w, sh)
+    base = m.generate([r])[0]
+    odd = dataclasses.replace(r, prefix_k=r.prefix_k.copy(), prefix_v=r.prefix_v.copy())
+    odd.prefix_k[1::2] = np.random.default_rng(1).standard_normal(odd.prefix_k[1::2].shape)
+    odd.prefix_v[1::2] = 0.0
+    np.testing.assert_array_equal(m.generate([odd])[0], base)
+    even = dataclasses.replace(r, prefix_k=r.prefix_k.copy(), prefix_v=r.prefix_v.copy())
+    even.prefix_v[0::2] *= -1.0
+    assert np.abs(m.generate([even])[0] - base).max() > 1e-3
 
 
 # ------------------------------------------------------------------ invariants
