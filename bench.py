@@ -46,8 +46,15 @@ def algorithmic_work(shape, reqs):
         "gemm_up": 2.0 * tok_steps * d * dff * L,
         "gemm_down": 2.0 * tok_steps * dff * d * L,
     }
-    attn_bytes = sum(r.prefix_len * r.steps for r in reqs) * L * 2 * nkv * hd * 2
-    attn_flops = sum(4.0 * nq * hd * r.horizon * (r.prefix_len + r.horizon) * r.steps for r in reqs) * L
+    if getattr(shape, "attention_layout", 0) == 1:
+        # alternating: the (L + 1) // 2 even layers read the prefix, the odd
+        # layers attend over the request's own action keys only
+        lc, ls = (L + 1) // 2, L // 2
+        attn_bytes = sum(r.prefix_len * r.steps for r in reqs) * lc * 2 * nkv * hd * 2
+        attn_flops = sum(4.0 * nq * hd * r.horizon * (lc * r.prefix_len + ls * r.horizon) * r.steps for r in reqs)
+    else:
+        attn_bytes = sum(r.prefix_len * r.steps for r in reqs) * L * 2 * nkv * hd * 2
+        attn_flops = sum(4.0 * nq * hd * r.horizon * (r.prefix_len + r.horizon) * r.steps for r in reqs) * L
     return w, float(attn_bytes), float(attn_flops), tok_steps
 
 
@@ -97,7 +104,11 @@ def cpu_baseline(preset, weights, reqs_meta, budget_s: float):
         sh = preset.shape
         per_tok = 2.0 * sh.n_layers * (sh.d_model * sh.qkv_dim + sh.n_q_heads * sh.head_dim * sh.d_model
                                        + 2 * sh.d_model * sh.d_mlp)
-        att = 4.0 * sh.n_layers * sh.n_q_heads * sh.head_dim * m.horizon * (m.prefix_len + m.horizon)
+        if getattr(sh, "attention_layout", 0) == 1:
+            att = 4.0 * sh.n_q_heads * sh.head_dim * m.horizon * (
+                (sh.n_layers + 1) // 2 * m.prefix_len + sh.n_layers // 2 * m.horizon)
+        else:
+            att = 4.0 * sh.n_layers * sh.n_q_heads * sh.head_dim * m.horizon * (m.prefix_len + m.horizon)
         return (per_tok * m.horizon + att) * m.steps
 
     done, t_used = [], 0.0
@@ -563,6 +574,9 @@ def main():
                     help="open-loop request arrivals served by one worker with whole-chunk batches vs "
                          "step-level batches (rosa_generate_steps); prints its own JSON line")
     ap.add_argument("--arrival-rate", type=float, default=2000.0, help="requests per second for --step-batching")
+    ap.add_argument("--attention-layout", choices=["joint", "alternating"], default="joint",
+                    help="the expert's attention layout: joint prefix + action attention in every layer, or "
+                         "alternating cross-attention (even layers) and self-attention (odd layers)")
     ap.add_argument("--prefill", action="store_true",
                     help="the prefix producer instead: a VLM backbone over 32 robots' prefixes "
                          "(prints its own JSON line)")
@@ -590,6 +604,11 @@ def main():
     from synthetic import PRESETS, make_metadata, make_requests, make_weights
 
     preset = PRESETS[args.workload]
+    workload = preset.name
+    if args.attention_layout == "alternating":
+        import dataclasses
+        preset = dataclasses.replace(preset, shape=dataclasses.replace(preset.shape, attention_layout=1))
+        workload += "_alternating"
     t0 = time.time()
     weights = make_weights(preset.shape, preset.dtype)
     meta = make_metadata(preset)
@@ -677,7 +696,7 @@ def main():
         "ms_per_step": round(ms_per_step, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": preset.name, "requests": B,
+        "config": {"workload": workload, "requests": B, "attention_layout": args.attention_layout,
                    "action_tokens": int(sum(r.horizon for r in reqs)),
                    "prefix_tokens": int(sum(r.prefix_len for r in reqs)),
                    "token_steps": int(tok_steps)},

@@ -19,7 +19,9 @@
  * (shift, scale, gate for attention and MLP); each block applies RMSNorm
  * (eps = rms_eps, no learned gain) modulated as norm*(1+scale)+shift,
  * grouped-query attention of the action tokens over [own prefix keys ; own
- * action keys] with scale 1/sqrt(head_dim), a gated residual, then the same
+ * action keys] (or, in the alternating layout, over the prefix keys in even
+ * layers and the action keys in odd layers) with scale 1/sqrt(head_dim), a
+ * gated residual, then the same
  * around a tanh-GELU MLP; a final modulated RMSNorm and an output projection
  * with bias give v.  The paper does not spell out these layers; the library
  * follows the readings above, which its CPU oracle states one by one.
@@ -60,9 +62,23 @@ typedef enum rosa_dtype {
   ROSA_FP32 = 1    /* everything fp32 (debug mode, for tight parity checks) */
 } rosa_dtype;
 
+/* Attention layout of the action expert's blocks.
+ *  ROSA_ATTN_JOINT: every layer attends over [own prefix keys ; own action
+ *    keys] (a pi0-style expert sharing the VLM's attention).
+ *  ROSA_ATTN_ALTERNATING: a DiT head that interleaves cross-attention to the
+ *    VLM context with self-attention (GR00T-style, Sec. 2.2.1): even layers
+ *    attend over the request's prefix keys only, odd layers over its own
+ *    action keys only.  Every request needs prefix_len >= 1; the prefix cache
+ *    keeps the [L][P][n_kv][hd] layout and odd layers' entries are not read. */
+typedef enum rosa_attention_layout {
+  ROSA_ATTN_JOINT = 0,
+  ROSA_ATTN_ALTERNATING = 1
+} rosa_attention_layout;
+
 /* Model shape.  Constraints (else ROSA_E_UNSUPPORTED): n_q_heads % n_kv_heads == 0;
  * head_dim in {32, 64, 128, 256}; d_model, d_mlp and n_q_heads*head_dim multiples
- * of 128; d_model <= 4096; 1 <= action_dim <= 64; time_emb_dim even and <= 8192. */
+ * of 128; d_model <= 4096; 1 <= action_dim <= 64; time_emb_dim even and <= 8192.
+ * attention_layout is a rosa_attention_layout (else ROSA_E_INVALID). */
 typedef struct rosa_model_config {
   int32_t n_layers;
   int32_t d_model;
@@ -74,6 +90,7 @@ typedef struct rosa_model_config {
   int32_t time_emb_dim;
   float   rms_eps;
   int32_t dtype;           /* rosa_dtype */
+  int32_t attention_layout;  /* rosa_attention_layout */
 } rosa_model_config;
 
 /* Weights: HOST float32 arrays, row-major [in][out] (y = x W), L = n_layers,
@@ -124,7 +141,7 @@ typedef struct rosa_request {
   const void  *prefix_v;
   const float *noise;
   float       *actions;
-  int32_t      prefix_len;    /* P >= 0 */
+  int32_t      prefix_len;    /* P >= 0 (>= 1 with ROSA_ATTN_ALTERNATING) */
   int32_t      horizon;       /* 1 <= H <= max_horizon */
   int32_t      num_steps;     /* 1 <= K <= max_steps; dt = 1/K, tau_k = k/K */
   int32_t      start_step;    /* 0 <= start_step < K */

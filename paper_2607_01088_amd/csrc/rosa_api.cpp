@@ -116,10 +116,20 @@ struct Plan {
   std::vector<int32_t> n_active;     // per step
   std::vector<float> taus;
   std::vector<int32_t> tau_idx;      // [max_K][n]
-  std::vector<AttnItem> items;
-  std::vector<AttnGroup> groups;
-  std::vector<int32_t> items_upto;   // items of plan requests [0, r]
-  std::vector<int32_t> groups_upto;
+  // Attention work: set 0 serves joint (or, alternating, cross-attention)
+  // layers, set 1 the self-attention layers of the alternating layout.  The
+  // device holds set 0's items then set 1's (likewise groups); launch orders
+  // index the whole item array; partial slots are numbered across both sets.
+  struct AttnSet {
+    std::vector<AttnItem> items;
+    std::vector<AttnGroup> groups;
+    std::vector<int32_t> items_upto;   // items of plan requests [0, r]
+    std::vector<int32_t> groups_upto;
+    int item_base = 0, group_base = 0;
+  };
+  AttnSet sets[2];
+  int n_sets = 1;
+  int slots = 0;
   int M0 = 0, Kmax = 0;
   // Lanes: disjoint request sets run as independent sub-batches on their own
   // streams.  Lane l owns plan positions [req_lo, req_hi) and stacked rows
@@ -128,9 +138,9 @@ struct Plan {
   struct Lane {
     int req_lo = 0, req_hi = 0, row_lo = 0, row_hi = 0;
     std::vector<int32_t> n_act, m;
-    // Per step: offset of the attention launch order in attn_lists, and the
-    // launch's block count (8 x the longest per-XCD item list).
-    std::vector<int32_t> list_at, list_blocks;
+    // Per attention set and step: offset of the attention launch order in
+    // attn_lists, and the launch's block count (8 x the longest per-XCD item list).
+    std::vector<int32_t> list_at[2], list_blocks[2];
   };
   std::vector<Lane> lanes;
   // Attention launch orders, one per distinct set of active requests of a
@@ -170,7 +180,8 @@ struct rosa_batch {
   int32_t *row_req = nullptr, *rowmod = nullptr, *ident = nullptr;
   float *modtab = nullptr, *emb = nullptr, *tc1 = nullptr, *tc2 = nullptr, *gemv_ws = nullptr;
   float *part_o = nullptr, *part_ml = nullptr;
-  int max_items = 0;
+  int max_items = 0;                 // attention work items per call, both sets
+  int max_slots = 0;                 // partial-result slots per call, both sets
 
 
   // plan buffers: device region + two pinned host staging copies
@@ -218,6 +229,7 @@ rosa_status check_config(const rosa_model_config *c) {
       c->d_mlp < 1 || c->action_dim < 1 || c->time_emb_dim < 2 || !(c->rms_eps >= 0.f))
     return ROSA_E_INVALID;
   if (c->dtype != ROSA_BF16 && c->dtype != ROSA_FP32) return ROSA_E_INVALID;
+  if (c->attention_layout != ROSA_ATTN_JOINT && c->attention_layout != ROSA_ATTN_ALTERNATING) return ROSA_E_INVALID;
   if (c->n_q_heads % c->n_kv_heads != 0) return ROSA_E_UNSUPPORTED;
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
     return ROSA_E_UNSUPPORTED;
@@ -251,6 +263,12 @@ Dims make_dims(const rosa_model_config *c) {
 int attn_query_blocks(int R, int per) { return ((R + 31) / 32 + per - 1) / per; }
 int attn_groups_per_block(const rosa_model_config *cfg) { return 4 * attn_groups_per_wave(cfg->head_dim); }
 
+// Attention set of a layer: 0 for joint layers and the alternating layout's
+// cross-attention (even) layers, 1 for its self-attention (odd) layers.
+int attn_set_of(const rosa_model_config *cfg, int layer) {
+  return cfg->attention_layout == ROSA_ATTN_ALTERNATING && (layer & 1) ? 1 : 0;
+}
+
 // Validation of a request set (all-or-nothing) and the batch plan.
 rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
                        int n, bool sort_by_steps, bool allow_split, int lanes_wanted, Plan &p, std::string &err,
@@ -277,6 +295,10 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
     }
     if ((r.start_step == 0 && !r.noise) || !r.actions || (r.prefix_len > 0 && (!r.prefix_k || !r.prefix_v))) {
       snprintf(buf, sizeof buf, "request %d: NULL pointer", i); err = buf; return ROSA_E_INVALID;
+    }
+    if (cfg->attention_layout == ROSA_ATTN_ALTERNATING && r.prefix_len < 1) {
+      snprintf(buf, sizeof buf, "request %d: the alternating layout needs a prefix (P >= 1)", i);
+      err = buf; return ROSA_E_INVALID;
     }
     sumH += r.horizon;
     sumP += r.prefix_len;
@@ -366,69 +388,89 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   }
 
   // Attention work items: per request and KV head, its query rows in blocks of
-  // at most kAttnQB rows (32-row groups spread evenly over the blocks); keys
-  // split over several items only when the batch is too small to fill the GPU.
+  // at most kAttnQB rows (32-row groups spread evenly over the blocks), over
+  // the set's key range of the request's key sequence [prefix ; actions]:
+  // set 0 all of it (joint) or the prefix (alternating), set 1 the actions.
+  // Keys are split over several items only when the batch is too small to
+  // fill the GPU.
   const int G = cfg->n_q_heads / cfg->n_kv_heads;
-  int64_t total_qb = 0;
   const int gpb = attn_groups_per_block(cfg);
+  const bool alternating = cfg->attention_layout == ROSA_ATTN_ALTERNATING;
+  p.n_sets = alternating ? 2 : 1;
+  int64_t total_qb = 0;
   for (int i = 0; i < n; ++i) total_qb += (int64_t)cfg->n_kv_heads * attn_query_blocks(reqs[i].horizon * G, gpb);
   const bool split = allow_split && total_qb > 0 && total_qb < kSplitTarget;
-  int slots = 0;
-  p.items_upto.resize(n);
-  p.groups_upto.resize(n);
-  for (int i = 0; i < n; ++i) {
-    const rosa_request &r = reqs[p.order[i]];
-    const int nk = r.prefix_len + r.horizon;
-    const int R = r.horizon * G, ngrp = (R + 31) / 32, nqb = attn_query_blocks(R, gpb);
-    int nsplit = 1, chunk = nk;
-    if (split) {
-      const int want = (int)((kSplitTarget + total_qb - 1) / total_qb);
-      const int most = std::max(1, (nk + kMinSplitKeys - 1) / kMinSplitKeys);
-      nsplit = std::min(want, most);
-      chunk = (nk + nsplit - 1) / nsplit;
-      chunk = (chunk + 63) / 64 * 64;          // whole 64-key tiles per item
-      nsplit = (nk + chunk - 1) / chunk;
-    }
-    for (int kvh = 0; kvh < cfg->n_kv_heads; ++kvh)
-      for (int qb = 0; qb < nqb; ++qb) {
-        const int q0 = 32 * (qb * ngrp / nqb);
-        const int nq = std::min(R, 32 * ((qb + 1) * ngrp / nqb)) - q0;
-        if (nsplit > 1) {
-          AttnGroup gr{i, kvh, q0, nq, slots, nsplit, 0, 0};
-          p.groups.push_back(gr);
-        }
-        for (int c = 0; c < nsplit; ++c) {
-          AttnItem it{};
-          it.pk = r.prefix_k; it.pv = r.prefix_v; it.P = r.prefix_len; it.tok_off = p.tok_off[i];
-          it.req = i; it.kvh = kvh; it.q0 = q0; it.nq = nq;
-          it.kbeg = c * chunk;
-          it.kend = std::min(nk, (c + 1) * chunk);
-          it.slot = nsplit > 1 ? slots++ : -1;
-          p.items.push_back(it);
-        }
+  for (int v = 0; v < p.n_sets; ++v) {
+    Plan::AttnSet &S = p.sets[v];
+    if (v == 1) { S.item_base = (int)p.sets[0].items.size(); S.group_base = (int)p.sets[0].groups.size(); }
+    S.items_upto.resize(n);
+    S.groups_upto.resize(n);
+    for (int i = 0; i < n; ++i) {
+      const rosa_request &r = reqs[p.order[i]];
+      const int key_lo = v == 1 ? r.prefix_len : 0;
+      const int key_hi = alternating && v == 0 ? r.prefix_len : r.prefix_len + r.horizon;
+      const int nk = key_hi - key_lo;
+      const int R = r.horizon * G, ngrp = (R + 31) / 32, nqb = attn_query_blocks(R, gpb);
+      int nsplit = 1, chunk = nk;
+      if (split) {
+        const int want = (int)((kSplitTarget + total_qb - 1) / total_qb);
+        const int most = std::max(1, (nk + kMinSplitKeys - 1) / kMinSplitKeys);
+        nsplit = std::min(want, most);
+        chunk = (nk + nsplit - 1) / nsplit;
+        chunk = (chunk + 63) / 64 * 64;          // whole 64-key tiles per item
+        nsplit = (nk + chunk - 1) / chunk;
       }
-    p.items_upto[i] = (int)p.items.size();
-    p.groups_upto[i] = (int)p.groups.size();
-  }
-  if (slots > kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
-
-  // Attention launch orders, one per distinct set of active requests of a lane.
-  for (Plan::Lane &ln : p.lanes) {
-    ln.list_at.assign(p.Kmax, -1);
-    ln.list_blocks.assign(p.Kmax, 0);
-    int prev_n = -1;
-    for (int k = 0; k < p.Kmax; ++k) {
-      const int na = ln.n_act[k];
-      if (na == 0) continue;
-      if (na == prev_n) { ln.list_at[k] = ln.list_at[k - 1]; ln.list_blocks[k] = ln.list_blocks[k - 1]; continue; }
-      prev_n = na;
-      std::vector<std::pair<int, int>> ranges;
-      for (int i = ln.req_lo; i < ln.req_lo + na; ++i)
-        ranges.push_back({i > 0 ? p.items_upto[i - 1] : 0, p.items_upto[i]});
-      ln.list_at[k] = (int)p.attn_lists.size();
-      ln.list_blocks[k] = attn_launch_order(p.items, ranges, p.attn_lists);
+      for (int kvh = 0; kvh < cfg->n_kv_heads; ++kvh)
+        for (int qb = 0; qb < nqb; ++qb) {
+          const int q0 = 32 * (qb * ngrp / nqb);
+          const int nq = std::min(R, 32 * ((qb + 1) * ngrp / nqb)) - q0;
+          if (nsplit > 1) {
+            AttnGroup gr{i, kvh, q0, nq, p.slots, nsplit, 0, 0};
+            S.groups.push_back(gr);
+          }
+          for (int c = 0; c < nsplit; ++c) {
+            AttnItem it{};
+            it.pk = r.prefix_k; it.pv = r.prefix_v; it.P = r.prefix_len; it.tok_off = p.tok_off[i];
+            it.req = i; it.kvh = kvh; it.q0 = q0; it.nq = nq;
+            it.kbeg = key_lo + c * chunk;
+            it.kend = std::min(key_hi, key_lo + (c + 1) * chunk);
+            it.slot = nsplit > 1 ? p.slots++ : -1;
+            S.items.push_back(it);
+          }
+        }
+      S.items_upto[i] = (int)S.items.size();
+      S.groups_upto[i] = (int)S.groups.size();
     }
   }
+  if (p.slots > p.n_sets * kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
+
+  // Attention launch orders, one per set and distinct set of active requests
+  // of a lane; entries index the whole device item array.
+  for (Plan::Lane &ln : p.lanes)
+    for (int v = 0; v < p.n_sets; ++v) {
+      const Plan::AttnSet &S = p.sets[v];
+      ln.list_at[v].assign(p.Kmax, -1);
+      ln.list_blocks[v].assign(p.Kmax, 0);
+      int prev_n = -1;
+      for (int k = 0; k < p.Kmax; ++k) {
+        const int na = ln.n_act[k];
+        if (na == 0) continue;
+        if (na == prev_n) {
+          ln.list_at[v][k] = ln.list_at[v][k - 1];
+          ln.list_blocks[v][k] = ln.list_blocks[v][k - 1];
+          continue;
+        }
+        prev_n = na;
+        std::vector<std::pair<int, int>> ranges;
+        for (int i = ln.req_lo; i < ln.req_lo + na; ++i)
+          ranges.push_back({i > 0 ? S.items_upto[i - 1] : 0, S.items_upto[i]});
+        const size_t at = p.attn_lists.size();
+        ln.list_at[v][k] = (int)at;
+        ln.list_blocks[v][k] = attn_launch_order(S.items, ranges, p.attn_lists);
+        for (size_t e = at; e < p.attn_lists.size(); ++e)
+          if (p.attn_lists[e] >= 0) p.attn_lists[e] += S.item_base;
+      }
+    }
   return ROSA_OK;
 }
 
@@ -492,8 +534,9 @@ hipError_t harvest_profile(rosa_batch *b) {
 
 // Copy the plan through a pinned staging buffer into the device plan region.
 hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, int n) {
-  if ((int64_t)p.items.size() > b->max_items || (int64_t)p.groups.size() > kMaxSlots ||
-      p.attn_lists.size() > b->max_list_ints)
+  const Plan::AttnSet &S0 = p.sets[0], &S1 = p.sets[1];
+  const size_t n_items = S0.items.size() + S1.items.size(), n_groups = S0.groups.size() + S1.groups.size();
+  if ((int64_t)n_items > b->max_items || (int64_t)n_groups > b->max_slots || p.attn_lists.size() > b->max_list_ints)
     return hipErrorInvalidValue;
   const int slot = b->plan_flip;
   b->plan_flip ^= 1;
@@ -513,8 +556,11 @@ hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, i
   }
   std::memcpy(hp + b->off_tau_idx, p.tau_idx.data(), p.tau_idx.size() * 4);
   std::memcpy(hp + b->off_taus, p.taus.data(), p.taus.size() * 4);
-  std::memcpy(hp + b->off_items, p.items.data(), p.items.size() * sizeof(AttnItem));
-  std::memcpy(hp + b->off_groups, p.groups.data(), p.groups.size() * sizeof(AttnGroup));
+  std::memcpy(hp + b->off_items, S0.items.data(), S0.items.size() * sizeof(AttnItem));
+  std::memcpy(hp + b->off_items + S0.items.size() * sizeof(AttnItem), S1.items.data(), S1.items.size() * sizeof(AttnItem));
+  std::memcpy(hp + b->off_groups, S0.groups.data(), S0.groups.size() * sizeof(AttnGroup));
+  std::memcpy(hp + b->off_groups + S0.groups.size() * sizeof(AttnGroup), S1.groups.data(),
+              S1.groups.size() * sizeof(AttnGroup));
   std::memcpy(hp + b->off_lists, p.attn_lists.data(), p.attn_lists.size() * 4);
   const size_t used = b->off_lists + p.attn_lists.size() * 4;
   hipError_t e = hipMemcpyAsync(b->d_plan, hp, used, hipMemcpyHostToDevice, b->stream);
@@ -547,14 +593,17 @@ hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int
   const int32_t *lists = (const int32_t *)((uint8_t *)b->d_plan + b->off_lists);
   const int r0 = ln.req_lo, n_act = ln.n_act[k];
   if (n_act <= 0) return hipSuccess;
-  const int it_lo = r0 > 0 ? p.items_upto[r0 - 1] : 0, it_hi = p.items_upto[r0 + n_act - 1];
-  const int gr_lo = r0 > 0 ? p.groups_upto[r0 - 1] : 0, gr_hi = p.groups_upto[r0 + n_act - 1];
+  const int v = attn_set_of(&b->cfg, layer);
+  const Plan::AttnSet &S = p.sets[v];
+  const int it_lo = S.item_base + (r0 > 0 ? S.items_upto[r0 - 1] : 0), it_hi = S.item_base + S.items_upto[r0 + n_act - 1];
+  const int gr_lo = S.group_base + (r0 > 0 ? S.groups_upto[r0 - 1] : 0);
+  const int gr_hi = S.group_base + S.groups_upto[r0 + n_act - 1];
   AttnArgs a{};
   a.items = items + it_lo; a.n_items = it_hi - it_lo;
   if (b->bf16) {   // launch order of this step's active set (indices into the whole item array)
     a.items = items;
-    a.list = lists + ln.list_at[k];
-    a.n_blocks = ln.list_blocks[k];
+    a.list = lists + ln.list_at[v][k];
+    a.n_blocks = ln.list_blocks[v][k];
   }
   a.reqs = reqs; a.layer = layer;
   a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
@@ -669,23 +718,25 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->tc1 = dalloc<float>(b, (size_t)kMaxTau * d, e);
     b->tc2 = dalloc<float>(b, (size_t)kMaxTau * d, e);
     b->gemv_ws = dalloc<float>(b, small_gemv_workspace_floats(std::max(D.mod_stride, D.d)), e);
-    b->part_o = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * D.hd, e);
-    b->part_ml = dalloc<float>(b, (size_t)kMaxSlots * kAttnQB * 2, e);
+    const int n_sets = cfg->attention_layout == ROSA_ATTN_ALTERNATING ? 2 : 1;
+    b->max_slots = n_sets * kMaxSlots;
+    b->part_o = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * D.hd, e);
+    b->part_ml = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * 2, e);
 
     // plan region
     const int G = D.nq / D.nkv;
     const int64_t qb_bound = (int64_t)D.nkv * (((int64_t)maxM * G + 127) / 128 + 2 * (int64_t)cap->max_requests);
-    b->max_items = (int)std::max<int64_t>(kMaxSlots + qb_bound, qb_bound);
+    b->max_items = (int)(n_sets * (kMaxSlots + qb_bound));
     auto align = [](size_t v) { return (v + 255) / 256 * 256; };
     b->off_reqs = 0;
     b->off_tau_idx = align(b->off_reqs + (size_t)cap->max_requests * sizeof(ReqDesc));
     b->off_taus = align(b->off_tau_idx + (size_t)cap->max_requests * cap->max_steps * 4);
     b->off_items = align(b->off_taus + kMaxTau * 4);
     b->off_groups = align(b->off_items + (size_t)b->max_items * sizeof(AttnItem));
-    b->off_lists = align(b->off_groups + (size_t)kMaxSlots * sizeof(AttnGroup));
+    b->off_lists = align(b->off_groups + (size_t)b->max_slots * sizeof(AttnGroup));
     // one launch order per step and lane at most: the lane's items plus at most
     // 7 empty slots per XCD row of blocks
-    b->max_list_ints = (size_t)cap->max_steps * (8 * (size_t)b->max_items + 8 * kMaxLanes);
+    b->max_list_ints = (size_t)cap->max_steps * (8 * (size_t)b->max_items + 8 * kMaxLanes * n_sets);
     b->plan_bytes = align(b->off_lists + b->max_list_ints * 4);
     b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
     if (e != hipSuccess) {
@@ -901,13 +952,13 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
       for (int k = 0; k < cap->max_steps; ++k) m_k[k] = k < p.Kmax ? p.m_k[k] : 0;
     if (counts) {
       counts[0] = (int32_t)p.taus.size();
-      counts[1] = (int32_t)p.items.size();
+      counts[1] = (int32_t)(p.sets[0].items.size() + p.sets[1].items.size());
       counts[2] = 0;
       for (int i = 0; i < n; ++i) {
         const int G = cfg->n_q_heads / cfg->n_kv_heads;
         counts[2] += cfg->n_kv_heads * attn_query_blocks(reqs[i].horizon * G, attn_groups_per_block(cfg));
       }
-      counts[3] = (int32_t)p.groups.size();
+      counts[3] = (int32_t)(p.sets[0].groups.size() + p.sets[1].groups.size());
     }
     return ROSA_OK;
   } catch (...) {

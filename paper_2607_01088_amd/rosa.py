@@ -24,7 +24,7 @@ class ModelConfig(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_mlp", C.c_int32),
                 ("action_dim", C.c_int32), ("time_emb_dim", C.c_int32), ("rms_eps", C.c_float),
-                ("dtype", C.c_int32)]
+                ("dtype", C.c_int32), ("attention_layout", C.c_int32)]
 
 
 _WEIGHT_FIELDS = ["w_in", "b_in", "w_t1", "b_t1", "w_t2", "b_t2", "w_mod", "b_mod", "w_qkv", "w_o",
@@ -190,7 +190,7 @@ def load(path: Optional[str] = None) -> C.CDLL:
 def model_config(shape, dtype: str) -> ModelConfig:
     return ModelConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
                        shape.d_mlp, shape.action_dim, shape.time_emb_dim, shape.rms_eps,
-                       ROSA_BF16 if dtype == "bf16" else ROSA_FP32)
+                       ROSA_BF16 if dtype == "bf16" else ROSA_FP32, getattr(shape, "attention_layout", 0))
 
 
 def capacity(max_requests: int, max_horizon: int, max_action_tokens: int, max_steps: int,

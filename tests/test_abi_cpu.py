@@ -133,3 +133,34 @@ def test_plan_too_many_distinct_taus():
     cap = rosa.capacity(64, 8, 512, 64, 1000)
     reqs = [req(1, 1, K) for K in range(40, 64)]
     assert _plan(reqs, cap, shape=TINY_SHAPE)[0] == rosa.ROSA_E_CAPACITY
+
+
+def test_plan_alternating_layout():
+    # Two attention sets: cross-attention items over the prefix and
+    # self-attention items over the actions, each one item per query block at
+    # this batch size; a request without a prefix is rejected.
+    from synthetic import PI0_ALT_SHAPE
+    reqs = [req(600, 50, 10) for _ in range(160)]
+    cap = rosa.capacity(256, 50, 256 * 50, 10, 256 * 2048)
+    st, _, _, _, counts = _plan(reqs, cap, shape=PI0_ALT_SHAPE)
+    assert st == rosa.ROSA_OK
+    assert counts[2] == 640 and counts[1] == 2 * 640 and counts[3] == 0
+    st, *_ = _plan([req(5, 8, 5), req(0, 8, 5, k=None, v=None)], shape=PI0_ALT_SHAPE)
+    assert st == rosa.ROSA_E_INVALID
+    # small batch: the prefix keys split over items (partial slots), the
+    # self-attention keys (H <= 256) never do
+    st, _, _, _, counts = _plan([req(1200, 50, 10)], shape=PI0_ALT_SHAPE)
+    assert st == rosa.ROSA_OK
+    assert counts[3] == counts[2] and counts[1] > 2 * counts[2]
+
+
+def test_create_rejects_unknown_layout():
+    lib = rosa.load()
+    h = C.c_void_p()
+    cfg = rosa.model_config(TINY_SHAPE, "fp32")
+    cfg.attention_layout = 2
+    cap = rosa.capacity(2, 8, 16, 4, 200)
+    w = rosa.Weights()      # NULL weights would be rejected later, with another message
+    assert lib.rosa_batch_create(C.byref(cfg), C.byref(w), C.byref(cap), None, C.byref(h)) == rosa.ROSA_E_INVALID
+    assert not h.value
+    assert b"configuration" in lib.rosa_last_error(None)
