@@ -64,10 +64,10 @@ def kernel_source_hash(name: str) -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_traffic(name: str, launches_per_call: float):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel source."""
-    path = os.path.join(PROFILES, f"traffic_{name}_factory_b256.json")
+def load_traffic(name: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary of this
+    kernel on this workload, if it was taken on the current kernel source."""
+    path = os.path.join(PROFILES, f"traffic_{name}_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -681,7 +681,7 @@ def main():
     d = kernels[dom]
     roofline = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 2), "peak": d["peak"],
                 "unit": d["unit"], "frac": round(d["frac"], 4),
-                "traffic": load_traffic(dom, d["launches_per_call"])}
+                "traffic": load_traffic(dom, workload)}
     gemm_total_ms = sum(kernels[k]["ms_per_call"] for k in gemm_flops if k in kernels)
     gemm_all = sum(gemm_flops.values()) / (gemm_total_ms * 1e-3) / 1e12
 

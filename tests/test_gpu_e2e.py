@@ -120,6 +120,25 @@ def test_factory_b256_full_batch_sampled(pi0_expert):
     _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "factory_b256")
 
 
+@pytest.mark.timeout(900)
+def test_stress_b512_full_batch_sampled():
+    """The largest preset: 512 requests with 1024-2048-token prefixes (14.5 GB
+    of prefix KV resident) in one call; the longest and shortest prefix and
+    one more request against the oracle, every result finite."""
+    w = cached_weights(PI0_SHAPE, "bf16")
+    p = PRESETS["stress_b512"]
+    meta = make_metadata(p)
+    e = _expert(PI0_SHAPE, "bf16", w, max_requests=512, max_prefix=sum(m.prefix_len for m in meta))
+    reqs = make_requests(p, threads=16)
+    got, db = _run(e, reqs, "bf16")
+    del db
+    pick = sorted({int(np.argmax([m.prefix_len for m in meta])), int(np.argmin([m.prefix_len for m in meta])), 300})
+    for g in got:
+        assert np.isfinite(g).all()
+    _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "stress_b512")
+    e.close()
+
+
 # ------------------------------------------------------------------ attention must be visible
 
 def _attention_isolating(w, shape):
