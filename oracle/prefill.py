@@ -20,10 +20,16 @@ Plain NumPy float64, one request at a time, one layer at a time; matrix
 products and the pinned attention, RMSNorm and GELU of ``rosa_oracle`` are
 its only steps.
 
+A second cache form serves an action head that cross-attends to the
+backbone's output instead (a GR00T-style DiT head): ``prefill_context`` runs
+every backbone layer, RMS-normalises the final hidden state and projects it
+with each head layer's own context weights into that layer's K and V.
+
 Pins (tests marked ``not gpu``): a scalar brute force on nested lists for a
-tiny backbone; with the residual branches zeroed every layer's cache is the
-closed form RMSNorm(x) W_k, W_v of that layer; permuting the prefix tokens
-permutes the cache rows (no causal mask, no positions).
+tiny backbone (both cache forms); with the residual branches zeroed every
+layer's cache is the closed form RMSNorm(x) W_k, W_v of that layer (context
+form: RMSNorm(x) W_ctx[e]); permuting the prefix tokens permutes the cache
+rows (no causal mask, no positions).
 """
 from __future__ import annotations
 
@@ -54,4 +60,32 @@ def prefill(x: np.ndarray, w: Dict[str, np.ndarray], shape) -> Tuple[np.ndarray,
         h = h + o.reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
         u = rms_norm(h, eps)
         h = h + gelu_tanh(u @ np.asarray(w["w_up"][l], dtype=F)) @ np.asarray(w["w_down"][l], dtype=F)
+    return K, V
+
+
+def prefill_context(x: np.ndarray, w: Dict[str, np.ndarray], shape, w_ctx: np.ndarray
+                    ) -> Tuple[np.ndarray, np.ndarray]:
+    """Context caches (K, V), each [L_e][P][n_kv][hd] float64, for an action
+    head that cross-attends to the backbone's output (the GR00T-style head):
+    every backbone layer runs in full, the final hidden state is RMS-normalised
+    (no gain), and action-head layer e projects it with its own context
+    weights w_ctx[e] ([d][2 n_kv hd], K columns then V)."""
+    L, nq, nkv, hd, eps = shape.n_layers, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.rms_eps
+    P = x.shape[0]
+    h = np.asarray(x, dtype=F).copy()
+    for l in range(L):
+        qkv = rms_norm(h, eps) @ np.asarray(w["w_qkv"][l], dtype=F)
+        q = qkv[:, :nq * hd].reshape(P, nq, hd)
+        k = qkv[:, nq * hd:(nq + nkv) * hd].reshape(P, nkv, hd)
+        v = qkv[:, (nq + nkv) * hd:].reshape(P, nkv, hd)
+        h = h + attention(q, k, v).reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
+        h = h + gelu_tanh(rms_norm(h, eps) @ np.asarray(w["w_up"][l], dtype=F)) @ np.asarray(w["w_down"][l], dtype=F)
+    u = rms_norm(h, eps)
+    Le = w_ctx.shape[0]
+    K = np.zeros((Le, P, nkv, hd), dtype=F)
+    V = np.zeros((Le, P, nkv, hd), dtype=F)
+    for e in range(Le):
+        kv = u @ np.asarray(w_ctx[e], dtype=F)
+        K[e] = kv[:, :nkv * hd].reshape(P, nkv, hd)
+        V[e] = kv[:, nkv * hd:].reshape(P, nkv, hd)
     return K, V

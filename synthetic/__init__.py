@@ -40,7 +40,7 @@ __all__ = [
     "TINY_SHAPE", "PI0_SHAPE", "TINY_ALT_SHAPE", "PI0_ALT_SHAPE", "bf16_round", "bf16_bits", "bits_to_f32",
     "make_weights", "make_metadata", "make_request", "make_requests",
     "weight_shapes", "VlmShape", "TINY_VLM", "PI0_VLM", "VLM_WEIGHT_ORDER", "vlm_weight_shapes",
-    "make_vlm_weights", "make_prefix_embeddings", "prefill_lengths",
+    "make_vlm_weights", "make_prefix_embeddings", "prefill_lengths", "make_context_weights",
 ]
 
 
@@ -324,3 +324,15 @@ def prefill_lengths(n_jobs: int = 32, lo: int = 600, hi: int = 1024, seed: int =
     instruction (600..1024 tokens, as the pi0_b32 preset)."""
     rng = np.random.default_rng(seed)
     return [int(p) for p in rng.integers(lo, hi + 1, size=n_jobs)]
+
+
+def make_context_weights(shape: VlmShape, head_layers: int, dtype: str = "bf16", seed: int = 2,
+                         std: float = 0.02) -> np.ndarray:
+    """Context projection weights of a cross-attending action head:
+    [head_layers][d][2 n_kv hd] (K columns, then V), N(0, std^2) from the
+    weights child of SeedSequence(seed); bf16-representable in bf16 mode."""
+    wss, _, _ = _children(seed, 0)
+    rng = np.random.Generator(np.random.PCG64(wss))
+    w = rng.standard_normal((head_layers, shape.d_model, 2 * shape.n_kv_heads * shape.head_dim), dtype=np.float32)
+    w *= np.float32(std)
+    return bf16_round(w) if dtype == "bf16" else w

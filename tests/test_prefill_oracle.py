@@ -4,8 +4,8 @@ import math
 
 import numpy as np
 
-from oracle import prefill
-from synthetic import TINY_VLM, VlmShape, make_prefix_embeddings, make_vlm_weights
+from oracle import prefill, prefill_context
+from synthetic import TINY_VLM, VlmShape, make_context_weights, make_prefix_embeddings, make_vlm_weights
 
 SMALL = VlmShape(n_layers=2, d_model=8, n_q_heads=4, n_kv_heads=2, head_dim=4, d_mlp=12)
 
@@ -50,7 +50,7 @@ def _brute_prefill(x, w, s):
             gl = [0.5 * z * (1.0 + math.tanh(math.sqrt(2.0 / math.pi) * (z + 0.044715 * z ** 3))) for z in up]
             new.append([a + b for a, b in zip(hr, matvec(gl, w["w_down"][l]))])
         h = new
-    return np.array(Ks), np.array(Vs)
+    return np.array(Ks), np.array(Vs), h
 
 
 def test_prefill_matches_scalar_bruteforce():
@@ -58,7 +58,7 @@ def test_prefill_matches_scalar_bruteforce():
     w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL, "fp32").items()}
     x = rng.standard_normal((5, SMALL.d_model))
     K, V = prefill(x, w, SMALL)
-    Kb, Vb = _brute_prefill(x, w, SMALL)
+    Kb, Vb, _ = _brute_prefill(x, w, SMALL)
     np.testing.assert_allclose(K, Kb, rtol=0, atol=1e-11)
     np.testing.assert_allclose(V, Vb, rtol=0, atol=1e-11)
 
@@ -85,3 +85,41 @@ def test_token_permutation_permutes_the_cache():
     Kp, Vp = prefill(x[perm], w, TINY_VLM)
     np.testing.assert_allclose(Kp, K[:, perm], rtol=1e-12, atol=1e-13)
     np.testing.assert_allclose(Vp, V[:, perm], rtol=1e-12, atol=1e-13)
+
+
+def test_context_form_matches_scalar_bruteforce():
+    rng = np.random.default_rng(1)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL, "fp32").items()}
+    wc = rng.standard_normal((3, SMALL.d_model, 2 * SMALL.n_kv_heads * SMALL.head_dim)) * 0.5
+    x = rng.standard_normal((4, SMALL.d_model))
+    K, V = prefill_context(x, w, SMALL, wc)
+    _, _, h = _brute_prefill(x, w, SMALL)
+    kvw = SMALL.n_kv_heads * SMALL.head_dim
+    for e in range(3):
+        for t in range(4):
+            ms = sum(z * z for z in h[t]) / len(h[t])
+            u = [z / math.sqrt(ms + SMALL.rms_eps) for z in h[t]]
+            kv = [sum(u[i] * wc[e][i][j] for i in range(len(u))) for j in range(2 * kvw)]
+            np.testing.assert_allclose(K[e, t].reshape(-1), kv[:kvw], rtol=0, atol=1e-11)
+            np.testing.assert_allclose(V[e, t].reshape(-1), kv[kvw:], rtol=0, atol=1e-11)
+
+
+def test_context_form_zero_residual_closed_form_and_permutation():
+    w = make_vlm_weights(TINY_VLM, "fp32", seed=4)
+    wc = make_context_weights(TINY_VLM, 3, "fp32")
+    x = make_prefix_embeddings(TINY_VLM, 9, "fp32", seed=5).astype(np.float64)
+    z = {k: v.copy() for k, v in w.items()}
+    z["w_o"][:] = 0.0
+    z["w_down"][:] = 0.0
+    K, V = prefill_context(x, z, TINY_VLM, wc)
+    kvw = TINY_VLM.n_kv_heads * TINY_VLM.head_dim
+    u = x / np.sqrt((x * x).mean(axis=1, keepdims=True) + TINY_VLM.rms_eps)
+    for e in range(3):
+        kv = u @ wc[e].astype(np.float64)
+        np.testing.assert_allclose(K[e].reshape(9, kvw), kv[:, :kvw], rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(V[e].reshape(9, kvw), kv[:, kvw:], rtol=1e-12, atol=1e-13)
+    perm = np.random.default_rng(9).permutation(9)
+    K1, V1 = prefill_context(x, w, TINY_VLM, wc)
+    Kp, Vp = prefill_context(x[perm], w, TINY_VLM, wc)
+    np.testing.assert_allclose(Kp, K1[:, perm], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Vp, V1[:, perm], rtol=1e-12, atol=1e-13)
