@@ -428,27 +428,31 @@ def step_batching(torch, rosa, expert, db, reqs, preset, args, n_req=1024, seed=
                       "clock": "virtual: advanced by each call's measured duration"}), flush=True)
 
 
-def prefill_work(shape, lens):
-    """Algorithmic flops of one prefix-producer call by kernel class.  Every
-    layer's QKV projection; the attention, output projection and MLP of all
-    layers but the last (its caches need only its K and V).  Attention:
-    4 * n_q * hd * P^2 per job and layer (QK^T and PV)."""
-    L, d, nq, hd, dff = shape.n_layers, shape.d_model, shape.n_q_heads, shape.head_dim, shape.d_mlp
+def prefill_work(shape, lens, head_layers: int = 0):
+    """Algorithmic flops of one prefix-producer call by kernel class.  Per-layer
+    form: every layer's QKV projection; the attention, output projection and
+    MLP of all layers but the last (its caches need only its K and V).
+    Context form (head_layers > 0): every layer in full, plus the context
+    projection for every head layer (counted with the QKV class, the same
+    kernel class).  Attention: 4 * n_q * hd * P^2 per job and layer."""
+    L, d, nq, nkv, hd, dff = (shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                              shape.d_mlp)
     M = float(sum(lens))
+    Lb = L if head_layers else L - 1
     return {
-        "gemm_qkv": 2.0 * M * d * shape.qkv_dim * L,
-        "gemm_o": 2.0 * M * nq * hd * d * (L - 1),
-        "gemm_up": 2.0 * M * d * dff * (L - 1),
-        "gemm_down": 2.0 * M * dff * d * (L - 1),
-        "attention": 4.0 * nq * hd * sum(float(P) * P for P in lens) * (L - 1),
+        "gemm_qkv": 2.0 * M * d * shape.qkv_dim * L + 2.0 * M * d * head_layers * 2 * nkv * hd,
+        "gemm_o": 2.0 * M * nq * hd * d * Lb,
+        "gemm_up": 2.0 * M * d * dff * Lb,
+        "gemm_down": 2.0 * M * dff * d * Lb,
+        "attention": 4.0 * nq * hd * sum(float(P) * P for P in lens) * Lb,
     }
 
 
-def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float):
+def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float, wctx=None):
     """The oracle backbone on a bounded sample: whole jobs of the batch, in
     order, until budget_s seconds have been spent; scaled to the whole batch by
     algorithmic flops (the oracle's cost is additive over jobs)."""
-    from oracle import prefill
+    from oracle import prefill, prefill_context
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -457,11 +461,15 @@ def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float):
     # the oracle runs every layer in full: 2 * (qkv + o + up + down) per token and layer, plus attention
     per_tok = 2.0 * (shape.d_model * shape.qkv_dim + shape.n_q_heads * shape.head_dim * shape.d_model
                      + 2 * shape.d_model * shape.d_mlp)
-    flops = lambda P: shape.n_layers * (per_tok * P + 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P)
+    ctx_tok = 0.0 if wctx is None else 2.0 * shape.d_model * wctx.shape[0] * wctx.shape[2]
+    flops = lambda P: shape.n_layers * (per_tok * P + 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P) + ctx_tok * P
     t_used, done = 0.0, 0
     for x in xs:
         t0 = time.perf_counter()
-        prefill(x, weights, shape)
+        if wctx is None:
+            prefill(x, weights, shape)
+        else:
+            prefill_context(x, weights, shape, wctx)
         t_used += time.perf_counter() - t0
         done += 1
         if t_used >= budget_s:
@@ -477,20 +485,24 @@ def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float):
 def prefill_bench(torch, rosa, args):
     """The prefix producer (a PaliGemma-sized VLM backbone, bf16) over one
     batch of robots' embedded prefixes; value = prefix tokens/s."""
-    from synthetic import PI0_VLM, make_prefix_embeddings, make_vlm_weights, prefill_lengths
+    from synthetic import PI0_VLM, make_context_weights, make_prefix_embeddings, make_vlm_weights, prefill_lengths
     shape = PI0_VLM
     lens = prefill_lengths()
+    context = args.prefill_cache == "context"
+    head_layers = 18
+    cache_layers = head_layers if context else shape.n_layers
     t0 = time.time()
     weights = make_vlm_weights(shape, "bf16")
+    wctx = make_context_weights(shape, head_layers, "bf16") if context else None
     xs = [make_prefix_embeddings(shape, P, "bf16", 4000 + i) for i, P in enumerate(lens)]
     print(f"[bench] generated backbone weights and {len(lens)} prefixes in {time.time() - t0:.1f} s",
           file=sys.stderr, flush=True)
     emb = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in xs]
-    kc = [torch.empty((shape.n_layers, P, shape.n_kv_heads, shape.head_dim), dtype=torch.bfloat16,
+    kc = [torch.empty((cache_layers, P, shape.n_kv_heads, shape.head_dim), dtype=torch.bfloat16,
                       device="cuda") for P in lens]
     vc = [torch.empty_like(k) for k in kc]
     jobs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(emb, kc, vc, lens)]
-    pp = rosa.PrefixProducer(shape, "bf16", weights, len(lens), sum(lens))
+    pp = rosa.PrefixProducer(shape, "bf16", weights, len(lens), sum(lens), context_weights=wctx)
     stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
         pp.run(jobs)
@@ -512,7 +524,7 @@ def prefill_bench(torch, rosa, args):
         pp.run(jobs)
     prof = pp.profile()
     pp.set_profiling(False)
-    work = prefill_work(shape, lens)
+    work = prefill_work(shape, lens, head_layers if context else 0)
     kernels = {}
     for name, (launches, ms) in prof.items():
         if launches == 0:
@@ -537,7 +549,8 @@ def prefill_bench(torch, rosa, args):
         "ms_per_step": round(ms_per_step, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "vlm_prefill_b32", "jobs": len(lens), "prefix_tokens": int(sum(lens)),
+        "config": {"workload": "vlm_prefill_b32" + ("_context" if context else ""), "jobs": len(lens),
+                   "prefix_tokens": int(sum(lens)), "cache_form": args.prefill_cache,
                    "backbone": "18 layers, width 2048, 8 query heads / 1 KV head of 256, MLP 16384"},
         "jobs_per_s": round(len(lens) * args.steps / elapsed, 2),
         "p50_ms": round(float(np.percentile(lat, 50)), 3),
@@ -551,7 +564,7 @@ def prefill_bench(torch, rosa, args):
     }
     pp.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs, lens, args.cpu_budget)
+        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs, lens, args.cpu_budget, wctx)
     print(json.dumps(out), flush=True)
 
 
@@ -580,6 +593,9 @@ def main():
     ap.add_argument("--prefill", action="store_true",
                     help="the prefix producer instead: a VLM backbone over 32 robots' prefixes "
                          "(prints its own JSON line)")
+    ap.add_argument("--prefill-cache", choices=["per_layer", "context"], default="per_layer",
+                    help="with --prefill: per-layer backbone K/V, or the context form (the backbone's "
+                         "normalised output projected for every layer of an 18-layer cross-attending head)")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="write the profiles/ summaries from rocprofv3 outputs under DIR and exit (no GPU)")
     ap.add_argument("--copy-probe", action="store_true",

@@ -35,9 +35,25 @@ extern "C" {
 
 typedef struct rosa_prefill rosa_prefill;   /* opaque handle */
 
+/* What the caches hold.
+ *  ROSA_CACHE_PER_LAYER: layer l's K and V projections of the prefix tokens
+ *    (a pi0-style expert sharing the backbone's attention; the caches have
+ *    n_layers layers).
+ *  ROSA_CACHE_CONTEXT: context K and V for an action head that cross-attends
+ *    to the backbone's output (GR00T-style, ROSA_ATTN_ALTERNATING): every
+ *    backbone layer runs in full, the final hidden state is RMS-normalised
+ *    (no gain), and head layer e projects it with w_ctx[e]; the caches have
+ *    head_layers layers. */
+typedef enum rosa_cache_form {
+  ROSA_CACHE_PER_LAYER = 0,
+  ROSA_CACHE_CONTEXT = 1
+} rosa_cache_form;
+
 /* Backbone shape.  Constraints (else ROSA_E_UNSUPPORTED): n_q_heads % n_kv_heads
  * == 0; head_dim in {32, 64, 128, 256}; d_model, d_mlp and n_q_heads*head_dim
- * multiples of 128; d_model <= 4096. */
+ * multiples of 128; d_model <= 4096.  cache_form is a rosa_cache_form and
+ * head_layers >= 1 with ROSA_CACHE_CONTEXT (ignored otherwise); else
+ * ROSA_E_INVALID. */
 typedef struct rosa_vlm_config {
   int32_t n_layers;
   int32_t d_model;
@@ -47,6 +63,8 @@ typedef struct rosa_vlm_config {
   int32_t d_mlp;
   float   rms_eps;
   int32_t dtype;           /* rosa_dtype */
+  int32_t cache_form;      /* rosa_cache_form */
+  int32_t head_layers;     /* ROSA_CACHE_CONTEXT: layers of the action head (L_e) */
 } rosa_vlm_config;
 
 /* Weights: HOST float32, row-major [in][out] (y = x W), L = n_layers, d = d_model,
@@ -57,13 +75,16 @@ typedef struct rosa_vlm_weights {
   const float *w_o;        /* [L][n_q head_dim][d] */
   const float *w_up;       /* [L][d][d_mlp] */
   const float *w_down;     /* [L][d_mlp][d] */
+  const float *w_ctx;      /* ROSA_CACHE_CONTEXT: [L_e][d][2 n_kv head_dim], K columns
+                              then V; ignored (may be NULL) otherwise */
 } rosa_vlm_weights;
 
 /* One request's prefix.  DEVICE pointers owned by the caller, valid until the
  * stream has passed the call.
  *   embeddings: [P][d] in the model dtype (read only);
- *   prefix_k, prefix_v: [L][P][n_kv][head_dim] in the model dtype, written
- *       (the layout rosa_request.prefix_k / prefix_v expects).          */
+ *   prefix_k, prefix_v: [L_c][P][n_kv][head_dim] in the model dtype, written
+ *       (the layout rosa_request.prefix_k / prefix_v expects); L_c = n_layers
+ *       (ROSA_CACHE_PER_LAYER) or head_layers (ROSA_CACHE_CONTEXT).      */
 typedef struct rosa_prefix_job {
   const void *embeddings;
   void       *prefix_k;

@@ -5,7 +5,9 @@
 // rows through the shared kernels: the plain RMSNorm is the modulated one with
 // zero shift and scale, the residual GEMM epilogue takes a gate of ones, and
 // the ragged attention runs with no cached prefix and each job's own tokens as
-// its key sequence.
+// its key sequence.  In the context form (for a head that cross-attends to the
+// backbone's output) the backbone runs in full and one more GEMM projects its
+// normalised output for every head layer.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -59,6 +61,11 @@ struct rosa_prefill {
   size_t max_list = 0;
 
   void *wt_qkv = nullptr, *wt_o = nullptr, *wt_up = nullptr, *wt_down = nullptr;  // [L][N][K]
+  // Context form: every head layer's [K | V] projection side by side,
+  // transposed ([Le * 2 n_kv hd][d]), and the projected rows [M][ctx_dim].
+  bool context = false;
+  int head_layers = 0, ctx_dim = 0;
+  void *wt_ctx = nullptr, *ctx = nullptr;
   float *h = nullptr;
   void *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr;
   int ldg = 0;                               // row stride of g: d_mlp + 64, off a power of two
@@ -169,6 +176,8 @@ rosa_status check_vlm_config(const rosa_vlm_config *c) {
     return ROSA_E_UNSUPPORTED;
   if (c->d_model % 128 || c->d_mlp % 128 || (c->n_q_heads * c->head_dim) % 128 || c->d_model > 4096)
     return ROSA_E_UNSUPPORTED;
+  if (c->cache_form != ROSA_CACHE_PER_LAYER && c->cache_form != ROSA_CACHE_CONTEXT) return ROSA_E_INVALID;
+  if (c->cache_form == ROSA_CACHE_CONTEXT && (c->head_layers < 1 || c->head_layers > 1024)) return ROSA_E_INVALID;
   return ROSA_OK;
 }
 
@@ -305,7 +314,8 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     if (st != ROSA_OK) return pfail(nullptr, st, "backbone configuration not supported");
     if (max_jobs < 1 || max_tokens < 1 || max_tokens > INT32_MAX / 2)
       return pfail(nullptr, ROSA_E_INVALID, "bad max_jobs / max_tokens");
-    if (!w->w_qkv || !w->w_o || !w->w_up || !w->w_down) return pfail(nullptr, ROSA_E_INVALID, "NULL weight pointer");
+    if (!w->w_qkv || !w->w_o || !w->w_up || !w->w_down || (cfg->cache_form == ROSA_CACHE_CONTEXT && !w->w_ctx))
+      return pfail(nullptr, ROSA_E_INVALID, "NULL weight pointer");
 
     rosa_prefill *h = new rosa_prefill();
     h->cfg = *cfg;
@@ -326,6 +336,13 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     h->wt_o = palloc<uint8_t>(h, L * d * h->o_dim * es, e);
     h->wt_up = palloc<uint8_t>(h, L * h->dff * d * es, e);
     h->wt_down = palloc<uint8_t>(h, L * d * h->dff * es, e);
+    h->context = cfg->cache_form == ROSA_CACHE_CONTEXT;
+    if (h->context) {
+      h->head_layers = cfg->head_layers;
+      h->ctx_dim = h->head_layers * 2 * h->nkv * h->hd;
+      h->wt_ctx = palloc<uint8_t>(h, (size_t)h->ctx_dim * d * es, e);
+      h->ctx = palloc<uint8_t>(h, (size_t)max_tokens * h->ctx_dim * es, e);
+    }
     h->h = palloc<float>(h, T * d, e);
     h->u = palloc<uint8_t>(h, T * d * es, e);
     h->qkv = palloc<uint8_t>(h, T * h->qkv_dim * es, e);
@@ -366,6 +383,15 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     if (e == hipSuccess) e = upload_weights_transposed(h->wt_o, w->w_o, h->L, h->o_dim, h->d, h->bf16);
     if (e == hipSuccess) e = upload_weights_transposed(h->wt_up, w->w_up, h->L, h->d, h->dff, h->bf16);
     if (e == hipSuccess) e = upload_weights_transposed(h->wt_down, w->w_down, h->L, h->dff, h->d, h->bf16);
+    if (e == hipSuccess && h->context) {
+      // [Le][d][2 kv] -> [d][Le * 2 kv], then transposed like every projection
+      const size_t kv2 = 2 * (size_t)h->nkv * h->hd;
+      std::vector<float> cat(d * (size_t)h->ctx_dim);
+      for (int l = 0; l < h->head_layers; ++l)
+        for (size_t i = 0; i < d; ++i)
+          std::memcpy(&cat[i * h->ctx_dim + l * kv2], w->w_ctx + ((size_t)l * d + i) * kv2, kv2 * 4);
+      e = upload_weights_transposed(h->wt_ctx, cat.data(), 1, h->d, h->ctx_dim, h->bf16);
+    }
     if (e == hipSuccess) {
       std::vector<float> one(d, 1.0f);
       e = hipMemcpy(h->ones, one.data(), d * 4, hipMemcpyHostToDevice);
@@ -419,12 +445,14 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       gq.M = M; gq.N = h->qkv_dim; gq.K = h->d; gq.epi = kEpiStore; gq.out = h->qkv; gq.ldo = h->qkv_dim;
       e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gq, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
-      e = ptimed(h, pcScatter, [&] {
-        return launch_prefill_kv_scatter(d_jobs, d_rows, M, h->qkv, h->qkv_dim, h->nq, h->nkv, h->hd, es, l, s);
-      });
-      // The last layer's attention and MLP feed nothing this call returns:
-      // its caches are complete once its K and V are stored.
-      if (e != hipSuccess || l == h->L - 1) break;
+      if (!h->context) {
+        e = ptimed(h, pcScatter, [&] {
+          return launch_prefill_kv_scatter(d_jobs, d_rows, M, h->qkv, h->qkv_dim, h->nq, h->nkv, h->hd, es, l, s);
+        });
+        // The last layer's attention and MLP feed nothing this call returns:
+        // its caches are complete once its K and V are stored.
+        if (e != hipSuccess || l == h->L - 1) break;
+      }
       AttnArgs a{};
       a.items = d_items; a.n_items = (int)p.items.size();
       a.list = d_list; a.n_blocks = p.n_blocks;
@@ -459,6 +487,23 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       gd.M = M; gd.N = h->d; gd.K = h->dff; gd.epi = kEpiGatedResidual; gd.out = h->h; gd.ldo = h->d;
       gd.gate = h->ones; gd.gate_stride = 0; gd.rowmod = h->rowmod;
       e = ptimed(h, pcGemmDown, [&] { return launch_gemm(gd, h->bf16, s, h->gemm_cfg); });
+    }
+    if (h->context && e == hipSuccess) {
+      // Final RMSNorm, one projection for every head layer, then each layer's
+      // [K | V] column block into the caches.
+      e = ptimed(h, pcNorm, [&] {
+        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s);
+      });
+      GemmArgs gc{};
+      gc.a = h->u; gc.lda = h->d; gc.wt = h->wt_ctx;
+      gc.M = M; gc.N = h->ctx_dim; gc.K = h->d; gc.epi = kEpiStore; gc.out = h->ctx; gc.ldo = h->ctx_dim;
+      if (e == hipSuccess) e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gc, h->bf16, s, h->gemm_cfg); });
+      const size_t kv2_bytes = 2 * (size_t)h->nkv * h->hd * es;
+      for (int l = 0; l < h->head_layers && e == hipSuccess; ++l)
+        e = ptimed(h, pcScatter, [&] {
+          return launch_prefill_kv_scatter(d_jobs, d_rows, M, (const uint8_t *)h->ctx + l * kv2_bytes, h->ctx_dim, 0,
+                                           h->nkv, h->hd, es, l, s);
+        });
     }
     if (e != hipSuccess) return pdevice_fail(h, e, "kernel launch");
     return ROSA_OK;

@@ -59,10 +59,12 @@ class S1Outcome(C.Structure):
 class VlmConfig(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_mlp", C.c_int32),
-                ("rms_eps", C.c_float), ("dtype", C.c_int32)]
+                ("rms_eps", C.c_float), ("dtype", C.c_int32), ("cache_form", C.c_int32),
+                ("head_layers", C.c_int32)]
 
 
-_VLM_WEIGHT_FIELDS = ["w_qkv", "w_o", "w_up", "w_down"]
+_VLM_WEIGHT_FIELDS = ["w_qkv", "w_o", "w_up", "w_down", "w_ctx"]
+ROSA_CACHE_PER_LAYER, ROSA_CACHE_CONTEXT = 0, 1
 
 
 class VlmWeights(C.Structure):
@@ -395,9 +397,11 @@ class ActionExpert:
             pass
 
 
-def vlm_config(shape, dtype: str) -> VlmConfig:
+def vlm_config(shape, dtype: str, head_layers: int = 0) -> VlmConfig:
+    """head_layers > 0: the context cache form for a head of that many layers."""
     return VlmConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
-                     shape.d_mlp, shape.rms_eps, ROSA_BF16 if dtype == "bf16" else ROSA_FP32)
+                     shape.d_mlp, shape.rms_eps, ROSA_BF16 if dtype == "bf16" else ROSA_FP32,
+                     ROSA_CACHE_CONTEXT if head_layers > 0 else ROSA_CACHE_PER_LAYER, head_layers)
 
 
 def prefix_job(embeddings, prefix_k, prefix_v, P: int) -> PrefixJob:
@@ -411,13 +415,18 @@ class PrefixProducer:
     """A rosa_prefill handle: the VLM backbone's weights on the GPU plus workspaces."""
 
     def __init__(self, shape, dtype: str, weights: Dict[str, np.ndarray], max_jobs: int, max_tokens: int,
-                 stream: Optional[int] = None):
+                 stream: Optional[int] = None, context_weights: Optional[np.ndarray] = None):
+        """context_weights ([L_e][d][2 n_kv hd]): the context cache form for a
+        cross-attending head of L_e layers; None: per-layer caches."""
         import torch
         self.lib = load()
         self.shape, self.dtype = shape, dtype
-        self._cfg = vlm_config(shape, dtype)
-        host = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in _VLM_WEIGHT_FIELDS}
-        w = VlmWeights(*[_f32_ptr(host[k]) for k in _VLM_WEIGHT_FIELDS])
+        head_layers = 0 if context_weights is None else int(context_weights.shape[0])
+        self._cfg = vlm_config(shape, dtype, head_layers)
+        host = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in _VLM_WEIGHT_FIELDS if k != "w_ctx"}
+        if context_weights is not None:
+            host["w_ctx"] = np.ascontiguousarray(context_weights, dtype=np.float32)
+        w = VlmWeights(*[_f32_ptr(host[k]) if k in host else None for k in _VLM_WEIGHT_FIELDS])
         if stream is None:
             stream = torch.cuda.current_stream().cuda_stream
         self.stream = stream

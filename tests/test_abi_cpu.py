@@ -164,3 +164,27 @@ def test_create_rejects_unknown_layout():
     assert lib.rosa_batch_create(C.byref(cfg), C.byref(w), C.byref(cap), None, C.byref(h)) == rosa.ROSA_E_INVALID
     assert not h.value
     assert b"configuration" in lib.rosa_last_error(None)
+
+
+def test_prefill_create_validates_before_touching_the_gpu():
+    from synthetic import TINY_VLM
+    lib = rosa.load()
+    h = C.c_void_p()
+    w = rosa.VlmWeights()
+    buf = (C.c_float * 4)()
+    for f in ("w_qkv", "w_o", "w_up", "w_down"):
+        setattr(w, f, C.cast(buf, C.POINTER(C.c_float)))
+    cases = [rosa.vlm_config(TINY_VLM, "fp32", head_layers=2),      # context form without w_ctx
+             rosa.vlm_config(TINY_VLM, "fp32")]
+    cases[1].cache_form = 5
+    bad_layers = rosa.vlm_config(TINY_VLM, "fp32", head_layers=2)
+    bad_layers.head_layers = 0
+    cases.append(bad_layers)
+    for cfg in cases:
+        assert lib.rosa_prefill_create(C.byref(cfg), C.byref(w), 1, 8, None, C.byref(h)) == rosa.ROSA_E_INVALID
+        assert not h.value and lib.rosa_prefill_last_error(None)
+    cfg = rosa.vlm_config(TINY_VLM, "fp32")
+    cfg.head_dim = 48
+    assert lib.rosa_prefill_create(C.byref(cfg), C.byref(w), 1, 8, None, C.byref(h)) == rosa.ROSA_E_UNSUPPORTED
+    assert lib.rosa_prefill_run(None, None, 0) == rosa.ROSA_E_INVALID
+    lib.rosa_prefill_destroy(None)

@@ -6,9 +6,9 @@ end to end; the full-size backbone on a sampled job; argument validation."""
 import numpy as np
 import pytest
 
-from oracle import OracleModel, prefill
-from synthetic import (PI0_VLM, TINY_SHAPE, TINY_VLM, VlmShape, custom_request, make_prefix_embeddings,
-                       make_vlm_weights, prefill_lengths)
+from oracle import OracleModel, prefill, prefill_context
+from synthetic import (PI0_VLM, TINY_ALT_SHAPE, TINY_SHAPE, TINY_VLM, VlmShape, custom_request,
+                       make_context_weights, make_prefix_embeddings, make_vlm_weights, prefill_lengths)
 from tests.helpers import cached_weights, rel_l2
 
 pytestmark = pytest.mark.gpu
@@ -48,13 +48,14 @@ def _tdtype(dtype):
 class _Jobs:
     """Embeddings on the device and NaN-filled cache buffers."""
 
-    def __init__(self, shape, dtype, lens, seed):
+    def __init__(self, shape, dtype, lens, seed, cache_layers=None):
         rosa = _rosa()
         self.lens = list(lens)
         self.x = [make_prefix_embeddings(shape, P, dtype, seed * 1000 + i) for i, P in enumerate(lens)]
         td = _tdtype(dtype)
         self.emb = [torch.from_numpy(x).to(td).cuda() for x in self.x]
-        cache = lambda P: torch.full((shape.n_layers, P, shape.n_kv_heads, shape.head_dim), float("nan"),
+        Lc = cache_layers or shape.n_layers
+        cache = lambda P: torch.full((Lc, P, shape.n_kv_heads, shape.head_dim), float("nan"),
                                      dtype=td, device="cuda")
         self.k = [cache(P) for P in lens]
         self.v = [cache(P) for P in lens]
@@ -144,6 +145,59 @@ def test_prefill_feeds_action_expert(dtype):
         ref = om.generate_chunk(r.noise, r.steps, K, V)
         err = rel_l2(out[i].cpu().numpy(), ref)
         print(f"request {i} P={lens[i]}: rel-L2 {err:.2e}", flush=True)
+        assert err <= TOL[dtype], (i, err)
+
+
+# ------------------------------------------------------------------ context form (cross-attending head)
+
+def _run_context(shape, dtype, lens, head_layers, seed):
+    rosa = _rosa()
+    w = _weights(shape, dtype)
+    wc = make_context_weights(shape, head_layers, dtype)
+    jobs = _Jobs(shape, dtype, lens, seed, cache_layers=head_layers)
+    pp = rosa.PrefixProducer(shape, dtype, w, len(lens), sum(lens), context_weights=wc)
+    pp.run(jobs.structs)
+    torch.cuda.synchronize()
+    pp.close()
+    return w, wc, jobs
+
+
+@pytest.mark.parametrize("shape,dtype,lens,head_layers", [
+    (TINY_VLM, "fp32", [1, 37, 300, 64], 2),
+    (TINY_VLM, "bf16", [1, 37, 300, 64], 3),
+    (PI0_VLM_2L, "bf16", [816, 65], 18),
+])
+def test_context_form_matches_oracle(shape, dtype, lens, head_layers):
+    w, wc, jobs = _run_context(shape, dtype, lens, head_layers, seed=6)
+    for i in range(len(lens)):
+        K, V = prefill_context(jobs.x[i], w, shape, wc)
+        gk, gv = jobs.caches(i)
+        for l in range(head_layers):
+            ek, ev = rel_l2(gk[l], K[l]), rel_l2(gv[l], V[l])
+            print(f"context job {i} P={lens[i]} head layer {l}: K {ek:.2e} V {ev:.2e}", flush=True)
+            assert ek <= TOL[dtype] and ev <= TOL[dtype], (i, l, ek, ev)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_context_form_feeds_alternating_head(dtype):
+    rosa = _rosa()
+    lens = [40, 3, 200]
+    w, wc, jobs = _run_context(TINY_VLM, dtype, lens, TINY_ALT_SHAPE.n_layers, seed=8)
+    ew = cached_weights(TINY_SHAPE, dtype)
+    reqs = [custom_request(TINY_ALT_SHAPE, dtype, 0, 8, 4, 80 + i) for i in range(len(lens))]
+    noise = [torch.from_numpy(np.ascontiguousarray(r.noise, dtype=np.float32)).cuda() for r in reqs]
+    out = [torch.full_like(n, float("nan")) for n in noise]
+    structs = [rosa.request_struct(jobs.k[i], jobs.v[i], noise[i], out[i], lens[i], r.horizon, r.steps)
+               for i, r in enumerate(reqs)]
+    e = rosa.ActionExpert(TINY_ALT_SHAPE, dtype, ew, rosa.capacity(len(reqs), 8, 8 * len(reqs), 4, sum(lens)))
+    e.generate(structs)
+    torch.cuda.synchronize()
+    e.close()
+    om = OracleModel(ew, TINY_ALT_SHAPE)
+    for i, r in enumerate(reqs):
+        K, V = prefill_context(jobs.x[i], w, TINY_VLM, wc)
+        err = rel_l2(out[i].cpu().numpy(), om.generate_chunk(r.noise, r.steps, K, V))
+        print(f"context -> alternating head, request {i} P={lens[i]}: rel-L2 {err:.2e}", flush=True)
         assert err <= TOL[dtype], (i, err)
 
 
