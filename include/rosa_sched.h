@@ -92,7 +92,8 @@ rosa_status rosa_s1_select_batch(const int32_t *batch_sizes, const double *batch
  * above the last point it is infeasible; below the first point it takes the
  * first point for b = 1 and is infeasible for b > 1 (a batch that waits for b
  * requests waits without bound as the load falls).
- * Cost: O(servers x robots x sum over b of k_max) per model and search step.
+ * Cost: O(servers x robots x sum over b of k_max) time and O(servers x
+ * robots) memory per model and search step.
  */
 
 /* Latency of one batch size at one aggregate request rate. */
@@ -135,8 +136,8 @@ typedef struct rosa_model_profile {
 } rosa_model_profile;
 
 typedef struct rosa_fleet {
-  int32_t robots;             /* |R| >= 1 */
-  int32_t servers;            /* |S| >= 1 (GPU workers, one model each) */
+  int32_t robots;             /* 1 <= |R| <= 4096 */
+  int32_t servers;            /* 1 <= |S| <= 1024 (GPU workers, one model each) */
   double  t_act_ms;           /* action execution time > 0 */
   int32_t horizon;            /* H >= 1: S1 actions per S2 plan */
   int32_t reserved;           /* must be 0 */

@@ -278,7 +278,7 @@ extern "C" rosa_status rosa_schedule_homogeneous(const rosa_fleet *fleet, const 
                                                  rosa_server_plan *servers_out) {
   if (!fleet || !models || !out || n_models < 1 || n_models > 16) return ROSA_E_INVALID;
   const rosa_fleet &F = *fleet;
-  if (F.robots < 1 || F.robots > 100000 || F.servers < 1 || F.servers > 4096 || !(F.t_act_ms > 0) ||
+  if (F.robots < 1 || F.robots > 4096 || F.servers < 1 || F.servers > 1024 || !(F.t_act_ms > 0) ||
       !std::isfinite(F.t_act_ms) || F.horizon < 1 || F.reserved != 0 || !(F.eps_hz > 0) || !std::isfinite(F.eps_hz))
     return ROSA_E_INVALID;
   for (int m = 0; m < n_models; ++m)

@@ -118,6 +118,7 @@ def test_validation():
     dup = dict(good, profile=_const(1, 10.0, 60.0) * 2)
     for models, fl in [([bad_sorted], fleet), ([dup], fleet), ([good], dict(fleet, robots=0)),
                        ([good], dict(fleet, eps_hz=0.0)), ([dict(good, role=7)], fleet),
+                       ([good], dict(fleet, robots=5000)), ([good], dict(fleet, servers=2000)),
                        ([dict(good, role=ROLE_OBLIGATION)], fleet)]:       # obligation without a rate
         with pytest.raises(rosa.RosaError):
             rosa.schedule_homogeneous(fl, models)
