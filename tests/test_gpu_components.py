@@ -78,7 +78,7 @@ def test_time_conditioning_matches_oracle(which, request):
 
 @pytest.mark.parametrize("which", ["tiny_fp32", "tiny_bf16", "pi0_bf16"])
 @pytest.mark.parametrize("proj", [0, 1, 2, 3])
-@pytest.mark.parametrize("M", [1, 50, 129, 1600])
+@pytest.mark.parametrize("M", [1, 50, 129, 256, 257, 1600])
 def test_projection_matches_float64(which, proj, M, request):
     e, w = request.getfixturevalue(which)
     sh, dtype = e.shape, e.dtype
