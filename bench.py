@@ -568,6 +568,63 @@ def prefill_bench(torch, rosa, args):
     print(json.dumps(out), flush=True)
 
 
+def pipeline_bench(torch, rosa, args):
+    """The whole System-1 path for a batch of robots: the VLM backbone fills
+    their prefix caches, then the action expert generates their chunks from
+    them, back to back on one stream (32 robots, prefixes of 600..1024
+    tokens, horizon 50, 10 Euler steps).  value = robot requests served per
+    second; the two phases are timed separately too."""
+    from synthetic import PI0_SHAPE, PI0_VLM, make_prefix_embeddings, make_vlm_weights, make_weights, prefill_lengths
+    lens = prefill_lengths()
+    H, K, A = 50, 10, PI0_SHAPE.action_dim
+    vw = make_vlm_weights(PI0_VLM, "bf16")
+    ew = make_weights(PI0_SHAPE, "bf16")
+    emb = [torch.from_numpy(make_prefix_embeddings(PI0_VLM, P, "bf16", 4000 + i)).to(torch.bfloat16).cuda()
+           for i, P in enumerate(lens)]
+    kc = [torch.empty((PI0_SHAPE.n_layers, P, 1, PI0_SHAPE.head_dim), dtype=torch.bfloat16, device="cuda")
+          for P in lens]
+    vc = [torch.empty_like(k) for k in kc]
+    rng = np.random.default_rng(5)
+    nz = [torch.from_numpy(rng.standard_normal((H, A)).astype(np.float32)).cuda() for _ in lens]
+    out = [torch.empty_like(n) for n in nz]
+    pp = rosa.PrefixProducer(PI0_VLM, "bf16", vw, len(lens), sum(lens))
+    ex = rosa.ActionExpert(PI0_SHAPE, "bf16", ew, rosa.capacity(len(lens), H, H * len(lens), K, sum(lens)))
+    jobs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(emb, kc, vc, lens)]
+    reqs = [rosa.request_struct(k, v, n, o, P, H, K) for k, v, n, o, P in zip(kc, vc, nz, out, lens)]
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        pp.run(jobs)
+        ex.generate(reqs)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b, c in evs:
+        a.record(stream)
+        pp.run(jobs)
+        b.record(stream)
+        ex.generate(reqs)
+        c.record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    pre = np.array([a.elapsed_time(b) for a, b, _ in evs])
+    gen = np.array([b.elapsed_time(c) for _, b, c in evs])
+    tot = np.array([a.elapsed_time(c) for a, _, c in evs])
+    pp.close()
+    ex.close()
+    print(json.dumps({
+        "metric": "robot requests/s through VLM prefill + action generation (System-1 path)",
+        "value": round(len(lens) * args.steps / elapsed, 2), "unit": "requests/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "s1_pipeline_b32", "robots": len(lens), "prefix_tokens": int(sum(lens)),
+                   "horizon": H, "steps": K},
+        "prefill_ms_p50": round(float(np.percentile(pre, 50)), 3),
+        "generate_ms_p50": round(float(np.percentile(gen, 50)), 3),
+        "total_ms_p50": round(float(np.percentile(tot, 50)), 3),
+        "total_ms_p99": round(float(np.percentile(tot, 99)), 3)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -593,6 +650,9 @@ def main():
     ap.add_argument("--prefill", action="store_true",
                     help="the prefix producer instead: a VLM backbone over 32 robots' prefixes "
                          "(prints its own JSON line)")
+    ap.add_argument("--pipeline", action="store_true",
+                    help="the whole System-1 path: VLM prefill then action generation for 32 robots "
+                         "(prints its own JSON line)")
     ap.add_argument("--prefill-cache", choices=["per_layer", "context"], default="per_layer",
                     help="with --prefill: per-layer backbone K/V, or the context form (the backbone's "
                          "normalised output projected for every layer of an 18-layer cross-attending head)")
@@ -616,6 +676,9 @@ def main():
     from paper_2607_01088_amd import rosa
     if args.prefill:
         prefill_bench(torch, rosa, args)
+        return
+    if args.pipeline:
+        pipeline_bench(torch, rosa, args)
         return
     from synthetic import PRESETS, make_metadata, make_requests, make_weights
 
