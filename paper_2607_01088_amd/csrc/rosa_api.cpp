@@ -670,6 +670,9 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     if (st != ROSA_OK) return fail(nullptr, st, "model configuration not supported");
     st = check_capacity(cap);
     if (st != ROSA_OK) return fail(nullptr, st, "bad capacity");
+    // a request's query rows (horizon x query heads per KV head) are int32 in the plan and kernels
+    if ((int64_t)cap->max_horizon * (cfg->n_q_heads / cfg->n_kv_heads) > (int64_t(1) << 30))
+      return fail(nullptr, ROSA_E_UNSUPPORTED, "max_horizon x query heads per KV head above 2^30");
     const float *need[] = {w->w_in, w->b_in, w->w_t1, w->b_t1, w->w_t2, w->b_t2, w->w_mod, w->b_mod, w->w_qkv,
                            w->w_o, w->w_up, w->w_down, w->w_fmod, w->b_fmod, w->w_out, w->b_out};
     for (const float *p : need)

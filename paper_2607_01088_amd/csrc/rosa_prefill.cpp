@@ -314,6 +314,9 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     if (st != ROSA_OK) return pfail(nullptr, st, "backbone configuration not supported");
     if (max_jobs < 1 || max_tokens < 1 || max_tokens > INT32_MAX / 2)
       return pfail(nullptr, ROSA_E_INVALID, "bad max_jobs / max_tokens");
+    // query rows of one job (tokens x query heads per KV head) are int32 in the plan and kernels
+    if (max_tokens * (cfg->n_q_heads / cfg->n_kv_heads) > (int64_t(1) << 30))
+      return pfail(nullptr, ROSA_E_UNSUPPORTED, "max_tokens x query heads per KV head above 2^30");
     if (!w->w_qkv || !w->w_o || !w->w_up || !w->w_down || (cfg->cache_form == ROSA_CACHE_CONTEXT && !w->w_ctx))
       return pfail(nullptr, ROSA_E_INVALID, "NULL weight pointer");
 

@@ -188,3 +188,19 @@ def test_prefill_create_validates_before_touching_the_gpu():
     assert lib.rosa_prefill_create(C.byref(cfg), C.byref(w), 1, 8, None, C.byref(h)) == rosa.ROSA_E_UNSUPPORTED
     assert lib.rosa_prefill_run(None, None, 0) == rosa.ROSA_E_INVALID
     lib.rosa_prefill_destroy(None)
+
+
+def test_create_rejects_query_row_counts_above_int32_range():
+    # a request's or job's query rows (tokens x query heads per KV head) are int32
+    from synthetic import TINY_VLM
+    lib = rosa.load()
+    h = C.c_void_p()
+    cfg = rosa.model_config(TINY_SHAPE, "fp32")                 # 4 query heads per KV head
+    cap = rosa.capacity(2, 1 << 29, 1 << 29, 4, 200)
+    w = rosa.Weights()
+    assert lib.rosa_batch_create(C.byref(cfg), C.byref(w), C.byref(cap), None, C.byref(h)) \
+        == rosa.ROSA_E_UNSUPPORTED
+    vcfg = rosa.vlm_config(TINY_VLM, "fp32")
+    assert lib.rosa_prefill_create(C.byref(vcfg), C.byref(rosa.VlmWeights()), 1, 1 << 29, None, C.byref(h)) \
+        == rosa.ROSA_E_UNSUPPORTED
+    assert not h.value
