@@ -93,7 +93,8 @@ rosa_status rosa_s1_select_batch(const int32_t *batch_sizes, const double *batch
  * first point for b = 1 and is infeasible for b > 1 (a batch that waits for b
  * requests waits without bound as the load falls).
  * Cost: O(servers x robots x sum over b of k_max) time and O(servers x
- * robots) memory per model and search step.
+ * robots) memory per model and search step; fleets with servers x robots^2 x
+ * (batch sizes over all models) above 4e10 return ROSA_E_UNSUPPORTED.
  */
 
 /* Latency of one batch size at one aggregate request rate. */

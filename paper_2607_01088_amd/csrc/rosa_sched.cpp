@@ -281,8 +281,13 @@ extern "C" rosa_status rosa_schedule_homogeneous(const rosa_fleet *fleet, const 
   if (F.robots < 1 || F.robots > 4096 || F.servers < 1 || F.servers > 1024 || !(F.t_act_ms > 0) ||
       !std::isfinite(F.t_act_ms) || F.horizon < 1 || F.reserved != 0 || !(F.eps_hz > 0) || !std::isfinite(F.eps_hz))
     return ROSA_E_INVALID;
-  for (int m = 0; m < n_models; ++m)
+  int64_t n_cfg = 0;
+  for (int m = 0; m < n_models; ++m) {
     if (!profile_ok(models[m])) return ROSA_E_INVALID;
+    n_cfg += models[m].n_configs;
+  }
+  // Packing work per search step: servers x robots x (configurations x robots).
+  if ((int64_t)F.servers * F.robots * F.robots * n_cfg > (int64_t)40000000000) return ROSA_E_UNSUPPORTED;
   try {
     *out = rosa_fleet_schedule{};
     const int R = F.robots;
