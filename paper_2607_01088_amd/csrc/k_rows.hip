@@ -104,31 +104,49 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
+  // The row's modulation index first; for rows of up to 1024 values its shift
+  // and scale loads are also issued with the row's own loads (wider rows would
+  // need so many registers that fewer waves fit).
+  constexpr bool kEarlyMod = NC <= 4;
+  const float *mrow = modtab + (size_t)rowmod[row] * mod_stride;
+  const float *shift = mrow + shift_off;
+  const float *scale = mrow + scale_off;
   const float *hr = h + (size_t)row * d;
-  float4 v[NC];
-  float ss = 0.f;
+  float4 v[NC], sc[kEarlyMod ? NC : 1], sh[kEarlyMod ? NC : 1];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int i = c * 256 + lane * 4;
     if (i < d) {
       v[c] = *reinterpret_cast<const float4 *>(hr + i);
-      ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+      if constexpr (kEarlyMod) {
+        sc[c] = *reinterpret_cast<const float4 *>(scale + i);
+        sh[c] = *reinterpret_cast<const float4 *>(shift + i);
+      }
     }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
   }
   ss = wave_sum(ss);
   const float r = 1.0f / sqrtf(ss / (float)d + eps);
-  const float *mrow = modtab + (size_t)rowmod[row] * mod_stride;
-  const float *shift = mrow + shift_off;
-  const float *scale = mrow + scale_off;
   OutT *ur = u + (size_t)row * d;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int i = c * 256 + lane * 4;
     if (i < d) {
-      const float4 sc = *reinterpret_cast<const float4 *>(scale + i);
-      const float4 sh = *reinterpret_cast<const float4 *>(shift + i);
-      store4<OutT>(ur + i, v[c].x * r * (1.0f + sc.x) + sh.x, v[c].y * r * (1.0f + sc.y) + sh.y,
-                   v[c].z * r * (1.0f + sc.z) + sh.z, v[c].w * r * (1.0f + sc.w) + sh.w);
+      float4 a, b;
+      if constexpr (kEarlyMod) {
+        a = sc[c];
+        b = sh[c];
+      } else {
+        a = *reinterpret_cast<const float4 *>(scale + i);
+        b = *reinterpret_cast<const float4 *>(shift + i);
+      }
+      store4<OutT>(ur + i, v[c].x * r * (1.0f + a.x) + b.x, v[c].y * r * (1.0f + a.y) + b.y,
+                   v[c].z * r * (1.0f + a.z) + b.z, v[c].w * r * (1.0f + a.w) + b.w);
     }
   }
 }
