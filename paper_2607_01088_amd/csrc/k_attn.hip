@@ -590,30 +590,56 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
                                                          const float *__restrict__ part_ml, OutT *o,
                                                          int ldo, int nq, int nkv, int hd) {
   const AttnGroup gr = groups[blockIdx.y];
-  const ReqDesc rq = reqs[gr.req];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int qloc = blockIdx.x * 4 + wave;
   const int G = nq / nkv;
   if (qloc >= gr.nq) return;
+  const int tok_off = reqs[gr.req].tok_off;   // issued now, used for the store
   const int qrow = gr.q0 + qloc;
   const int qt = qrow / G, qg = gr.kvh * G + qrow % G;
+  // Partials are read CH slots at a time, every load of a batch in flight
+  // together; they are combined in slot order, as one slot at a time would.
+  constexpr int CH = 8;
+  constexpr int kMaxE = 256 / 64;             // head-dim elements per lane (head_dim <= 256)
+  const float2 *ml = reinterpret_cast<const float2 *>(part_ml);
   float mx = -INFINITY;
-  for (int c = 0; c < gr.n; ++c) mx = fmaxf(mx, part_ml[((size_t)(gr.first_slot + c) * kAttnQB + qloc) * 2]);
+  for (int c0 = 0; c0 < gr.n; c0 += CH) {
+    float m[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c)
+      m[c] = c0 + c < gr.n ? ml[(size_t)(gr.first_slot + c0 + c) * kAttnQB + qloc].x : -INFINITY;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) mx = fmaxf(mx, m[c]);
+  }
   float L = 0.f;
-  for (int c = 0; c < gr.n; ++c) {
-    const float *pm = part_ml + ((size_t)(gr.first_slot + c) * kAttnQB + qloc) * 2;
-    L += exp2f(pm[0] - mx) * pm[1];
+  float acc[kMaxE];
+#pragma unroll
+  for (int j = 0; j < kMaxE; ++j) acc[j] = 0.f;
+  for (int c0 = 0; c0 < gr.n; c0 += CH) {
+    float2 p[CH];
+    float ov[CH][kMaxE];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const size_t base = (size_t)(gr.first_slot + c0 + c) * kAttnQB + qloc;
+      const bool live = c0 + c < gr.n;
+      p[c] = live ? ml[base] : make_float2(0.f, 0.f);
+#pragma unroll
+      for (int j = 0; j < kMaxE; ++j) ov[c][j] = live && lane + 64 * j < hd ? part_o[base * hd + lane + 64 * j] : 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      if (c0 + c >= gr.n) break;
+      const float wgt = exp2f(p[c].x - mx);
+      L += wgt * p[c].y;
+#pragma unroll
+      for (int j = 0; j < kMaxE; ++j) acc[j] += wgt * ov[c][j];
+    }
   }
   const float inv = 1.0f / L;
-  OutT *op = o + (size_t)(rq.tok_off + qt) * ldo + (size_t)qg * hd;
-  for (int e = lane; e < hd; e += 64) {
-    float acc = 0.f;
-    for (int c = 0; c < gr.n; ++c) {
-      const size_t base = (size_t)(gr.first_slot + c) * kAttnQB + qloc;
-      acc += exp2f(part_ml[base * 2] - mx) * part_o[base * hd + e];
-    }
-    op[e] = from_f32<OutT>(acc * inv);
-  }
+  OutT *op = o + (size_t)(tok_off + qt) * ldo + (size_t)qg * hd;
+#pragma unroll
+  for (int j = 0; j < kMaxE; ++j)
+    if (lane + 64 * j < hd) op[lane + 64 * j] = from_f32<OutT>(acc[j] * inv);
 }
 
 hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
@@ -645,6 +671,7 @@ hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDes
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16_mode, hipStream_t s) {
   if (n_groups <= 0) return hipSuccess;
+  if (hd > 256) return hipErrorInvalidValue;   // a lane holds at most 4 head-dim elements
   dim3 grid(kAttnQB / 4, n_groups);
   if (bf16_mode)
     hipLaunchKernelGGL(attn_merge_kernel<bf16>, grid, dim3(256), 0, s, groups, reqs, part_o, part_ml,
