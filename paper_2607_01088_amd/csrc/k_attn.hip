@@ -104,9 +104,8 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[8 * TILEB];
   static_assert(4 * TILEB <= 65536, "stage offsets must fit the LDS immediate");
 
-  const int item = a.list[blockIdx.x];
-  if (item < 0) return;
-  const AttnItem it = a.items[item];
+  const AttnItem it = a.ordered[blockIdx.x];
+  if (it.nq <= 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
   const int half = lane >> 5;

@@ -58,6 +58,17 @@ int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std:
   return (int)(8 * most);
 }
 
+void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, size_t n, AttnItem *dst) {
+  for (size_t e = 0; e < n; ++e) {
+    if (order[e] >= 0) {
+      dst[e] = items[order[e]];
+    } else {
+      dst[e] = AttnItem{};
+      dst[e].nq = 0;
+    }
+  }
+}
+
 uint16_t f32_to_bf16_rne(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -561,8 +572,12 @@ hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, i
   std::memcpy(hp + b->off_groups, S0.groups.data(), S0.groups.size() * sizeof(AttnGroup));
   std::memcpy(hp + b->off_groups + S0.groups.size() * sizeof(AttnGroup), S1.groups.data(),
               S1.groups.size() * sizeof(AttnGroup));
-  std::memcpy(hp + b->off_lists, p.attn_lists.data(), p.attn_lists.size() * 4);
-  const size_t used = b->off_lists + p.attn_lists.size() * 4;
+  {
+    std::vector<AttnItem> all(S0.items);
+    all.insert(all.end(), S1.items.begin(), S1.items.end());
+    attn_order_items(all, p.attn_lists.data(), p.attn_lists.size(), (AttnItem *)(hp + b->off_lists));
+  }
+  const size_t used = b->off_lists + p.attn_lists.size() * sizeof(AttnItem);
   hipError_t e = hipMemcpyAsync(b->d_plan, hp, used, hipMemcpyHostToDevice, b->stream);
   if (e != hipSuccess) return e;
   e = hipEventRecord(b->plan_copied[slot], b->stream);
@@ -590,7 +605,7 @@ hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int
   const ReqDesc *reqs = (const ReqDesc *)((uint8_t *)b->d_plan + b->off_reqs);
   const AttnItem *items = (const AttnItem *)((uint8_t *)b->d_plan + b->off_items);
   const AttnGroup *groups = (const AttnGroup *)((uint8_t *)b->d_plan + b->off_groups);
-  const int32_t *lists = (const int32_t *)((uint8_t *)b->d_plan + b->off_lists);
+  const AttnItem *lists = (const AttnItem *)((uint8_t *)b->d_plan + b->off_lists);
   const int r0 = ln.req_lo, n_act = ln.n_act[k];
   if (n_act <= 0) return hipSuccess;
   const int v = attn_set_of(&b->cfg, layer);
@@ -602,7 +617,7 @@ hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int
   a.items = items + it_lo; a.n_items = it_hi - it_lo;
   if (b->bf16) {   // launch order of this step's active set (indices into the whole item array)
     a.items = items;
-    a.list = lists + ln.list_at[v][k];
+    a.ordered = lists + ln.list_at[v][k];
     a.n_blocks = ln.list_blocks[v][k];
   }
   a.reqs = reqs; a.layer = layer;
@@ -740,7 +755,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     // one launch order per step and lane at most: the lane's items plus at most
     // 7 empty slots per XCD row of blocks
     b->max_list_ints = (size_t)cap->max_steps * (8 * (size_t)b->max_items + 8 * kMaxLanes * n_sets);
-    b->plan_bytes = align(b->off_lists + b->max_list_ints * 4);
+    b->plan_bytes = align(b->off_lists + b->max_list_ints * sizeof(AttnItem));
     b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
     if (e != hipSuccess) {
       rosa_status s2 = e == hipErrorOutOfMemory ? fail(nullptr, ROSA_E_NOMEM, "device allocation failed")

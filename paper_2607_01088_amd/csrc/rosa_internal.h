@@ -142,9 +142,9 @@ hipError_t launch_prefill_kv_scatter(const PrefillJob *jobs, const int32_t *row_
 // Attention of one layer.
 struct AttnArgs {
   const AttnItem *items; int n_items;
-  // bf16: launch order.  Block b runs item items[list[b]], or exits if
-  // list[b] < 0; n_blocks blocks.  n_items is then unused.
-  const int32_t *list; int n_blocks;
+  // bf16: the items in launch order.  Block b runs ordered[b], or exits if
+  // its nq is 0; n_blocks blocks.  items and n_items are then unused.
+  const AttnItem *ordered; int n_blocks;
   const ReqDesc *reqs;
   int layer;
   const void *qkv; int ldqkv;      // q at column g*hd, k_a at (nq+j)*hd, v_a at (nq+nkv+j)*hd
@@ -155,7 +155,8 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
 // Host: XCD-balanced, longest-first block -> item table for the items of the
-// given requests (contiguous item ranges); appended to out; returns the block count.
+// given requests (contiguous item ranges); appended to out (-1: an idle
+// block); returns the block count.
 int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std::pair<int, int>> &ranges,
                       std::vector<int32_t> &out);
 // Host: round-to-nearest-even fp32 -> bf16 bits (NaN stays a quiet NaN).
@@ -163,6 +164,9 @@ uint16_t f32_to_bf16_rne(float f);
 // Host: upload L stacked [K][N] fp32 matrices as [L][N][K] (K contiguous), in
 // bf16 or fp32; synchronous.
 hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16);
+// Host: the items of a block -> item table in block order (an idle block
+// gets an item with nq = 0), written to dst.
+void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, size_t n, AttnItem *dst);
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16, hipStream_t s);

@@ -286,8 +286,8 @@ hipError_t upload_prefill_plan(rosa_prefill *h, const PrefillPlan &p) {
   std::memcpy(hp + h->off_rows, p.row_job.data(), p.row_job.size() * 4);
   std::memcpy(hp + h->off_items, p.items.data(), p.items.size() * sizeof(AttnItem));
   std::memcpy(hp + h->off_groups, p.groups.data(), p.groups.size() * sizeof(AttnGroup));
-  std::memcpy(hp + h->off_list, p.list.data(), p.list.size() * 4);
-  const size_t used = h->off_list + p.list.size() * 4;
+  attn_order_items(p.items, p.list.data(), p.list.size(), (AttnItem *)(hp + h->off_list));
+  const size_t used = h->off_list + p.list.size() * sizeof(AttnItem);
   hipError_t e = hipMemcpyAsync(h->d_plan, hp, used, hipMemcpyHostToDevice, h->stream);
   if (e != hipSuccess) return e;
   e = hipEventRecord(h->plan_copied[slot], h->stream);
@@ -369,7 +369,7 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     h->off_items = align(h->off_rows + T * 4);
     h->off_groups = align(h->off_items + (size_t)h->max_items * sizeof(AttnItem));
     h->off_list = align(h->off_groups + (size_t)kAttnMaxSlots * sizeof(AttnGroup));
-    h->plan_bytes = align(h->off_list + h->max_list * 4);
+    h->plan_bytes = align(h->off_list + h->max_list * sizeof(AttnItem));
     h->d_plan = palloc<uint8_t>(h, h->plan_bytes, e);
     if (e != hipSuccess) {
       rosa_status s2 = e == hipErrorOutOfMemory ? pfail(nullptr, ROSA_E_NOMEM, "device allocation failed")
@@ -432,7 +432,7 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
     const int32_t *d_rows = (const int32_t *)(dp + h->off_rows);
     const AttnItem *d_items = (const AttnItem *)(dp + h->off_items);
     const AttnGroup *d_groups = (const AttnGroup *)(dp + h->off_groups);
-    const int32_t *d_list = (const int32_t *)(dp + h->off_list);
+    const AttnItem *d_list = (const AttnItem *)(dp + h->off_list);
     const int M = (int)p.M;
     const size_t es = h->esz;
     const hipStream_t s = h->stream;
@@ -458,7 +458,7 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       }
       AttnArgs a{};
       a.items = d_items; a.n_items = (int)p.items.size();
-      a.list = d_list; a.n_blocks = p.n_blocks;
+      a.ordered = d_list; a.n_blocks = p.n_blocks;
       a.reqs = d_reqs; a.layer = 0;
       a.qkv = h->qkv; a.ldqkv = h->qkv_dim; a.o = h->o; a.ldo = h->o_dim;
       a.nq = h->nq; a.nkv = h->nkv; a.hd = h->hd;
