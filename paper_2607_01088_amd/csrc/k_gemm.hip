@@ -195,6 +195,21 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
     const int sb = wave / T::PERB;
     uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
     float *H = reinterpret_cast<float *>(g.out);
+    // Gate rows of every row this lane touches, loaded once up front so that
+    // no gate load waits for its row's modulation index (32-bit offsets: the
+    // gate table has far fewer than 2^31 elements).  Tiles of 16 waves have no
+    // registers to spare (128 per lane) and look the index up per use.
+    constexpr bool kHoist = T::NW < 16;
+    int goff[kHoist ? MBW : 1][4];
+    if constexpr (kHoist) {
+#pragma unroll
+      for (int i = 0; i < MBW; ++i)
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int row = min(m0 + (wm * MBW + i) * 32 + 8 * p + (lane >> 3), g.M - 1);
+          goff[i][p] = g.rowmod[row] * g.gate_stride;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
@@ -216,7 +231,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           const int row = rb + rr;
           if (row < g.M && col < g.N) {
             hv[p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
-            gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
+            if constexpr (kHoist) gt[p] = *reinterpret_cast<const float4 *>(g.gate + goff[i][p] + col);
+            else gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
           }
         }
 #pragma unroll
