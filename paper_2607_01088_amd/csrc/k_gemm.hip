@@ -5,6 +5,8 @@
 // Epilogues fuse what follows each projection: plain store (QKV), tanh-GELU
 // (MLP up), and the gated residual h += gate * C whose gate row is the
 // row's flow-time modulation (attention output and MLP down).
+#include <algorithm>
+
 #include "rosa_device.h"
 #include "rosa_internal.h"
 
@@ -188,8 +190,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
   // columns n0 + 32 (wn TN + j) + 8 (r / 4) + 4 (lane / 32) + r % 4: four
   // consecutive columns per 4 registers.
   const int r32 = lane & 31, half = lane >> 5;
-  if constexpr (EPI == kEpiGatedResidual) {
-    // h += gate[rowmod[row]] * acc.  Each wave stages one 32 x 32 tile at a
+  if constexpr (EPI == kEpiGatedResidual || EPI == kEpiPartial) {
+    // h += gate[rowmod[row]] * acc (or, for a K slice, out = acc in fp32).
+    // Each wave stages one 32 x 32 tile at a
     // time in its own 4 KB slot (fp32: 32 rows x 8 chunks of 16 B, chunk c of
     // row r at c ^ ((r / 2) % 8)), then reads it back row-contiguous.
     const int sb = wave / T::PERB;
@@ -199,7 +202,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
     // no gate load waits for its row's modulation index (32-bit offsets: the
     // gate table has far fewer than 2^31 elements).  Tiles of 16 waves have no
     // registers to spare (128 per lane) and look the index up per use.
-    constexpr bool kHoist = T::NW < 16;
+    constexpr bool kHoist = T::NW < 16 && EPI == kEpiGatedResidual;
     int goff[kHoist ? MBW : 1][4];
     if constexpr (kHoist) {
 #pragma unroll
@@ -229,7 +232,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           const int rr = 8 * p + (lane >> 3), c = lane & 7;
           v[p] = *reinterpret_cast<const float4 *>(stg + rr * 128 + ((c ^ ((rr >> 1) & 7)) * 16));
           const int row = rb + rr;
-          if (row < g.M && col < g.N) {
+          if (EPI == kEpiGatedResidual && row < g.M && col < g.N) {
             hv[p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
             if constexpr (kHoist) gt[p] = *reinterpret_cast<const float4 *>(g.gate + goff[i][p] + col);
             else gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
@@ -239,12 +242,16 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
         for (int p = 0; p < 4; ++p) {
           const int row = rb + 8 * p + (lane >> 3);
           if (row < g.M && col < g.N) {
-            float4 h = hv[p];
-            h.x = h.x + gt[p].x * v[p].x;
-            h.y = h.y + gt[p].y * v[p].y;
-            h.z = h.z + gt[p].z * v[p].z;
-            h.w = h.w + gt[p].w * v[p].w;
-            *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
+            if constexpr (EPI == kEpiPartial) {
+              *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = v[p];
+            } else {
+              float4 h = hv[p];
+              h.x = h.x + gt[p].x * v[p].x;
+              h.y = h.y + gt[p].y * v[p].y;
+              h.z = h.z + gt[p].z * v[p].z;
+              h.w = h.w + gt[p].w * v[p].w;
+              *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
+            }
           }
         }
       }
@@ -285,23 +292,34 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
 }
 
 template <typename T, int EPI>
-__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct) {
+__global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct, int ksplit) {
   constexpr int SBYTES = T::SBYTES;
   __shared__ __attribute__((aligned(1024))) uint8_t L0[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L1[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L2[SBYTES];
   __shared__ __attribute__((aligned(1024))) uint8_t L3[SBYTES];
 
-  // Tile of this block: XCD x = b % 8 takes the x-th eighth of the tile list.
-  const int n_tiles = nrt * nct;
+  // Work unit of this block: XCD x = b % 8 takes the x-th eighth of the unit
+  // list; unit u is K slice u / n_tiles of tile u % n_tiles (one slice
+  // unless the product is split).
+  const int n_tiles = nrt * nct, n_units = n_tiles * ksplit;
   const int b = blockIdx.x, x = b & 7, q = b >> 3;
-  const int per = n_tiles >> 3, extra = n_tiles & 7;
+  const int per = n_units >> 3, extra = n_units & 7;
   if (q >= per + (x < extra ? 1 : 0)) return;
-  const int tile = x * per + min(x, extra) + q;
+  const int unit = x * per + min(x, extra) + q;
+  const int tile = unit % n_tiles, slice = unit / n_tiles;
   const int m0 = (tile / nct) * T::BM, n0 = (tile % nct) * T::BN;
+  const int nks = g.K / T::BK / ksplit;
   f32x16 acc[T::MBW][T::TN];
-  gemm_mainloop<T>(g, m0, n0, 0, g.K / T::BK, L0, L1, L2, L3, acc);
-  gemm_epilogue<T, EPI>(g, m0, n0, L0, L1, L2, L3, acc);
+  gemm_mainloop<T>(g, m0, n0, slice * nks, nks, L0, L1, L2, L3, acc);
+  if constexpr (EPI == kEpiPartial) {
+    GemmArgs gp = g;
+    gp.out = g.part + (size_t)slice * g.M * g.N;
+    gp.ldo = g.N;
+    gemm_epilogue<T, EPI>(gp, m0, n0, L0, L1, L2, L3, acc);
+  } else {
+    gemm_epilogue<T, EPI>(g, m0, n0, L0, L1, L2, L3, acc);
+  }
 }
 
 // Block configurations and their measured cost on MI355X (one round of
@@ -344,36 +362,96 @@ static_assert(cfg_matches<Cfg0>(kCfgs[0]) && cfg_matches<Cfg1>(kCfgs[1]) && cfg_
               cfg_matches<Cfg9>(kCfgs[9]) && cfg_matches<Cfg10>(kCfgs[10]),
               "cost table matches the tiles");
 
+// Sum of the K slices of a split product, in slice order, and the epilogue
+// of the whole product; 4 consecutive columns per thread.
+template <int EPI>
+__global__ void __launch_bounds__(256) gemm_split_reduce_kernel(GemmArgs g, int ksplit) {
+  const size_t n4 = (size_t)g.M * g.N / 4;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (size_t)gridDim.x * 256) {
+    const size_t e = i * 4;
+    const int row = (int)(e / g.N), col = (int)(e % g.N);
+    f32x4 v = *reinterpret_cast<const f32x4 *>(g.part + e);
+    for (int s2 = 1; s2 < ksplit; ++s2) {
+      const f32x4 p = *reinterpret_cast<const f32x4 *>(g.part + (size_t)s2 * g.M * g.N + e);
+      v[0] += p[0]; v[1] += p[1]; v[2] += p[2]; v[3] += p[3];
+    }
+    if constexpr (EPI == kEpiGatedResidual) {
+      float *hp = reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo + col;
+      const float4 gt = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
+      float4 hv = *reinterpret_cast<const float4 *>(hp);
+      hv.x = hv.x + gt.x * v[0];
+      hv.y = hv.y + gt.y * v[1];
+      hv.z = hv.z + gt.z * v[2];
+      hv.w = hv.w + gt.w * v[3];
+      *reinterpret_cast<float4 *>(hp) = hv;
+    } else {
+      float a0 = v[0], a1 = v[1], a2 = v[2], a3 = v[3];
+      if constexpr (EPI == kEpiGelu) {
+        a0 = gelu_tanh_f(a0); a1 = gelu_tanh_f(a1); a2 = gelu_tanh_f(a2); a3 = gelu_tanh_f(a3);
+      }
+      bf16x4 o;
+      o[0] = (bf16)a0; o[1] = (bf16)a1; o[2] = (bf16)a2; o[3] = (bf16)a3;
+      *reinterpret_cast<bf16x4 *>(reinterpret_cast<bf16 *>(g.out) + (size_t)row * g.ldo + col) = o;
+    }
+  }
+}
+
+// K slices for a launch of n_tiles tiles of BK-deep stages (1: no split).
+int gemm_split_count(const GemmArgs &g, int n_tiles, int bk) {
+  if (!g.part || n_tiles >= kSplitMinTiles || g.N % 4 || g.ldo % 4) return 1;
+  const int nk = g.K / bk;
+  for (int ks = kSplitMax; ks >= 2; ks /= 2)
+    if (n_tiles * ks <= 256 && nk % ks == 0 && nk / ks >= 4 && (size_t)ks * g.M * g.N <= g.part_floats) return ks;
+  return 1;
+}
+
 template <typename T>
-static hipError_t launch_tile(const GemmArgs &g, hipStream_t s) {
+static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split) {
   const int nrt = (g.M + T::BM - 1) / T::BM, nct = (g.N + T::BN - 1) / T::BN;
-  dim3 grid((nrt * nct + 7) / 8 * 8);
+  const int ks = allow_split ? gemm_split_count(g, nrt * nct, T::BK) : 1;
+  dim3 grid((nrt * nct * ks + 7) / 8 * 8);
+  if (ks > 1) {
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiPartial>), grid, dim3(T::NT), 0, s, g, nrt, nct, ks);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int rgrid = (int)std::min<size_t>(((size_t)g.M * g.N / 4 + 255) / 256, 4096);
+    switch (g.epi) {
+      case kEpiStore: hipLaunchKernelGGL(gemm_split_reduce_kernel<kEpiStore>, dim3(rgrid), dim3(256), 0, s, g, ks); break;
+      case kEpiGelu: hipLaunchKernelGGL(gemm_split_reduce_kernel<kEpiGelu>, dim3(rgrid), dim3(256), 0, s, g, ks); break;
+      default: hipLaunchKernelGGL(gemm_split_reduce_kernel<kEpiGatedResidual>, dim3(rgrid), dim3(256), 0, s, g, ks); break;
+    }
+    return hipGetLastError();
+  }
   switch (g.epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
-    case kEpiGelu: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
-    default: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGatedResidual>), grid, dim3(T::NT), 0, s, g, nrt, nct); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1); break;
+    case kEpiGelu: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1); break;
+    default: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGatedResidual>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1); break;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) {
+static hipError_t launch_cfg(const GemmArgs &g, int cfg, hipStream_t s, bool allow_split) {
   if (g.M <= 0) return hipSuccess;
   if (g.K % 128 != 0 || g.N % 8 != 0) return hipErrorInvalidValue;
   switch (cfg) {
-    case 0: return launch_tile<Cfg0>(g, s);
-    case 1: return launch_tile<Cfg1>(g, s);
-    case 2: return launch_tile<Cfg2>(g, s);
-    case 3: return launch_tile<Cfg3>(g, s);
-    case 4: return launch_tile<Cfg4>(g, s);
-    case 5: return launch_tile<Cfg5>(g, s);
-    case 6: return launch_tile<Cfg6>(g, s);
-    case 7: return launch_tile<Cfg7>(g, s);
-    case 8: return launch_tile<Cfg8>(g, s);
-    case 9: return launch_tile<Cfg9>(g, s);
-    case 10: return launch_tile<Cfg10>(g, s);
+    case 0: return launch_tile<Cfg0>(g, s, allow_split);
+    case 1: return launch_tile<Cfg1>(g, s, allow_split);
+    case 2: return launch_tile<Cfg2>(g, s, allow_split);
+    case 3: return launch_tile<Cfg3>(g, s, allow_split);
+    case 4: return launch_tile<Cfg4>(g, s, allow_split);
+    case 5: return launch_tile<Cfg5>(g, s, allow_split);
+    case 6: return launch_tile<Cfg6>(g, s, allow_split);
+    case 7: return launch_tile<Cfg7>(g, s, allow_split);
+    case 8: return launch_tile<Cfg8>(g, s, allow_split);
+    case 9: return launch_tile<Cfg9>(g, s, allow_split);
+    case 10: return launch_tile<Cfg10>(g, s, allow_split);
     default: return hipErrorInvalidValue;
   }
 }
+
+// A forced configuration never splits K: every configuration then computes
+// each output with the same instruction sequence.
+hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s) { return launch_cfg(g, cfg, s, false); }
 
 int gemm_pick_config(int M, int N, int K, int epi, int n_cu) {
   const int e = epi < 0 || epi > 2 ? 2 : epi;
@@ -457,8 +535,8 @@ hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int for
       else
         n_cu = 256;
     }
-    const int cfg = force_cfg >= 0 ? force_cfg : gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu);
-    return launch_gemm_cfg(g, cfg, s);
+    if (force_cfg >= 0) return launch_cfg(g, force_cfg, s, false);
+    return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true);
   }
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   switch (g.epi) {

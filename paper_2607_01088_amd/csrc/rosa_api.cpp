@@ -191,6 +191,8 @@ struct rosa_batch {
   int32_t *row_req = nullptr, *rowmod = nullptr, *ident = nullptr;
   float *modtab = nullptr, *emb = nullptr, *tc1 = nullptr, *tc2 = nullptr, *gemv_ws = nullptr;
   float *part_o = nullptr, *part_ml = nullptr;
+  float *gemm_part = nullptr;        // K-slice products of split projections (one lane only)
+  size_t gemm_part_floats = 0;
   int max_items = 0;                 // attention work items per call, both sets
   int max_slots = 0;                 // partial-result slots per call, both sets
 
@@ -738,6 +740,10 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->gemv_ws = dalloc<float>(b, small_gemv_workspace_floats(std::max(D.mod_stride, D.d)), e);
     const int n_sets = cfg->attention_layout == ROSA_ATTN_ALTERNATING ? 2 : 1;
     b->max_slots = n_sets * kMaxSlots;
+    b->gemm_part_floats = b->bf16 ? std::min<size_t>((size_t)kSplitMax * maxM * std::max(D.qkv_dim, std::max(D.dff, D.d)),
+                                                     (size_t)16 << 20)
+                                  : 0;
+    if (b->gemm_part_floats) b->gemm_part = dalloc<float>(b, b->gemm_part_floats, e);
     b->part_o = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * D.hd, e);
     b->part_ml = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * 2, e);
 
@@ -876,6 +882,7 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           });
           if (e != hipSuccess) break;
           GemmArgs gq{};
+          if (nl == 1) { gq.part = b->gemm_part; gq.part_floats = b->gemm_part_floats; }
           gq.a = u; gq.lda = D.d; gq.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * es;
           gq.M = M; gq.N = D.qkv_dim; gq.K = D.d; gq.epi = kEpiStore; gq.out = qkv; gq.ldo = D.qkv_dim;
           e = timed(b, kcGemmQKV, [&] { return launch_gemm(gq, b->bf16, st, b->gemm_cfg); });
@@ -883,6 +890,7 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           e = run_attention(b, p, ln, k, l, b->qkv, b->o, st);
           if (e != hipSuccess) break;
           GemmArgs go{};
+          if (nl == 1) { go.part = b->gemm_part; go.part_floats = b->gemm_part_floats; }
           go.a = o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
           go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = h; go.ldo = D.d;
           go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
@@ -894,11 +902,13 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           });
           if (e != hipSuccess) break;
           GemmArgs gu{};
+          if (nl == 1) { gu.part = b->gemm_part; gu.part_floats = b->gemm_part_floats; }
           gu.a = u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * es;
           gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = g; gu.ldo = D.dff;
           e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
           GemmArgs gd{};
+          if (nl == 1) { gd.part = b->gemm_part; gd.part_floats = b->gemm_part_floats; }
           gd.a = g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * es;
           gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = h; gd.ldo = D.d;
           gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
@@ -1035,6 +1045,7 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
       return fail(b, ROSA_E_INVALID, "gemm operands must be 16-byte aligned");
     GemmArgs g{};
     g.a = a; g.M = M; g.out = out; g.gate = gate; g.rowmod = b->ident;
+    g.part = b->gemm_part; g.part_floats = b->gemm_part_floats;
     switch (which) {
       case 0: g.lda = D.d; g.K = D.d; g.N = D.qkv_dim; g.epi = kEpiStore; g.ldo = D.qkv_dim;
               g.wt = (uint8_t *)b->wt_qkv + (size_t)layer * D.qkv_dim * D.d * b->esz; break;

@@ -68,6 +68,7 @@ enum Epilogue : int {
   kEpiStore = 0,          // out = acc                      (activation dtype)
   kEpiGelu = 1,           // out = gelu_tanh(acc)           (activation dtype)
   kEpiGatedResidual = 2,  // h += gate[rowmod[m]][n] * acc  (fp32)
+  kEpiPartial = 3,        // out = acc (fp32): one K slice of a split product
 };
 
 // One job of the prefix producer on the device (32 bytes): its embedded
@@ -121,7 +122,14 @@ struct GemmArgs {
   int epi;
   void *out; int ldo;        // kEpiStore / kEpiGelu: activation dtype; kEpiGatedResidual: fp32 h
   const float *gate; int gate_stride; const int32_t *rowmod;  // gate = gate[rowmod[m]*gate_stride + n]
+  // Optional fp32 workspace of part_floats floats.  When a launch would have
+  // fewer than kSplitMinTiles tiles (few rows), K is split over up to
+  // kSplitMax blocks per tile: each writes its slice's product here, and a
+  // second kernel sums the slices in order and applies the epilogue.
+  float *part; size_t part_floats;
 };
+constexpr int kSplitMinTiles = 64;
+constexpr int kSplitMax = 8;
 // force_cfg < 0: block configuration chosen by the cost model.
 hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1);
 // bf16 GEMM with a given block configuration (0: 384x128, 1: 256x256, 2: 128x256,

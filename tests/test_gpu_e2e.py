@@ -248,7 +248,9 @@ def test_repeat_runs_are_bitwise_identical(pi0_expert):
 
 def test_projection_block_configs_bitwise_identical(pi0_expert):
     """The whole call gives bitwise the same actions whichever projection
-    block configuration is forced."""
+    block configuration is forced.  The default path may split K over blocks
+    for launches with few tiles (this 4-request batch), which sums in another
+    order: the same actions to rounding."""
     e, _ = pi0_expert
     reqs = make_requests(PRESETS["factory_b256"], indices=[0, 7, 21, 40])
     db = _rosa().DeviceBatch(reqs, "bf16")
@@ -262,9 +264,11 @@ def test_projection_block_configs_bitwise_identical(pi0_expert):
             outs.append(db.results())
     finally:
         e.gemm_config(-1)
-    for o in outs[1:]:
-        for a, b in zip(o, outs[0]):
+    for o in outs[2:]:
+        for a, b in zip(o, outs[1]):
             assert np.array_equal(a, b)
+    for a, b in zip(outs[0], outs[1]):
+        assert rel_l2(a, b) < 5e-3
 
 
 def test_lane_counts_bitwise_identical(pi0_expert):
