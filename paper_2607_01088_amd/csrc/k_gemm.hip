@@ -398,7 +398,8 @@ __global__ void __launch_bounds__(256) gemm_split_reduce_kernel(GemmArgs g, int 
 
 // K slices for a launch of n_tiles tiles of BK-deep stages (1: no split).
 int gemm_split_count(const GemmArgs &g, int n_tiles, int bk) {
-  if (!g.part || n_tiles >= kSplitMinTiles || g.N % 4 || g.ldo % 4) return 1;
+  // K = 1024 products are too short for the saving to pay for the second launch.
+  if (!g.part || n_tiles >= kSplitMinTiles || g.K < 2048 || g.N % 4 || g.ldo % 4) return 1;
   const int nk = g.K / bk;
   for (int ks = kSplitMax; ks >= 2; ks /= 2)
     if (n_tiles * ks <= 256 && nk % ks == 0 && nk / ks >= 4 && (size_t)ks * g.M * g.N <= g.part_floats) return ks;
