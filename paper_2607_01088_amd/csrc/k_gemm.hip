@@ -4,7 +4,10 @@
 //
 // Epilogues fuse what follows each projection: plain store (QKV), tanh-GELU
 // (MLP up), and the gated residual h += gate * C whose gate row is the
-// row's flow-time modulation (attention output and MLP down).
+// row's flow-time modulation (attention output and MLP down).  Launches with
+// few tiles (few rows) may split K over several blocks per tile: each block
+// stores its slice's fp32 product (kEpiPartial) and a second kernel sums the
+// slices in order and applies the epilogue.
 #include <algorithm>
 
 #include "rosa_device.h"
