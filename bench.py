@@ -157,9 +157,9 @@ def _summarize_prefill(out):
     lines = ["# Kernel-time summary: vlm_prefill_b32 workload (32 robots' prefixes, 26,173 tokens, "
              "18-layer width-2048 VLM backbone, bf16)", "",
              "Command (one MI355X, repository root, library built in-tree):", "", "```",
-             "export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_prefill "
+             f"export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d {out}/prof_prefill "
              "-o prefill -- python3 -u bench.py --prefill --steps 3 --warmup 1 --no-cpu-baseline",
-             "python bench.py --summarize-profiles gpurun_out", "```", "",
+             f"python bench.py --summarize-profiles {out}", "```", "",
              "The profiled process runs 1 warm-up + 3 timed + 2 per-kernel-timing prefill calls (6 calls); each "
              "call is 18 QKV projections and K/V scatters and 17 attention, output-projection and MLP layers "
              "(the last layer's caches need only its K and V).",
@@ -189,7 +189,7 @@ def summarize_profiles(out):
     lines = ["# Kernel-time summary: factory_b256 workload (256 ragged requests, pi0-shaped expert, bf16)", "",
              "Command (one MI355X, repository root, library built in-tree; one lane, so every dispatch",
              "runs alone as in bench.py's per-kernel timing pass):", "", "```",
-             "export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_factory "
+             f"export TMPDIR=/tmp; rocprofv3 --kernel-trace --stats --output-format csv -d {out}/prof_factory "
              "-o factory -- python -u bench.py --steps 3 --warmup 1 --no-cpu-baseline --lanes 1", "```", "",
              "The profiled process runs 1 warm-up + 3 timed + 2 per-kernel-timing generate calls (6 calls).",
              "Table from `factory_kernel_stats.csv`, sorted by total time.", "",
@@ -216,15 +216,15 @@ def summarize_profiles(out):
     md = ["# HBM traffic of the attention kernel, factory_b256 workload", "",
           "Commands (one MI355X, repository root, library built in-tree; one counter per run, one lane):", "", "```",
           "export TMPDIR=/tmp",
-          "timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o f -- "
+          f"timeout -s KILL 300 rocprofv3 --pmc FETCH_SIZE --output-format csv -d {out}/pmc_fetch -o f -- "
           "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
-          "timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o w -- "
+          f"timeout -s KILL 300 rocprofv3 --pmc WRITE_SIZE --output-format csv -d {out}/pmc_write -o w -- "
           "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
-          "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_cfetch -o f -- "
+          f"timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv -d {out}/pmc_cfetch -o f -- "
           "python -u bench.py --copy-probe",
-          "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_cwrite -o w -- "
+          f"timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv -d {out}/pmc_cwrite -o w -- "
           "python -u bench.py --copy-probe",
-          "python bench.py --summarize-profiles gpurun_out", "```", "",
+          f"python bench.py --summarize-profiles {out}", "```", "",
           f"Calibration: the copy probe reads and writes 1 GiB (1048576 KiB) per launch; FETCH_SIZE reads "
           f"{cf:.1f} KiB and WRITE_SIZE {cw:.1f} KiB per dispatch, so FETCH_SIZE is scaled by {ff:.4f} and "
           f"WRITE_SIZE by {wf:.4f}.", "",
@@ -665,8 +665,8 @@ def main():
         summarize_profiles(args.summarize_profiles)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported in this build "
-              "(requests shard across GPUs with no exchange; see DESIGN.md).", file=sys.stderr)
+        print(f"bench.py measures one GPU: --gpus {args.gpus} is not supported (requests shard across GPUs "
+              "with no exchange, so each GPU's share is measured on its own).", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -18,7 +18,7 @@ SOURCES = ["k_time.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_prefill.hi
            "rosa_prefill.cpp", "rosa_sched.cpp"]
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wno-unused-result",
-         # packed fp32 VALU ops stay disabled (compiler-formed v_pk_* fp32 ops)
+         # packed fp32 VALU ops stay disabled: compiler-formed packed fp32 forms are avoided
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
