@@ -28,6 +28,15 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
                             const rosa_request *reqs, int32_t n, int32_t *order,
                             int32_t *tok_off, int32_t *m_k, int32_t *counts);
 
+/* Host-only lane assignment of a request set (no GPU needed, nothing
+ * enqueued): the lanes a bf16 call would split this set into when `lanes`
+ * lanes are configured (rosa_debug_set_lanes), with the same rule as
+ * rosa_generate_actions (at most n / 64 lanes).  lane_of[n] (by caller index)
+ * receives each request's lane in [0, lanes).  Returns the status
+ * rosa_generate_actions would return for this set. */
+rosa_status rosa_debug_plan_lanes(const rosa_model_config *cfg, const rosa_capacity *cap,
+                                  const rosa_request *reqs, int32_t n, int32_t lanes, int32_t *lane_of);
+
 /* Time conditioning alone: for n flow times taus (HOST fp32), write the
  * modulation table rows to out (DEVICE fp32 [n][L*6d + 2d]): per layer l the
  * six d-wide vectors [shift_a|scale_a|gate_a|shift_m|scale_m|gate_m] at offset

@@ -42,8 +42,6 @@ constexpr int waitcnt_lgkm0 = 15 | (3 << 14) | (7 << 4);   // lgkmcnt(0), others
 // chunks that the transpose reads of a 32-lane half touch (V operand), then
 // fall in distinct bank groups.
 __device__ __forceinline__ int swz(int r, int cpr) { return (((r & 3) << 2) | ((r >> 2) & 3)) & (cpr - 1); }
-constexpr int kChains = 2;          // independent S accumulator chains (even / odd k-steps)
-constexpr bool kSpreadCopies = false; // copies spread over the step, else in the first slots
 }  // namespace at
 
 #define ROSA_LDS_A(p) ((__attribute__((address_space(3))) void *)(p))
@@ -55,10 +53,25 @@ constexpr bool kSpreadCopies = false; // copies spread over the step, else in th
 // the next MFMA, which would cap the LDS reads in flight at one.  The kernel
 // waits for the copies itself (vmcnt) and sets M0, which nothing else in these
 // kernels uses; the s_nop is the wait state the M0 write needs before the copy.
+// dma_1k_s takes a wave-uniform 64-bit base (SGPRs) plus a 32-bit per-lane
+// byte offset; dma_1k a full per-lane address.
 __device__ __forceinline__ void dma_1k(const void *src, uint32_t lds) {
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+__device__ __forceinline__ void dma_1k_s(const void *base, uint32_t off, uint32_t lds) {
+  // The base is wave-uniform by construction; reading it through readfirstlane
+  // keeps it in SGPRs even where the compiler cannot prove that.
+  const uint64_t b64 = (uint64_t)(size_t)base;
+  const uint64_t ub = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b64 >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b64);
+  const void *bs = (const void *)(size_t)ub;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(bs), "s"(lds)
+               : "memory", "m0");
 #pragma clang diagnostic pop
 }
 __device__ __forceinline__ uint32_t lds_u32(const uint8_t *p) {
@@ -74,35 +87,40 @@ __device__ __forceinline__ bf16x8 lds_tr_pair(const lds_u8 *p0, const lds_u8 *p1
   const uint2 u1 = __builtin_bit_cast(uint2, v1);
   return __builtin_bit_cast(bf16x8, make_uint4(u0.x, u0.y, u1.x, u1.y));
 }
-template <int HD>
+template <int HD, int NG>
 struct AttnTile {
   static constexpr int ROWB = HD * 2;             // bytes per K or V row
   static constexpr int CPR = ROWB / 16;           // 16-byte chunks per row
   static constexpr int TILEB = 32 * ROWB;         // bytes of one 32-key K (or V) tile
-  static constexpr int UNITS = 2 * TILEB / 1024;  // 1 KB copies per stage (K then V)
-  static constexpr int CPW = 2 * ((UNITS / 2 + 3) / 4);   // copies per copying wave per stage
+  static constexpr int UNITS = TILEB / 1024;      // 1 KB copies per tile
+  static constexpr int UPW = (UNITS + 3) / 4;     // copies per copying wave per tile
   static constexpr int RPU = 1024 / ROWB;         // rows per 1 KB copy
-  // A wave copies CPW units of a stage or none, so waiting until at most
-  // 2 CPW copies are outstanding leaves exactly the two next stages in flight.
-  static constexpr int WAIT = at::waitcnt_vm(2 * CPW);
-  static constexpr int WAIT0 = at::waitcnt_vm(0);
-  static_assert((UNITS / 2) % 4 == 0 || UNITS / 2 < 4, "copy split");
+  static constexpr int KST = 3, VST = 2;          // K ring and V ring depths
+  static constexpr int RINGB = (KST + VST) * TILEB;
+  static constexpr int STGB = 4 * NG * 32 * 2 * HD;   // output staging of the block's query rows
+  static constexpr int LDSB = RINGB > STGB ? RINGB : STGB;
+  static_assert(UNITS % 4 == 0 || UNITS < 4, "copy split");
 };
 
+// Two blocks of four waves share a CU (two waves per SIMD): the register file
+// (at most 256 per lane) and LDS (at most 80 KB) are sized for that, and each
+// SIMD interleaves the two waves, so one wave's LDS waits and softmax work
+// overlap the other's MFMAs.  A wave owns NG groups of 32 query rows (groups
+// w and w + 4 of the item).  Step t (one 32-key tile): wait for K tile t and
+// V tile t, one barrier, issue the copies of V tile t + 1 and K tile t + 2,
+// S^T = K Q^T, the softmax of the tile, O^T += V^T P^T.
 template <int HD, int NG>
-__global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   using at::TK;
-  using T = AttnTile<HD>;
+  using T = AttnTile<HD, NG>;
   constexpr int NS = HD / 16;       // MFMA k-steps over head_dim for S
   constexpr int NT = HD / 32;       // 32-row output tiles over head_dim
-  constexpr int NF = NS + 2 * NT;   // LDS operand fragments (and MFMA slots) per step
-  constexpr int CPR = T::CPR, ROWB = T::ROWB, TILEB = T::TILEB;
-  // K ring and V ring of four 32-key tiles each: K stage s at s TILEB, V
-  // stage s at (4 + s) TILEB.  Step t computes S for tile t and O += P V for
-  // tile t - 1, so the V ring runs one tile behind the K ring.  Every stage
-  // offset from a ring's lane base fits a ds_read immediate.
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[8 * TILEB];
-  static_assert(4 * TILEB <= 65536, "stage offsets must fit the LDS immediate");
+  constexpr int CPR = T::CPR, ROWB = T::ROWB, TILEB = T::TILEB, UPW = T::UPW;
+  constexpr int KST = T::KST, VST = T::VST;
+  // K stage s at s TILEB (s < 3), V stage s at (3 + s) TILEB (s < 2).  Every
+  // stage offset from a lane base fits a ds_read immediate.
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[T::LDSB];
+  static_assert(T::RINGB <= 65536 + TILEB, "stage offsets must fit the LDS immediate");
 
   const AttnItem it = a.ordered[blockIdx.x];
   if (it.nq <= 0) return;
@@ -111,28 +129,6 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   const int half = lane >> 5;
   const int G = a.nq / a.nkv;
   const bf16 *qkv = reinterpret_cast<const bf16 *>(a.qkv);
-
-  // Q^T operand of group g, held for the whole item: lane holds
-  // Q[row][16 s + 8 half .. + 7] for its row; rows past the item's queries
-  // read the item's first row instead (their results are never stored).
-  // Loaded right after the first copy group is issued, so the two latencies
-  // overlap: the compiler does not see the copies, and its wait for Q (all
-  // loads it knows of) then also covers the copy group issued before it.
-  bf16x8 qf[NG][NS];
-  auto load_q = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      const int loc = 32 * (wave + 4 * g) + (lane & 31);
-      const int qrow = it.q0 + (loc < it.nq ? loc : 0);
-      const bf16 *qp = qkv + (size_t)(it.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
-    }
-#pragma unroll
-    for (int g = 0; g < NG; ++g)
-#pragma unroll
-      for (int s = 0; s < NS; ++s) asm volatile("" : "+v"(qf[g][s]));
-  };
 
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
   const bf16 *pk = reinterpret_cast<const bf16 *>(it.pk) + (size_t)a.layer * it.P * prow + (size_t)it.kvh * HD;
@@ -149,90 +145,95 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
 
   // Copies: 1 KB units, unit u of a tile by wave u % 4; lane i fills physical
   // chunk i % CPR of row u * RPU + i / CPR, which holds logical chunk
-  // (i % CPR) ^ swz(row).  Keys below the range load the first valid key
-  // (finite values; their scores are masked).  A tile that lies wholly in the
-  // prefix (all but at most three per item) takes its sources from a uniform
-  // base plus per-lane offsets fixed for the whole item; the others compute
-  // each lane's key.  Tile indices past the last tile copy the last tile
-  // again (harmless: that stage is not in use).
-  constexpr int UPW = (T::UNITS / 2 + 3) / 4;    // units of one tile per copying wave
-  constexpr int NCP = 2 * UPW;                   // copies per group (K units, then V units)
-  int poff[UPW];
+  // (i % CPR) ^ swz(row).  A tile wholly in the prefix takes its sources from
+  // a wave-uniform base plus per-lane byte offsets fixed for the whole item;
+  // the others (at most two per item) compute each lane's key: keys below the
+  // range load the first valid key (finite values; their scores are masked).
+  // Tile indices past the last tile copy the last tile again into a stage no
+  // step reads, so every step issues the same number of copies.
+  uint32_t poff[UPW];
 #pragma unroll
   for (int j = 0; j < UPW; ++j) {
     const int row = (4 * j + wave) * T::RPU + lane / CPR;
-    poff[j] = row * (int)prow + (((lane % CPR) ^ at::swz(row, CPR)) << 3);
+    poff[j] = (uint32_t)((row * (int)prow + (((lane % CPR) ^ at::swz(row, CPR)) << 3)) * 2);
   }
-  struct TileSrc {
-    const bf16 *lane[UPW];
-  };
-  auto sources = [&](int t, const bf16 *pbase, const bf16 *abase, TileSrc &ts) __attribute__((always_inline)) {
+  auto copy_tile = [&](int t, const bf16 *pbase, const bf16 *abase, uint32_t dst_stage) __attribute__((always_inline)) {
     const int kt0 = k0 + max(0, min(t, nkt - 1)) * TK;
     if (kt0 >= it.kbeg && kt0 + TK <= it.P) {
       const bf16 *b = pbase + (size_t)kt0 * prow;
 #pragma unroll
-      for (int j = 0; j < UPW; ++j) ts.lane[j] = b + poff[j];
+      for (int j = 0; j < UPW; ++j)
+        if (4 * j + wave < T::UNITS) dma_1k_s(b, poff[j], dst_stage + (4 * j + wave) * 1024);
     } else {
       // Recomputed from an opaque copy of the lane index at every use, so the
       // compiler does not hoist these per-lane addresses out of the key loop
-      // (they would hold registers for the whole loop).
+      // (they would hold registers for the whole item).
       int ln = lane;
       asm volatile("" : "+v"(ln));
 #pragma unroll
       for (int j = 0; j < UPW; ++j) {
+        if (4 * j + wave >= T::UNITS) continue;
         const int row = (4 * j + wave) * T::RPU + ln / CPR;
         const int c = (ln % CPR) ^ at::swz(row, CPR);
         const int key = max(kt0 + row, it.kbeg);
         const bool pre = key < it.P;
         const long roff = (pre ? (long)key * (long)prow : (long)(key - it.P) * ldq) + c * 8;
-        ts.lane[j] = (pre ? pbase : abase) + roff;
+        dma_1k((pre ? pbase : abase) + roff, dst_stage + (4 * j + wave) * 1024);
       }
     }
   };
-  // Copy c of a group: K tile -> K stage kst (c < UPW), V tile -> V stage vst.
-  auto copy = [&](const TileSrc &k, const TileSrc &v, int kst, int vst, int c) __attribute__((always_inline)) {
-    const int j = c % UPW;
-    if (4 * j + wave >= T::UNITS / 2) return;
-    const uint32_t dst = lds0 + (c < UPW ? kst : 4 + vst) * TILEB + (4 * j + wave) * 1024;
-    dma_1k(c < UPW ? k.lane[j] : v.lane[j], dst);
-  };
+  auto kstage = [&](int s) { return lds0 + (uint32_t)(s * TILEB); };
+  auto vstage = [&](int s) { return lds0 + (uint32_t)((KST + s) * TILEB); };
 
-  // K operand: row lane%32, logical chunk 2 ks + half.  The swizzle touches
-  // the low four chunk bits only, so k-steps 8 apart differ by 256 bytes.
+  // K operand: row lane%32, logical chunk 2 ks + half at physical chunk
+  // (2 ks + half) ^ swz(row).  The swizzle's upper bits act on bits 5.. of
+  // the byte offset, which the row offset (a multiple of ROWB >= 64) and the
+  // 1 KB-aligned ring leave clear, so the address of k-step ks < 8 is one
+  // base XOR 32 ks; k-steps 8 apart differ by 256 bytes (an immediate).
   const int krow = lane & 31;
-  constexpr int NKO = NS < 8 ? NS : 8;
-  uint32_t kb[NKO];
-#pragma unroll
-  for (int i = 0; i < NKO; ++i) {
-    kb[i] = lds0 + krow * ROWB + (((2 * i + half) ^ at::swz(krow, CPR)) << 4);
-    asm volatile("" : "+v"(kb[i]));   // a lane base: stage offsets become immediates
+  uint32_t kbase;
+  {
+    const int sw = at::swz(krow, CPR);
+    kbase = (lds0 + krow * ROWB + ((half ^ (sw & 1)) << 4)) ^ ((uint32_t)(sw >> 1) << 5);
   }
   // V transpose reads: source lane s of 16-lane group G16 reads 8 bytes at
   // row 16 ks + 4 half + s/4 (and 8 rows further), head-dim column
-  // 32 n + 16 G16 + 4 (s%4).  The row's swizzle does not depend on ks, and
-  // output tiles 4 apart differ by 256 bytes.
+  // 32 n + 16 G16 + 4 (s%4).  Output tile n < 4 sits at base XOR 64 n (the
+  // swizzle's upper bits act on bits 6-7 only); tiles 4 apart differ by 256
+  // bytes, k-steps by 16 rows.
   const int src16 = lane & 15, g16 = (lane >> 4) & 1;
-  const int vcol = 16 * g16 + 4 * (src16 & 3);
-  constexpr int NVO = NT < 4 ? NT : 4;
-  uint32_t vb[2][NVO];
+  uint32_t vbase[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int r = half * 4 + (src16 >> 2) + 8 * h;
     const int sw = at::swz(r, CPR);
-#pragma unroll
-    for (int n = 0; n < NVO; ++n) {
-      const int x = n * 32 + vcol;
-      vb[h][n] = lds0 + 4 * TILEB + r * ROWB + (((x >> 3) ^ sw) << 4) + ((x & 7) << 1);
-      asm volatile("" : "+v"(vb[h][n]));
-    }
+    const int cl = (2 * g16 + ((src16 >> 1) & 1)) ^ (sw & 3);
+    vbase[h] = (lds0 + KST * TILEB + r * ROWB + 16 * cl + 8 * (src16 & 1)) ^ ((uint32_t)(sw >> 2) << 6);
   }
-  // Fragment j of a step (K stage ks, V stage vs): j < NS is K k-step j (S^T
-  // operand); the others are V^T k-step (j - NS) / NT, output tile (j - NS) % NT.
-  auto load_frag = [&](int kst, int vst, int j) __attribute__((always_inline)) -> bf16x8 {
-    if (j < NS) return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8 *>(lds_ptr(kb[j % 8]) + kst * TILEB + (j / 8) * 256);
-    const int ks = (j - NS) / NT, n = (j - NS) % NT;
+  auto kfrag = [&](int kst, int i) __attribute__((always_inline)) -> bf16x8 {
+    return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8 *>(
+        lds_ptr(kbase ^ (uint32_t)(32 * (i % 8))) + kst * TILEB + (i / 8) * 256);
+  };
+  auto vfrag = [&](int vst, int j) __attribute__((always_inline)) -> bf16x8 {
+    const int ks = j / NT, n = j % NT;
     const int c = vst * TILEB + (n / 4) * 256 + ks * 16 * ROWB;
-    return lds_tr_pair(lds_ptr(vb[0][n % 4]) + c, lds_ptr(vb[1][n % 4]) + c);
+    const uint32_t x = (uint32_t)(64 * (n % 4));
+    return lds_tr_pair(lds_ptr(vbase[0] ^ x) + c, lds_ptr(vbase[1] ^ x) + c);
+  };
+
+  // Q^T operand of group g, held for the whole item: lane holds
+  // Q[row][16 s + 8 half .. + 7] for its row; rows past the item's queries
+  // read the item's first row instead (their results are never stored).
+  bf16x8 qf[NG][NS];
+  auto load_q = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int loc = 32 * (wave + 4 * g) + (lane & 31);
+      const int qrow = it.q0 + (loc < it.nq ? loc : 0);
+      const bf16 *qp = qkv + (size_t)(it.tok_off + qrow / G) * a.ldqkv + (size_t)(it.kvh * G + qrow % G) * HD + half * 8;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) qf[g][s] = *reinterpret_cast<const bf16x8 *>(qp + 16 * s);
+    }
   };
 
   f32x16 o[NG][NT];
@@ -243,141 +244,115 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   // 2^64 (room to spare below fp32 overflow for the sums), the block runs the
   // item a second time with the true max as reference, where P <= 1.  Either
   // way the output accumulators are only touched by MFMAs in the loop.  The
-  // two 32-lane halves hold different keys of the same query: after the first
-  // tile they keep their own running max and sum, combined at the end.
-  float m_ref[NG], m_true[NG], l_run[NG], mb[NG];
+  // two 32-lane halves hold different keys of the same query: they keep their
+  // own sums, combined at the end.
+  float m_ref[NG], m_true[NG], l_run[NG];
 #pragma unroll
   for (int g = 0; g < NG; ++g) m_true[g] = -INFINITY;
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
   const float over = 64.0f / sl2;           // raw score excess that asks for the second pass
   int ovf = 0;
 
-  // One step = NF slots in a fixed order (sched_barrier fences keep the
-  // compiler from regrouping them): slot j issues the LDS read of fragment
-  // j + 2 and the MFMAs of fragment j, so every MFMA finds its operand two
-  // reads ahead.  S^T (32 keys x 32 queries; lane = query lane%32, register
-  // r = key (r/4)*8 + 4 half + r%4) accumulates in kChains independent MFMA
-  // chains per group (k-steps alternate between them).  The copies
-  // of the next group are spread evenly over the slots; the softmax of this
-  // tile (P^T for the next step) fills the PV slots from slot NS + 1.
-  bf16x8 pp[NG][2];   // P^T of the previous tile: PV k-step ks uses registers 8 ks .. 8 ks + 7
-  auto run_step = [&](auto has_s_t, auto has_pv_t, int t, int kst, int vst, int kref, int vref)
-                      __attribute__((always_inline)) {
-    constexpr bool HAS_S = decltype(has_s_t)::value, HAS_PV = decltype(has_pv_t)::value;
-    constexpr bool COPY = HAS_S && HAS_PV;
-    constexpr int J0 = HAS_S ? 0 : NS, J1 = HAS_PV ? NF : NS;
-    constexpr int CSTRIDE = at::kSpreadCopies ? NF / NCP : 1;   // slots between copies
-    TileSrc ksrc, vsrc;
-    if constexpr (COPY) {
-      sources(t + 3, pk, ak, ksrc);
-      sources(t + 2, pv, av, vsrc);
-    }
-    f32x16 s[NG][at::kChains];
-    float tmax[NG], psum[NG];
-    bf16x8 pn[NG][2];
-#pragma unroll
-    for (int g = 0; g < NG; ++g)
-#pragma unroll
-      for (int c = 0; c < at::kChains; ++c)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[g][c][r] = 0.f;
-#pragma unroll
-    for (int g = 0; g < NG; ++g) { tmax[g] = -INFINITY; psum[g] = 0.f; }
-    // Softmax of scores r, r + 1 of group g (a step after the first tile).
-    auto soft_pair = [&](int g, int r) __attribute__((always_inline)) {
-      float x0 = s[g][0][r], x1 = s[g][0][r + 1];
-      if (at::kChains == 2) { x0 += s[g][1][r]; x1 += s[g][1][r + 1]; }
-      tmax[g] = fmaxf(tmax[g], fmaxf(x0, x1));
-      const float e0 = __builtin_amdgcn_exp2f(fmaf(x0, sl2, mb[g]));
-      const float e1 = __builtin_amdgcn_exp2f(fmaf(x1, sl2, mb[g]));
-      psum[g] += e0;
-      psum[g] += e1;
-      pn[g][r >> 3][r & 7] = (bf16)e0;
-      pn[g][r >> 3][(r & 7) + 1] = (bf16)e1;
-      // Keep the work in this slot: the values are only used a step later,
-      // and the compiler would otherwise move it next to that use.
-      asm volatile("" : "+v"(pn[g][r >> 3]), "+v"(psum[g]), "+v"(tmax[g]));
-    };
-    constexpr int NPAIR = 8 * NG;                        // score pairs per tile
-    constexpr int SOFT0 = NS + 1;                        // first slot that takes softmax work
-    constexpr int NSOFT = NF - SOFT0;                    // slots that take it
-    bf16x8 fr[3];
-#pragma unroll
-    for (int j = J0; j < J0 + 2 && j < J1; ++j) fr[j % 3] = load_frag(kst, vst, j);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int j = J0; j < J1; ++j) {
-      if (j + 2 < J1) fr[(j + 2) % 3] = load_frag(kst, vst, j + 2);
-      if (COPY && j % CSTRIDE == 0 && j / CSTRIDE < NCP) copy(ksrc, vsrc, kref, vref, j / CSTRIDE);
-      if (j < NS) {
-#pragma unroll
-        for (int g = 0; g < NG; ++g) {
-          f32x16 &acc = s[g][j % at::kChains];
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[j % 3], qf[g][j], acc, 0, 0, 0);
-        }
-      } else {
-        const int ks = (j - NS) / NT, n = (j - NS) % NT;
-#pragma unroll
-        for (int g = 0; g < NG; ++g) o[g][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[j % 3], pp[g][ks], o[g][n], 0, 0, 0);
-        if (HAS_S && j >= SOFT0) {
-          // pairs [p0, p1) of this slot, spread evenly over the softmax slots
-          const int p0 = (j - SOFT0) * NPAIR / NSOFT, p1 = (j - SOFT0 + 1) * NPAIR / NSOFT;
-#pragma unroll
-          for (int p = p0; p < p1; ++p) soft_pair(p / 8, 2 * (p % 8));
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (HAS_S && HAS_PV) {
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        m_true[g] = fmaxf(m_true[g], tmax[g]);
-        ovf |= tmax[g] > m_ref[g] + over;
-        l_run[g] += psum[g];
-        pp[g][0] = pn[g][0];
-        pp[g][1] = pn[g][1];
-      }
-    }
-  };
-  // The first tile: S, then its softmax whole (it may set the reference max
-  // and carries the mask of keys below the range).
-  auto first_tile = [&](bool set_ref) __attribute__((always_inline)) {
-    f32x16 s[NG];
+  // S^T (32 keys x 32 queries; lane = query lane%32, register r = key
+  // (r/4)*8 + 4 half + r%4) of K stage kst for every group.  Each slot (one
+  // scheduling region) issues the read of fragment i + 2 and the MFMAs of
+  // fragment i, so reads run two ahead and no more fragments are held in
+  // registers (the same holds for the V^T fragments of O^T += V^T P^T).
+  auto scores = [&](int kst, f32x16 (&s)[NG]) __attribute__((always_inline)) {
 #pragma unroll
     for (int g = 0; g < NG; ++g)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
+    bf16x8 fr[3];
+    fr[0] = kfrag(kst, 0);
+    fr[1] = kfrag(kst, 1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int ks = 0; ks < NS; ++ks) {
-      const bf16x8 kf = load_frag(0, 0, ks);
+    for (int i = 0; i < NS; ++i) {
+      if (i + 2 < NS) fr[(i + 2) % 3] = kfrag(kst, i + 2);
 #pragma unroll
-      for (int g = 0; g < NG; ++g) s[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[g][ks], s[g], 0, 0, 0);
+      for (int g = 0; g < NG; ++g) s[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i % 3], qf[g][i], s[g], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  // O^T += V^T P^T over V stage vst: P^T k-step ks is registers 8 ks .. 8 ks + 7
+  // of the score tile (keys permuted identically on both operands).
+  auto pv_acc = [&](int vst, const bf16x8 (&pp)[NG][2]) __attribute__((always_inline)) {
+    constexpr int NJ = 2 * NT;
+    bf16x8 fr[3];
+    fr[0] = vfrag(vst, 0);
+    fr[1] = vfrag(vst, 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (j + 2 < NJ) fr[(j + 2) % 3] = vfrag(vst, j + 2);
+      const int ks = j / NT, n = j % NT;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) o[g][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[j % 3], pp[g][ks], o[g][n], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // Softmax of one tile into P^T; first: the item's first tile (masks keys
+  // below the range and may set the reference max).
+  auto softmax = [&](f32x16 (&s)[NG], bf16x8 (&pp)[NG][2], bool first, bool set_ref) __attribute__((always_inline)) {
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
+      if (first) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
-        if (key < it.kbeg) s[g][r] = -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
+          if (key < it.kbeg) s[g][r] = -INFINITY;
+        }
       }
-      float tmax = s[g][0];
+      float tmax = fmaxf(s[g][0], s[g][1]);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) tmax = fmaxf(tmax, s[g][r]);
-      if (set_ref) m_ref[g] = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      mb[g] = -m_ref[g] * sl2;
+      for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, s[g][r]);
+      if (first && set_ref) m_ref[g] = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float mb = -m_ref[g] * sl2;
       m_true[g] = fmaxf(m_true[g], tmax);
       ovf |= tmax > m_ref[g] + over;
-      float ps = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pe = __builtin_amdgcn_exp2f(fmaf(s[g][r], sl2, mb[g]));
-        ps += pe;
-        pp[g][r >> 3][r & 7] = (bf16)pe;
+      for (int r = 0; r < 16; ++r) s[g][r] = __builtin_amdgcn_exp2f(fmaf(s[g][r], sl2, mb));
+      float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        ps0 += s[g][r];
+        ps1 += s[g][r + 1];
+        pp[g][r >> 3][r & 7] = (bf16)s[g][r];
+        pp[g][r >> 3][(r & 7) + 1] = (bf16)s[g][r + 1];
       }
-      l_run[g] += ps;
+      l_run[g] += ps0 + ps1;
     }
   };
 
+  // vmcnt after which this wave's copies of K tile t and V tile t have landed
+  // at step t: the K copies of tile t + 1 (issued last) may still be in flight.
+  constexpr int WAIT = at::waitcnt_vm(UPW);
+  // Step t with K tile t in K stage KS = t % 3 and V tile t in V stage VS =
+  // t % 2 (compile-time, so every stage offset is an immediate): wait for
+  // both, refill the stages tile t - 1 left with V tile t + 1 and K tile
+  // t + 2, then S, softmax and O += P V.  The LDS bases are re-pinned per step
+  // so the compiler keeps one register per base rather than hoisting every
+  // derived address out of the loop.
+  auto step = [&](int t, auto ks_t, auto vs_t, bool first, bool set_ref) __attribute__((always_inline)) {
+    constexpr int KS = decltype(ks_t)::value, VS = decltype(vs_t)::value;
+    __builtin_amdgcn_s_waitcnt(WAIT);       // this wave's copies of K tile t and V tile t have landed
+    __builtin_amdgcn_s_barrier();           // ... and every wave's; the stages of tile t - 1 are free
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("" : "+v"(kbase), "+v"(vbase[0]), "+v"(vbase[1]));
+    copy_tile(t + 1, pv, av, vstage(VS ^ 1));
+    copy_tile(t + 2, pk, ak, kstage((KS + 2) % 3));
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 sc[NG];
+    scores(KS, sc);
+    bf16x8 pp[NG][2];
+    softmax(sc, pp, first, set_ref);
+    __builtin_amdgcn_sched_barrier(0);
+    pv_acc(VS, pp);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
   for (int pass = 0; pass < 2; ++pass) {
     const bool pass0 = pass == 0;
 #pragma unroll
@@ -388,63 +363,48 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[g][n][r] = 0.f;
     }
-    // Step t (1 <= t < nkt): wait for copy group t, refill with group t + 3
-    // (K tile t + 3 into the stage K tile t - 1 left, V tile t + 2 into the
-    // stage V tile t - 2 left), S of tile t, O += P V of tile t - 1, P of
-    // tile t.  Copy group j = K tile j and V tile j - 1.
-    auto step = [&](int t, int kst, int vst, int kref, int vref) __attribute__((always_inline)) {
-      __builtin_amdgcn_s_waitcnt(T::WAIT);    // this wave's copies of group t have landed
-      __builtin_amdgcn_s_barrier();           // ... and every wave's; the refilled stages are free
-      __builtin_amdgcn_sched_barrier(0);
-      run_step(std::true_type{}, std::true_type{}, t, kst, vst, kref, vref);
-    };
+    // Prologue: K tile 0, V tile 0, K tile 1 (then Q on the first pass, all in
+    // flight together).
+    copy_tile(0, pk, ak, kstage(0));
+    copy_tile(0, pv, av, vstage(0));
+    copy_tile(1, pk, ak, kstage(1));
+    if (pass0) {
+      load_q();
+      // Wait here for Q (and so for the copies issued before it): the key
+      // loop then holds no wait for loads the compiler knows of, which would
+      // also wait for the copies issued inside the loop.
 #pragma unroll
-    for (int j = 0; j < 3; ++j) {
-      TileSrc ksrc, vsrc;
-      sources(j, pk, ak, ksrc);
-      sources(j - 1, pv, av, vsrc);
+      for (int g = 0; g < NG; ++g)
 #pragma unroll
-      for (int c = 0; c < NCP; ++c) copy(ksrc, vsrc, j, (j + 3) & 3, c);
-      if (j == 0 && pass0) load_q();        // lands with copy group 0
+        for (int i = 0; i < NS; ++i) asm volatile("" : "+v"(qf[g][i]));
     }
-    {   // step 0: S and P of the first tile, refill with group 3
-      __builtin_amdgcn_s_waitcnt(T::WAIT);
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      TileSrc ksrc, vsrc;
-      sources(3, pk, ak, ksrc);
-      sources(2, pv, av, vsrc);
-#pragma unroll
-      for (int c = 0; c < NCP; ++c) copy(ksrc, vsrc, 3, 2, c);
-      first_tile(pass0);
+    step(0, I0{}, I0{}, true, pass0);
+    // Steps 1 .. nkt - 1, six per round (the period of the two rings).
+    for (int t = 1; t < nkt;) {
+      step(t, I1{}, I1{}, false, false);
+      if (++t >= nkt) break;
+      step(t, I2{}, I0{}, false, false);
+      if (++t >= nkt) break;
+      step(t, I0{}, I1{}, false, false);
+      if (++t >= nkt) break;
+      step(t, I1{}, I0{}, false, false);
+      if (++t >= nkt) break;
+      step(t, I2{}, I1{}, false, false);
+      if (++t >= nkt) break;
+      step(t, I0{}, I0{}, false, false);
+      ++t;
     }
-    // Whole groups of four steps, then the last one to three steps.
-    int t = 1;
-    for (; t + 4 <= nkt; t += 4) {
-      step(t, 1, 0, 0, 3);
-      step(t + 1, 2, 1, 1, 0);
-      step(t + 2, 3, 2, 2, 1);
-      step(t + 3, 0, 3, 3, 2);
-    }
-    if (t < nkt) {
-      step(t, 1, 0, 0, 3);
-      if (t + 1 < nkt) {
-        step(t + 1, 2, 1, 1, 0);
-        if (t + 2 < nkt) step(t + 2, 3, 2, 2, 1);
-      }
-    }
-    // O += P V of the last tile, once every copy has landed.
-    __builtin_amdgcn_s_waitcnt(T::WAIT0);   // no copy may outlive the pass (or the block's LDS)
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    switch ((nkt - 1) & 3) {
-      case 0: run_step(std::false_type{}, std::true_type{}, 0, 0, 0, 0, 0); break;
-      case 1: run_step(std::false_type{}, std::true_type{}, 0, 0, 1, 0, 0); break;
-      case 2: run_step(std::false_type{}, std::true_type{}, 0, 0, 2, 0, 0); break;
-      default: run_step(std::false_type{}, std::true_type{}, 0, 0, 3, 0, 0); break;
-    }
-    // Block-uniform decision: every wave has finished reading the stages.
-    if (!pass0 || !__syncthreads_or(ovf)) break;
+    __builtin_amdgcn_s_waitcnt(at::waitcnt_vm(0));   // no copy may outlive the pass (or the block's LDS)
+    __syncthreads();                                 // every wave's copies have landed and its reads are done
+    if (!pass0) break;
+    // Block-wide vote on the second pass, through the (now idle) ring memory.
+    uint32_t *vote = reinterpret_cast<uint32_t *>(smem);
+    const bool any = __ballot(ovf != 0) != 0;
+    if (lane == 0) vote[wave] = any ? 1u : 0u;
+    __syncthreads();
+    const uint32_t again = vote[0] | vote[1] | vote[2] | vote[3];
+    __syncthreads();                                 // the votes are read before the copies refill the rings
+    if (!again) break;
 #pragma unroll
     for (int g = 0; g < NG; ++g) m_ref[g] = fmaxf(m_true[g], __shfl_xor(m_true[g], 32, 64));
   }
@@ -452,7 +412,6 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
   // Accumulator layout: lane holds query (lane & 31) of the group; register r
   // of tile n holds head-dim index 32 n + (r/4)*8 + 4 half + r%4.
   constexpr int CPRO = HD / 8;              // 16-byte chunks per output row
-  static_assert(4 * NG * 32 * 2 * HD <= 8 * TILEB, "output staging fits the rings");
   __syncthreads();                          // every wave is done with the rings
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
@@ -460,7 +419,7 @@ __global__ void __launch_bounds__(256, 1) attention_bf16_kernel(AttnArgs a) {
     const int loc = 32 * (wave + 4 * g) + (lane & 31);
     if (loc >= it.nq) continue;
     if (it.slot < 0) {
-      // Through LDS (the K ring, free now): lane q writes its query row's 8-byte
+      // Through LDS (the rings, free now): lane q writes its query row's 8-byte
       // pieces, chunk c of a row at c ^ (q % CPRO); then rows go out as whole
       // 16-byte chunks, consecutive lanes on consecutive chunks of a row.
       const float inv = 1.0f / l_all;

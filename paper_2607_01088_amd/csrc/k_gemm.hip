@@ -9,6 +9,7 @@
 // stores its slice's fp32 product (kEpiPartial) and a second kernel sums the
 // slices in order and applies the epilogue.
 #include <algorithm>
+#include <atomic>
 
 #include "rosa_device.h"
 #include "rosa_internal.h"
@@ -527,18 +528,23 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs g) {
   }
 }
 
+// Compute units of the current device, cached per device (any host thread).
+static int device_cu_count() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
 hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int force_cfg) {
   if (g.M <= 0) return hipSuccess;
   if (bf16_mode) {
-    static int n_cu = 0;
-    if (n_cu == 0) {
-      int dev = 0, v = 0;
-      if (hipGetDevice(&dev) == hipSuccess &&
-          hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-        n_cu = v;
-      else
-        n_cu = 256;
-    }
+    const int n_cu = device_cu_count();
     if (force_cfg >= 0) return launch_cfg(g, force_cfg, s, false);
     return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true);
   }

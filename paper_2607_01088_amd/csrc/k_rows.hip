@@ -6,6 +6,7 @@
 // one 64-lane wavefront owns one row so that the RMS reduction is a single
 // wave reduction with no block barrier.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "rosa_device.h"
@@ -261,12 +262,12 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
   const int resident = lds_res <= kLdsMax ? 1 : 0;
   const size_t lds = resident ? lds_res : ((size_t)kFinalChunk * a_pad + (size_t)R * d) * sizeof(float);
   if (lds > kLdsMax) return hipErrorInvalidValue;
-  static bool lds_raised = false;   // the attribute is per function: raise it to the maximum once
-  if (!lds_raised) {
+  static std::atomic<bool> lds_raised{false};   // the attribute is per function: raise it to the maximum once
+  if (!lds_raised.load(std::memory_order_acquire)) {
     const hipError_t e = hipFuncSetAttribute((const void *)final_euler_kernel,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e != hipSuccess) return e;
-    lds_raised = true;
+    lds_raised.store(true, std::memory_order_release);
   }
   // Resident: one block per CU walks the groups (W_out is loaded once per block).
   const int blocks = resident ? std::min(groups, 256) : std::min(groups, 1024);
@@ -365,12 +366,12 @@ hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, co
   const int nb = A <= 32 ? 1 : 2;
   const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
   const size_t lds = (size_t)nb * 32 * kc * 2;
-  static bool lds_raised[2] = {false, false};
-  if (!lds_raised[nb - 1]) {
+  static std::atomic<bool> lds_raised[2];   // zero-initialized (static storage)
+  if (!lds_raised[nb - 1].load(std::memory_order_acquire)) {
     const hipError_t e = hipFuncSetAttribute(nb == 1 ? (const void *)out_proj_euler_kernel<1> : (const void *)out_proj_euler_kernel<2>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     if (e != hipSuccess) return e;
-    lds_raised[nb - 1] = true;
+    lds_raised[nb - 1].store(true, std::memory_order_release);
   }
   const int nrb = (M + 31) / 32;
   const int blocks = std::min((nrb + 3) / 4, 256);

@@ -933,12 +933,21 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
         }
       }
     }
-    // Join: the caller's stream waits for every lane.
-    for (int li = 1; li < nl && e == hipSuccess; ++li) {
-      e = hipEventRecord(b->ev_join[li], b->lane_stream[li]);
-      if (e == hipSuccess) e = hipStreamWaitEvent(b->stream, b->ev_join[li], 0);
+    // Join: the caller's stream waits for every lane.  After a failed launch
+    // the lanes are still joined (and then drained), so that no lane can be
+    // reading the caller's buffers or the handle's workspaces once the call
+    // has returned its error.
+    const hipError_t launch_err = e;
+    hipError_t join_err = hipSuccess;
+    for (int li = 1; li < nl; ++li) {
+      hipError_t j = hipEventRecord(b->ev_join[li], b->lane_stream[li]);
+      if (j == hipSuccess) j = hipStreamWaitEvent(b->stream, b->ev_join[li], 0);
+      if (j != hipSuccess && join_err == hipSuccess) join_err = j;
     }
-    if (e != hipSuccess) return device_fail(b, e, "kernel launch");
+    if (launch_err != hipSuccess || join_err != hipSuccess) {
+      for (int li = 0; li < nl; ++li) (void)hipStreamSynchronize(b->lane_stream[li]);
+      return device_fail(b, launch_err != hipSuccess ? launch_err : join_err, "kernel launch");
+    }
     return ROSA_OK;
   } catch (const std::bad_alloc &) {
     return fail(b, ROSA_E_NOMEM, "host allocation failed");
@@ -952,6 +961,8 @@ void rosa_destroy(rosa_batch *b) {
   try {
     hipSetDevice(b->device);
     hipStreamSynchronize(b->stream);
+    for (int l = 1; l < kMaxLanes; ++l)
+      if (b->lane_stream[l]) hipStreamSynchronize(b->lane_stream[l]);
     free_all(b);
   } catch (...) {
   }
@@ -988,6 +999,27 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
       }
       counts[3] = (int32_t)(p.sets[0].groups.size() + p.sets[1].groups.size());
     }
+    return ROSA_OK;
+  } catch (...) {
+    return ROSA_E_NOMEM;
+  }
+}
+
+rosa_status rosa_debug_plan_lanes(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
+                                  int32_t n, int32_t lanes, int32_t *lane_of) {
+  try {
+    if (!cfg || !cap || !lane_of || lanes < 1 || lanes > kMaxLanes) return ROSA_E_INVALID;
+    rosa_status st = check_config(cfg);
+    if (st != ROSA_OK) return st;
+    st = check_capacity(cap);
+    if (st != ROSA_OK) return st;
+    const int nl = cfg->dtype == ROSA_BF16 ? std::max(1, std::min<int>(lanes, n / kMinLaneRequests)) : 1;
+    Plan p;
+    std::string err;
+    st = build_plan(cfg, cap, reqs, n, true, cfg->dtype == ROSA_BF16, nl, p, err);
+    if (st != ROSA_OK) return st;
+    for (int l = 0; l < (int)p.lanes.size(); ++l)
+      for (int i = p.lanes[l].req_lo; i < p.lanes[l].req_hi; ++i) lane_of[p.order[i]] = l;
     return ROSA_OK;
   } catch (...) {
     return ROSA_E_NOMEM;

@@ -47,8 +47,9 @@ static_assert(sizeof(AttnGroup) == 32, "AttnGroup is 32 bytes");
 
 constexpr int kAttnQB = 256;       // most query rows per attention work item (4 waves x 2 x 32)
 // 32-row query groups per wave of the bf16 attention kernel: two where Q^T and
-// O^T of both fit the register file.  Work items hold at most 128 x this rows.
-constexpr int attn_groups_per_wave(int hd) { return hd <= 128 ? 2 : 1; }
+// O^T of both fit half the register file (two waves share a SIMD), one from
+// head_dim 128.  Work items hold at most 128 x this rows.
+constexpr int attn_groups_per_wave(int hd) { return hd <= 64 ? 2 : 1; }
 // Keys of a query block are split over several work items only while a
 // launch has fewer than kAttnSplitTarget items; a split item holds at least
 // kAttnMinSplitKeys keys; at most kAttnMaxSlots partial-result slots per launch.

@@ -145,6 +145,9 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_plan.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32,
                                     C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)]
     lib.rosa_debug_plan.restype = C.c_int
+    lib.rosa_debug_plan_lanes.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32, i32,
+                                          C.POINTER(i32)]
+    lib.rosa_debug_plan_lanes.restype = C.c_int
     lib.rosa_debug_time_conditioning.argtypes = [vp, C.POINTER(C.c_float), i32, vp]
     lib.rosa_debug_time_conditioning.restype = C.c_int
     lib.rosa_debug_attention.argtypes = [vp, C.POINTER(Request), i32, i32, vp, vp]
@@ -232,6 +235,16 @@ def plan(shape, dtype: str, cap: Capacity, reqs: Sequence[Request]):
     counts = (C.c_int32 * 4)()
     st = lib.rosa_debug_plan(C.byref(cfg), C.byref(cap), arr, n, order, tok, mk, counts)
     return st, list(order)[:n], list(tok)[:n], list(mk)[:cap.max_steps], list(counts)
+
+
+def plan_lanes(shape, dtype: str, cap: Capacity, reqs: Sequence[Request], lanes: int):
+    """Host-only lane assignment (rosa_debug_plan_lanes): (status, lane of each request)."""
+    lib = load()
+    cfg = model_config(shape, dtype)
+    n = len(reqs)
+    out = (C.c_int32 * max(1, n))()
+    st = lib.rosa_debug_plan_lanes(C.byref(cfg), C.byref(cap), request_array(reqs), n, lanes, out)
+    return st, list(out)[:n]
 
 
 def s1_simulate(robots: int, batch: int, batch_ms: float, t_act_ms: float, n_batches: int = 256) -> Dict[str, float]:

@@ -11,6 +11,20 @@ import numpy as np
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
+def _shape(**kw):
+    from synthetic import ModelShape
+    return ModelShape(**kw)
+
+
+# Whole-call and attention tests at the head widths the presets do not use:
+# grouped-query attention with two query heads per KV head at head_dim 64,
+# plain multi-head attention at head_dim 128.
+HD64_SHAPE = _shape(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64, d_mlp=512, action_dim=7,
+                    time_emb_dim=128)
+HD128_SHAPE = _shape(n_layers=3, d_model=384, n_q_heads=3, n_kv_heads=3, head_dim=128, d_mlp=768, action_dim=14,
+                     time_emb_dim=64)
+
+
 def declared_functions() -> List[str]:
     """Every function the public headers declare."""
     names = []

@@ -86,6 +86,26 @@ def test_plan_no_split_for_a_full_batch():
     assert counts[1] == counts[2] == 640 and counts[3] == 0
 
 
+def test_plan_lanes_balance_and_cover_every_request():
+    """Lane assignment (rosa_debug_plan_lanes): every request gets a lane, both
+    lanes of a 256-request factory-shaped set carry similar work, and fewer
+    than 64 requests per lane keep a single lane."""
+    import numpy as np
+    rng = np.random.default_rng(1)
+    reqs = [req(int(rng.integers(512, 1281)), int(rng.choice([16, 50])), int(rng.choice([5, 10]))) for _ in range(256)]
+    cap = rosa.capacity(256, 50, 256 * 50, 10, 256 * 1280)
+    st, lanes = rosa.plan_lanes(PI0_SHAPE, "bf16", cap, reqs, 2)
+    assert st == rosa.ROSA_OK and sorted(set(lanes)) == [0, 1]
+    work = [0.0, 0.0]
+    for r, l in zip(reqs, lanes):
+        work[l] += r.horizon * r.num_steps * (1.0 + (r.prefix_len + r.horizon) / 1800.0)
+    assert abs(work[0] - work[1]) / sum(work) < 0.01
+    st, lanes = rosa.plan_lanes(PI0_SHAPE, "bf16", cap, reqs[:100], 2)
+    assert st == rosa.ROSA_OK and set(lanes) == {0}
+    st, lanes = rosa.plan_lanes(PI0_SHAPE, "fp32", cap, reqs, 2)
+    assert st == rosa.ROSA_OK and set(lanes) == {0}
+
+
 @pytest.mark.parametrize("bad,status", [
     (dict(P=-1), rosa.ROSA_E_INVALID),
     (dict(H=0), rosa.ROSA_E_INVALID),

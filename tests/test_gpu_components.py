@@ -37,6 +37,22 @@ def tiny_bf16():
 
 
 @pytest.fixture(scope="module")
+def hd64_bf16():
+    from tests.helpers import HD64_SHAPE
+    e, w = _expert(HD64_SHAPE, "bf16")
+    yield e, w
+    e.close()
+
+
+@pytest.fixture(scope="module")
+def hd128_bf16():
+    from tests.helpers import HD128_SHAPE
+    e, w = _expert(HD128_SHAPE, "bf16")
+    yield e, w
+    e.close()
+
+
+@pytest.fixture(scope="module")
 def pi0_bf16():
     e, w = _expert(PI0_SHAPE, "bf16", max_requests=160, max_tokens=160 * 50)
     yield e, w
@@ -177,8 +193,11 @@ def _attn_case(e, shapes, seed, fill_q=None, tags=None):
         k = rng.standard_normal((L, P + guard, nkv, hd)).astype(np.float32)
         v = rng.standard_normal((L, P + guard, nkv, hd)).astype(np.float32)
         if tags is not None:
-            v[:] = tags[i]
-            qkv[row:row + H, (nq + nkv) * hd:] = tags[i]
+            # one tag per request, or one per (request, KV head)
+            t = np.broadcast_to(np.asarray(tags[i], dtype=np.float32), (nkv,))
+            for j in range(nkv):
+                v[:, :, j, :] = t[j]
+                qkv[row:row + H, (nq + nkv + j) * hd:(nq + nkv + j + 1) * hd] = t[j]
         k[:, P:] = np.nan                                # guard tokens after each prefix
         v[:, P:] = np.nan
         if dtype == "bf16":
@@ -216,6 +235,9 @@ def _oracle_attn(sh, qkv, host, layer):
 ATTN_CASES = {
     "tiny": [(64, 8), (96, 8), (0, 3), (1, 1), (65, 5)],
     "pi0_ragged": [(816, 50), (63, 16), (64, 1), (65, 50), (0, 16), (2048, 50), (1, 16)],
+    # head_dim 64 / 128 shapes: several 32-key tiles, ragged tails, P = 0 and 1,
+    # one and several query blocks, a prefix long enough to split over items
+    "head_dims": [(97, 17), (0, 5), (1, 1), (64, 33), (300, 50), (1500, 50), (31, 16)],
 }
 
 
@@ -300,3 +322,45 @@ def test_attention_tag_bitwise(which, case, request):
     got = _thost(o)
     for (P, H), (_, _, row, _), t in zip(shapes, host, tags):
         assert np.array_equal(got[row:row + H], np.full_like(got[row:row + H], t)), (P, H)
+
+
+@pytest.mark.parametrize("which", ["hd64_bf16", "hd128_bf16"])
+@pytest.mark.parametrize("layer_sel", ["first", "last"])
+def test_attention_head_dims_matches_oracle(which, layer_sel, request):
+    """The bf16 attention kernel at head_dim 64 (two query heads per KV head,
+    two KV heads) and 128 (three KV heads, one query head each), element by
+    element against the oracle; nothing is written past the batch."""
+    e, _ = request.getfixturevalue(which)
+    sh = e.shape
+    layer = 0 if layer_sel == "first" else sh.n_layers - 1
+    shapes = ATTN_CASES["head_dims"]
+    qkv, qkv_d, o, structs, host, keep = _attn_case(e, shapes, seed=11)
+    e.attention(structs, layer, qkv_d, o)
+    got = _thost(o)
+    refs = _oracle_attn(sh, qkv, host, layer)
+    M = sum(H for _, H in shapes)
+    assert np.isnan(got[M:]).all()
+    for (P, H), (_, _, row, _), ref in zip(shapes, host, refs):
+        err = rel_l2(got[row:row + H], ref)
+        assert err < 1e-2, (P, H, err)
+
+
+@pytest.mark.parametrize("which", ["hd64_bf16", "hd128_bf16"])
+def test_attention_head_dims_tag_bitwise(which, request):
+    """Q = 0 and every value of KV head j of request r equal to its own tag
+    t_rj: each output of query head g is exactly t_r(g // G), so a wrong KV
+    head, request or row offset fails bitwise."""
+    e, _ = request.getfixturevalue(which)
+    sh = e.shape
+    nq, nkv, hd = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    G = nq // nkv
+    shapes = ATTN_CASES["head_dims"]
+    tags = [[float(4 * i + j + 1) for j in range(nkv)] for i in range(len(shapes))]
+    qkv, qkv_d, o, structs, host, keep = _attn_case(e, shapes, seed=3, fill_q=0.0, tags=tags)
+    e.attention(structs, sh.n_layers - 1, qkv_d, o)
+    got = _thost(o)
+    for (P, H), (_, _, row, _), t in zip(shapes, host, tags):
+        want = np.empty((H, nq, hd), dtype=np.float32)
+        for g in range(nq):
+            want[:, g, :] = t[g // G]
+        assert np.array_equal(got[row:row + H].reshape(H, nq, hd), want), (P, H)

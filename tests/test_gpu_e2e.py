@@ -35,6 +35,9 @@ def _run(expert, requests, dtype):
 
 
 def _check(got, requests, weights, shape, tol, label):
+    """Each chunk against the oracle: rel-L2 of x_K, and (bf16 gate) rel-L2 of
+    the displacement x_K - x_0, which attention moves by a larger fraction
+    than it moves x_K."""
     om = OracleModel(weights, shape)
     worst = 0.0
     for i, (g, r) in enumerate(zip(got, requests)):
@@ -45,6 +48,8 @@ def _check(got, requests, weights, shape, tol, label):
               f"(displacement {disp:.3e})", flush=True)
         worst = max(worst, err)
         assert err <= tol, (i, err)
+        if tol >= 1e-3:
+            assert disp <= tol, (i, disp)
     return worst
 
 
@@ -118,6 +123,59 @@ def test_factory_b256_full_batch_sampled(pi0_expert):
     for g in got:
         assert np.isfinite(g).all()
     _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "factory_b256")
+
+
+@pytest.mark.timeout(900)
+def test_pi0_b32_preset_sampled(pi0_expert):
+    """The 32-robot pi0 preset (prefixes 600-1024 tokens, each with its own KV
+    cache) in one call: the longest and shortest prefix and two more requests
+    against the oracle, every chunk finite."""
+    e, w = pi0_expert
+    p = PRESETS["pi0_b32"]
+    reqs = make_requests(p)
+    got, _ = _run(e, reqs, "bf16")
+    meta = make_metadata(p)
+    pick = sorted({int(np.argmax([m.prefix_len for m in meta])), int(np.argmin([m.prefix_len for m in meta])), 7, 20})
+    for g in got:
+        assert np.isfinite(g).all()
+    _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "pi0_b32")
+
+
+@pytest.mark.timeout(900)
+def test_factory_b256_attention_isolating_both_lanes():
+    """The benchmark's whole batch with the MLP removed and the attention gate
+    biased to one, so that attention decides the result: the default call
+    (two lanes, per-step launch lists), checked on one request per
+    horizon x steps class in each lane plus the longest and shortest prefix
+    among each lane's ten-step requests (the only ones active in steps 5-9)."""
+    from paper_2607_01088_amd import rosa
+    base = cached_weights(PI0_SHAPE, "bf16")
+    w = _attention_isolating(base, PI0_SHAPE)
+    p = PRESETS["factory_b256"]
+    meta = make_metadata(p)
+    e = _expert(PI0_SHAPE, "bf16", w, max_requests=256, max_prefix=256 * 1280)
+    reqs = make_requests(p)
+    db = rosa.DeviceBatch(reqs, "bf16")
+    st, lanes = rosa.plan_lanes(PI0_SHAPE, "bf16", e.cap, db.structs, 2)
+    assert st == 0 and sorted(set(lanes)) == [0, 1]
+    e.generate(db.structs)
+    torch.cuda.synchronize()
+    got = db.results()
+    for g in got:
+        assert np.isfinite(g).all()
+    pick = set()
+    for lane in (0, 1):
+        mine = [i for i in range(len(meta)) if lanes[i] == lane]
+        for H in (16, 50):
+            for K in (5, 10):
+                pick.add(next(i for i in mine if meta[i].horizon == H and meta[i].steps == K))
+        ten = [i for i in mine if meta[i].steps == 10]
+        pick.add(max(ten, key=lambda i: meta[i].prefix_len))
+        pick.add(min(ten, key=lambda i: meta[i].prefix_len))
+    pick = sorted(pick)
+    print("lanes of the checked requests:", [lanes[i] for i in pick], flush=True)
+    _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "factory_b256 isolating")
+    e.close()
 
 
 @pytest.mark.timeout(900)

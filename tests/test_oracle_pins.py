@@ -6,7 +6,7 @@ import math
 import numpy as np
 import pytest
 
-from oracle import (OracleModel, attention, gelu_tanh, rms_norm, tau_grid, timestep_embedding)
+from oracle import (OracleModel, attention, gelu_tanh, rms_norm, silu, tau_grid, timestep_embedding)
 from synthetic import ModelShape, TINY_SHAPE, custom_request, make_weights
 
 pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
@@ -146,6 +146,35 @@ def test_gelu_tanh_against_erf_gelu():
     assert gelu_tanh(np.array([0.0]))[0] == 0.0
     assert abs(gelu_tanh(np.array([10.0]))[0] - 10.0) < 1e-12
     assert abs(gelu_tanh(np.array([-10.0]))[0]) < 1e-12
+
+
+def test_gelu_tanh_pinned_values():
+    """The tanh form's published cubic coefficient 0.044715 and its sqrt(2/pi)
+    scale, pinned at points where they are fixed in closed form: at x = 1 the
+    argument of tanh is sqrt(2/pi) * 1.044715, at x = 2 it is sqrt(2/pi) *
+    (2 + 8 * 0.044715).  A coefficient off by 1e-9 moves these values by more
+    than the tolerance.  The odd part of any x * (1 + tanh(odd(x))) / 2 is x / 2,
+    so gelu(x) - gelu(-x) = x exactly in real arithmetic."""
+    k = math.sqrt(2.0 / math.pi)
+    assert abs(gelu_tanh(np.array([1.0]))[0] - 0.5 * (1.0 + math.tanh(k * 1.044715))) < 1e-15
+    assert abs(gelu_tanh(np.array([2.0]))[0] - (1.0 + math.tanh(k * 2.35772))) < 1e-15
+    assert abs(gelu_tanh(np.array([1.0]))[0] - 0.8411919906082768) < 1e-14   # 0.5 (1 + tanh(0.83356197))
+    x = np.linspace(-5.0, 5.0, 101)
+    np.testing.assert_allclose(gelu_tanh(x) - gelu_tanh(-x), x, rtol=0, atol=1e-14)
+
+
+def test_silu_closed_forms():
+    """SiLU(x) = x sigmoid(x): sigmoid(ln 3) = 3/4 gives SiLU(ln 3) = 0.75 ln 3,
+    sigmoid(-ln 3) = 1/4; sigmoid(x) + sigmoid(-x) = 1 gives SiLU(x) - SiLU(-x) = x;
+    SiLU(0) = 0 and SiLU(x) -> x, 0 at the two ends."""
+    l3 = math.log(3.0)
+    assert abs(silu(np.array([l3]))[0] - 0.75 * l3) < 1e-15
+    assert abs(silu(np.array([-l3]))[0] + 0.25 * l3) < 1e-15
+    assert silu(np.array([0.0]))[0] == 0.0
+    x = np.linspace(-8.0, 8.0, 161)
+    np.testing.assert_allclose(silu(x) - silu(-x), x, rtol=0, atol=1e-14)
+    assert abs(silu(np.array([40.0]))[0] - 40.0) < 1e-12
+    assert abs(silu(np.array([-40.0]))[0]) < 1e-12
 
 
 # ------------------------------------------------------------------ Euler closed forms
