@@ -182,6 +182,37 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
 /* Wait for the handle's stream, then free everything.  NULL-safe. */
 void rosa_destroy(rosa_batch *b);
 
+/* Ragged prefix + action attention of one layer that allocates nothing: for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  It needs no handle.
+ * Computes exactly what rosa_generate_actions computes at layer `layer` of
+ * cfg's expert: each action token of request r attends over r's prefix keys
+ * and values of that layer followed by r's own action keys and values (or,
+ * with ROSA_ATTN_ALTERNATING, the prefix in even layers and the action keys in
+ * odd layers), grouped-query heads, scale 1/sqrt(head_dim).
+ *   reqs[n]: prefix_k / prefix_v / prefix_len / horizon / num_steps are read
+ *            and validated as in rosa_generate_actions (noise and actions are
+ *            not touched); rows follow the caller's request order.
+ *   qkv: DEVICE [sum H][(n_q+2n_kv)*head_dim] in cfg's dtype, 16-byte aligned:
+ *        the fused q | k | v projection of every request's action tokens.
+ *   o:   DEVICE [sum H][n_q*head_dim] in cfg's dtype, 16-byte aligned, written.
+ *   hip_stream: hipStream_t the work is enqueued on (NULL = default stream).
+ * The plan of the call and the partial results of key ranges split over
+ * several work items live in a library-owned device array of 16.7 MiB per GPU
+ * (obtained once per device, held until the process ends): at most 1024
+ * requests, 4096 attention work items and 64 split partials per call (fewer
+ * key splits are made than rosa_generate_actions would make for a small
+ * batch, so results can differ from it by rounding).  Every call on one GPU
+ * reuses that array, so calls that overlap on a GPU (other streams, other
+ * host threads) race; stream-ordered calls do not.  The plan is copied from
+ * host memory with hipMemcpyAsync.  Errors: ROSA_E_INVALID, ROSA_E_UNSUPPORTED
+ * (as rosa_batch_create for cfg, as rosa_generate_actions for the requests;
+ * also misaligned qkv / o or a layer outside [0, n_layers)), ROSA_E_CAPACITY
+ * (beyond the limits above), ROSA_E_DEVICE (HIP failure); rosa_last_error(NULL)
+ * gives the detail.  n == 0 is a no-op. */
+rosa_status rosa_attention_noalloc(const rosa_model_config *cfg, const rosa_request *reqs, int32_t n,
+                                   int32_t layer, const void *qkv, void *o, void *hip_stream);
+
 /* Static text for a status code. */
 const char *rosa_status_string(rosa_status s);
 

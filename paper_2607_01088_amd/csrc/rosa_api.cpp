@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -285,7 +286,7 @@ int attn_set_of(const rosa_model_config *cfg, int layer) {
 // Validation of a request set (all-or-nothing) and the batch plan.
 rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
                        int n, bool sort_by_steps, bool allow_split, int lanes_wanted, Plan &p, std::string &err,
-                       int max_steps_call = INT32_MAX) {
+                       int max_steps_call = INT32_MAX, int max_slots = -1) {
   if (n < 0) { err = "n_reqs < 0"; return ROSA_E_INVALID; }
   if (n > 0 && !reqs) { err = "reqs is NULL"; return ROSA_E_INVALID; }
   if (n > cap->max_requests) { err = "more requests than max_requests"; return ROSA_E_CAPACITY; }
@@ -412,7 +413,12 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
   p.n_sets = alternating ? 2 : 1;
   int64_t total_qb = 0;
   for (int i = 0; i < n; ++i) total_qb += (int64_t)cfg->n_kv_heads * attn_query_blocks(reqs[i].horizon * G, gpb);
-  const bool split = allow_split && total_qb > 0 && total_qb < kSplitTarget;
+  // Partial-result slots available per attention set (every split item takes one).
+  const int64_t slot_budget = (max_slots < 0 ? (int64_t)p.n_sets * kMaxSlots : (int64_t)max_slots) / p.n_sets;
+  const int64_t want_all = total_qb > 0 ? (kSplitTarget + total_qb - 1) / total_qb : 1;
+  const int64_t want_fit = total_qb > 0 ? slot_budget / total_qb : 0;
+  const int want_split = (int)std::min(want_all, want_fit);
+  const bool split = allow_split && total_qb > 0 && total_qb < kSplitTarget && want_split >= 2;
   for (int v = 0; v < p.n_sets; ++v) {
     Plan::AttnSet &S = p.sets[v];
     if (v == 1) { S.item_base = (int)p.sets[0].items.size(); S.group_base = (int)p.sets[0].groups.size(); }
@@ -426,7 +432,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
       const int R = r.horizon * G, ngrp = (R + 31) / 32, nqb = attn_query_blocks(R, gpb);
       int nsplit = 1, chunk = nk;
       if (split) {
-        const int want = (int)((kSplitTarget + total_qb - 1) / total_qb);
+        const int want = want_split;
         const int most = std::max(1, (nk + kMinSplitKeys - 1) / kMinSplitKeys);
         nsplit = std::min(want, most);
         chunk = (nk + nsplit - 1) / nsplit;
@@ -455,7 +461,10 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
       S.groups_upto[i] = (int)S.groups.size();
     }
   }
-  if (p.slots > p.n_sets * kMaxSlots) { err = "internal: attention partial slots exceeded"; return ROSA_E_CAPACITY; }
+  if (p.slots > (max_slots < 0 ? p.n_sets * kMaxSlots : max_slots)) {
+    err = "internal: attention partial slots exceeded";
+    return ROSA_E_CAPACITY;
+  }
 
   // Attention launch orders, one per set and distinct set of active requests
   // of a lane; entries index the whole device item array.
@@ -654,6 +663,53 @@ void free_all(rosa_batch *b) {
   b->ev_fork = nullptr;
 }
 
+}  // namespace
+
+// ====================================================================== allocation-free attention
+// Scratch of rosa_attention_noalloc: the plan of a call (request descriptors,
+// work items, merge groups, the block -> item table) and the partial results
+// of key ranges split over several items.  One copy per GPU, held until the
+// process ends; every call on a GPU reuses it (calls that overlap on one GPU
+// race).  Nothing in it has to start at zero: each call uploads its plan and
+// every partial slot is written by its item before the merge reads it.
+namespace {
+constexpr int kNaMaxRequests = 1024;
+constexpr int kNaMaxItems = 4096;          // work items, and blocks of the launch order
+constexpr int kNaMaxSlots = 64;            // partial-result slots (query blocks x key splits)
+constexpr int kNaMaxHeadDim = 256;
+constexpr size_t kNaOffReqs = 0;
+constexpr size_t kNaOffItems = kNaOffReqs + (size_t)kNaMaxRequests * sizeof(ReqDesc);
+constexpr size_t kNaOffGroups = kNaOffItems + (size_t)kNaMaxItems * sizeof(AttnItem);
+constexpr size_t kNaOffLists = kNaOffGroups + (size_t)kNaMaxSlots * sizeof(AttnGroup);
+constexpr size_t kNaOffMl = kNaOffLists + (size_t)kNaMaxItems * sizeof(AttnItem);
+constexpr size_t kNaOffO = kNaOffMl + (size_t)kNaMaxSlots * kAttnQB * 2 * sizeof(float);
+constexpr size_t kNaBytes = kNaOffO + (size_t)kNaMaxSlots * kAttnQB * kNaMaxHeadDim * sizeof(float);
+static_assert(kNaOffItems % 256 == 0 && kNaOffGroups % 256 == 0 && kNaOffLists % 256 == 0 &&
+              kNaOffMl % 256 == 0 && kNaOffO % 256 == 0, "scratch regions stay 256-byte aligned");
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kNaBytes];
+
+namespace {
+// Device address of `scratch` on the current device.  The array's name is a
+// host-side stand-in in host code; the address comes from the runtime, once
+// per device (with that device current), and is cached.
+hipError_t noalloc_scratch(int dev, uint8_t **out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static uint8_t *addr[kMaxDevices] = {};
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    addr[dev] = static_cast<uint8_t *>(ptr);
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 }  // namespace
 
 // ====================================================================== C ABI
@@ -1061,6 +1117,103 @@ rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_
     return ROSA_OK;
   } catch (...) {
     return fail(b, ROSA_E_DEVICE, "unexpected exception");
+  }
+}
+
+rosa_status rosa_attention_noalloc(const rosa_model_config *cfg, const rosa_request *reqs, int32_t n, int32_t layer,
+                                   const void *qkv, void *o, void *hip_stream) {
+  try {
+    g_create_error.clear();
+    if (!cfg) return fail(nullptr, ROSA_E_INVALID, "cfg is NULL");
+    rosa_status st = check_config(cfg);
+    if (st != ROSA_OK) return fail(nullptr, st, "model configuration not supported");
+    if (n < 0 || (n > 0 && !reqs) || layer < 0 || layer >= cfg->n_layers)
+      return fail(nullptr, ROSA_E_INVALID, "bad request count, request array or layer");
+    if (n > kNaMaxRequests) return fail(nullptr, ROSA_E_CAPACITY, "more than 1024 requests");
+    if (n == 0) return ROSA_OK;
+    if (!qkv || !o || ((uintptr_t)qkv | (uintptr_t)o) & 15)
+      return fail(nullptr, ROSA_E_INVALID, "qkv and o must be non-NULL and 16-byte aligned");
+    // Capacity of exactly this request set (build_plan validates every request).
+    rosa_capacity cap{};
+    cap.max_requests = n;
+    cap.max_steps = 1;
+    int64_t sum_h = 0, sum_p = 0;
+    for (int i = 0; i < n; ++i) {
+      cap.max_horizon = std::max(cap.max_horizon, reqs[i].horizon);
+      cap.max_steps = std::max(cap.max_steps, reqs[i].num_steps);
+      sum_h += std::max(reqs[i].horizon, 0);
+      sum_p += std::max(reqs[i].prefix_len, 0);
+    }
+    if (sum_h > INT32_MAX || cap.max_steps > kMaxSteps)
+      return fail(nullptr, ROSA_E_INVALID, "sum of horizons or a step count out of range");
+    cap.max_action_tokens = (int32_t)std::max<int64_t>(sum_h, 1);
+    cap.max_horizon = std::max(cap.max_horizon, 1);
+    cap.max_prefix_tokens = sum_p;
+    const bool bf16 = cfg->dtype == ROSA_BF16;
+    Plan p;
+    std::string err;
+    st = build_plan(cfg, &cap, reqs, n, false, bf16, 1, p, err, INT32_MAX, kNaMaxSlots);
+    if (st != ROSA_OK) return fail(nullptr, st, err);
+    const Plan::AttnSet &S0 = p.sets[0], &S1 = p.sets[1];
+    const size_t n_items = S0.items.size() + S1.items.size(), n_groups = S0.groups.size() + S1.groups.size();
+    if (n_items > (size_t)kNaMaxItems || n_groups > (size_t)kNaMaxSlots || p.attn_lists.size() > (size_t)kNaMaxItems)
+      return fail(nullptr, ROSA_E_CAPACITY, "more than 4096 attention work items or launch blocks");
+
+    // Host image of the plan regions, copied into the scratch in one transfer.
+    std::vector<uint8_t> img(kNaOffMl, 0);
+    ReqDesc *rd = reinterpret_cast<ReqDesc *>(img.data() + kNaOffReqs);
+    for (int i = 0; i < n; ++i) {
+      const rosa_request &r = reqs[p.order[i]];
+      ReqDesc d{};
+      d.pk = r.prefix_k; d.pv = r.prefix_v; d.noise = r.noise; d.actions = r.actions;
+      d.P = r.prefix_len; d.H = r.horizon; d.K = r.num_steps; d.tok_off = p.tok_off[i]; d.orig = p.order[i];
+      d.k0 = r.start_step; d.S = p.steps[i];
+      rd[i] = d;
+    }
+    std::vector<AttnItem> all(S0.items);
+    all.insert(all.end(), S1.items.begin(), S1.items.end());
+    std::memcpy(img.data() + kNaOffItems, all.data(), all.size() * sizeof(AttnItem));
+    std::memcpy(img.data() + kNaOffGroups, S0.groups.data(), S0.groups.size() * sizeof(AttnGroup));
+    std::memcpy(img.data() + kNaOffGroups + S0.groups.size() * sizeof(AttnGroup), S1.groups.data(),
+                S1.groups.size() * sizeof(AttnGroup));
+    attn_order_items(all, p.attn_lists.data(), p.attn_lists.size(), reinterpret_cast<AttnItem *>(img.data() + kNaOffLists));
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    uint8_t *sp = nullptr;
+    if (e == hipSuccess) e = noalloc_scratch(dev, &sp);
+    const hipStream_t stream = (hipStream_t)hip_stream;
+    const size_t used = kNaOffLists + p.attn_lists.size() * sizeof(AttnItem);
+    if (e == hipSuccess) e = hipMemcpyAsync(sp, img.data(), used, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return device_fail(nullptr, e, "scratch address or plan upload");
+
+    const Dims D = make_dims(cfg);
+    const Plan::Lane &ln = p.lanes[0];
+    const int v = attn_set_of(cfg, layer);
+    const Plan::AttnSet &S = p.sets[v];
+    AttnArgs a{};
+    a.items = reinterpret_cast<const AttnItem *>(sp + kNaOffItems) + S.item_base;
+    a.n_items = (int)S.items.size();
+    if (bf16) {
+      a.items = reinterpret_cast<const AttnItem *>(sp + kNaOffItems);
+      a.ordered = reinterpret_cast<const AttnItem *>(sp + kNaOffLists) + ln.list_at[v][0];
+      a.n_blocks = ln.list_blocks[v][0];
+    }
+    a.reqs = reinterpret_cast<const ReqDesc *>(sp + kNaOffReqs);
+    a.layer = layer;
+    a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
+    a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
+    a.part_o = reinterpret_cast<float *>(sp + kNaOffO);
+    a.part_ml = reinterpret_cast<float *>(sp + kNaOffMl);
+    e = launch_attention(a, bf16, stream);
+    if (e == hipSuccess && !S.groups.empty())
+      e = launch_attn_merge(reinterpret_cast<const AttnGroup *>(sp + kNaOffGroups) + S.group_base, (int)S.groups.size(),
+                            a.reqs, a.part_o, a.part_ml, o, D.o_dim, D.nq, D.nkv, D.hd, bf16, stream);
+    return e == hipSuccess ? ROSA_OK : device_fail(nullptr, e, "attention launch");
+  } catch (const std::bad_alloc &) {
+    return fail(nullptr, ROSA_E_NOMEM, "host allocation failed");
+  } catch (...) {
+    return fail(nullptr, ROSA_E_DEVICE, "unexpected exception");
   }
 }
 

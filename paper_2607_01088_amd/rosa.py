@@ -145,6 +145,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_plan.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32,
                                     C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)]
     lib.rosa_debug_plan.restype = C.c_int
+    lib.rosa_attention_noalloc.argtypes = [C.POINTER(ModelConfig), C.POINTER(Request), i32, i32, vp, vp, vp]
+    lib.rosa_attention_noalloc.restype = C.c_int
     lib.rosa_debug_plan_lanes.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32, i32,
                                           C.POINTER(i32)]
     lib.rosa_debug_plan_lanes.restype = C.c_int
@@ -235,6 +237,24 @@ def plan(shape, dtype: str, cap: Capacity, reqs: Sequence[Request]):
     counts = (C.c_int32 * 4)()
     st = lib.rosa_debug_plan(C.byref(cfg), C.byref(cap), arr, n, order, tok, mk, counts)
     return st, list(order)[:n], list(tok)[:n], list(mk)[:cap.max_steps], list(counts)
+
+
+def attention_noalloc(shape, dtype: str, reqs: Sequence[Request], layer: int, qkv, o,
+                      stream: Optional[int] = None) -> int:
+    """rosa_attention_noalloc (no handle, no allocation) on torch tensors qkv and o;
+    returns the status."""
+    import torch
+    lib = load()
+    cfg = model_config(shape, dtype)
+    if stream is None:
+        stream = torch.cuda.current_stream().cuda_stream
+    return lib.rosa_attention_noalloc(C.byref(cfg), request_array(reqs), len(reqs), layer, C.c_void_p(qkv.data_ptr()),
+                                      C.c_void_p(o.data_ptr()), C.c_void_p(stream))
+
+
+def last_error_global() -> str:
+    """rosa_last_error(NULL): detail of the last failure of a handle-free call."""
+    return load().rosa_last_error(None).decode()
 
 
 def plan_lanes(shape, dtype: str, cap: Capacity, reqs: Sequence[Request], lanes: int):
