@@ -239,18 +239,16 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   f32x16 o[NG][NT];
   // Softmax without rescaling the output inside the key loop: each query's
   // reference max m_ref is its max over the item's first 32-key tile, and
-  // P = 2^((s - m_ref) log2(e) / sqrt(hd)) may exceed 1.  The loop tracks the
-  // true max; if any query's later scores exceed its reference by more than
-  // 2^64 (room to spare below fp32 overflow for the sums), the block runs the
-  // item a second time with the true max as reference, where P <= 1.  Either
-  // way the output accumulators are only touched by MFMAs in the loop.  The
-  // two 32-lane halves hold different keys of the same query: they keep their
-  // own sums, combined at the end.
+  // P = 2^((s - m_ref) log2(e) / sqrt(hd)) may exceed 1.  If a tile's sum of P
+  // exceeds 2^64 (room to spare below fp32 overflow for the running sums),
+  // the block finds every query's true max and runs the item again with it as
+  // reference, where P <= 1.  Either way the output accumulators are only
+  // touched by MFMAs in the loop.  The two 32-lane halves hold different keys
+  // of the same query: they keep their own sums, combined at the end.
   float m_ref[NG], m_true[NG], l_run[NG];
 #pragma unroll
   for (int g = 0; g < NG; ++g) m_true[g] = -INFINITY;
   const float sl2 = 1.4426950408889634f / sqrtf((float)HD);   // log2(e) / sqrt(hd)
-  const float over = 64.0f / sl2;           // raw score excess that asks for the second pass
   int ovf = 0;
 
   // S^T (32 keys x 32 queries; lane = query lane%32, register r = key
@@ -259,10 +257,6 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   // fragment i, so reads run two ahead and no more fragments are held in
   // registers (the same holds for the V^T fragments of O^T += V^T P^T).
   auto scores = [&](int kst, f32x16 (&s)[NG]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int g = 0; g < NG; ++g)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[g][r] = 0.f;
     bf16x8 fr[3];
     fr[0] = kfrag(kst, 0);
     fr[1] = kfrag(kst, 1);
@@ -271,7 +265,11 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
     for (int i = 0; i < NS; ++i) {
       if (i + 2 < NS) fr[(i + 2) % 3] = kfrag(kst, i + 2);
 #pragma unroll
-      for (int g = 0; g < NG; ++g) s[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i % 3], qf[g][i], s[g], 0, 0, 0);
+      for (int g = 0; g < NG; ++g) {
+        // the first k-step accumulates onto an inline zero (no register clearing)
+        const f32x16 c = i == 0 ? f32x16{} : s[g];
+        s[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[i % 3], qf[g][i], c, 0, 0, 0);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -292,36 +290,53 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // Softmax of one tile into P^T; first: the item's first tile (masks keys
-  // below the range and may set the reference max).
-  auto softmax = [&](f32x16 (&s)[NG], bf16x8 (&pp)[NG][2], bool first, bool set_ref) __attribute__((always_inline)) {
+  // Keys of the item's first tile below its key range take no weight.
+  auto mask_first = [&](f32x16 (&s)[NG]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
+        if (key < it.kbeg) s[g][r] = -INFINITY;
+      }
+  };
+  auto tile_max = [&](const f32x16 &s) __attribute__((always_inline)) -> float {
+    float tmax = fmaxf(s[0], s[1]);
+#pragma unroll
+    for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, s[r]);
+    return tmax;
+  };
+  // Softmax of one tile into P^T (bf16) and its sum.  The sum is taken over
+  // the bf16 values that enter O += V^T P^T (two per dot-product instruction),
+  // so numerator and denominator see the same weights.  A sum above 2^64 (or
+  // not finite) means a score overshot the reference by about that much: the
+  // block then finds the true maxima and runs the item again.
+  auto softmax = [&](f32x16 (&s)[NG], bf16x8 (&pp)[NG][2]) __attribute__((always_inline)) {
+    typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+    const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      if (first) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + (r >> 2) * 8 + half * 4 + (r & 3);
-          if (key < it.kbeg) s[g][r] = -INFINITY;
-        }
-      }
-      float tmax = fmaxf(s[g][0], s[g][1]);
-#pragma unroll
-      for (int r = 2; r < 16; ++r) tmax = fmaxf(tmax, s[g][r]);
-      if (first && set_ref) m_ref[g] = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
       const float mb = -m_ref[g] * sl2;
-      m_true[g] = fmaxf(m_true[g], tmax);
-      ovf |= tmax > m_ref[g] + over;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[g][r] = __builtin_amdgcn_exp2f(fmaf(s[g][r], sl2, mb));
-      float ps0 = 0.f, ps1 = 0.f;
+      // Pairs are packed one at a time and P^T is assembled from the packed
+      // words (extracting words from a packed bf16 vector was mis-lowered).
+      float ps = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        ps0 += s[g][r];
-        ps1 += s[g][r + 1];
-        pp[g][r >> 3][r & 7] = (bf16)s[g][r];
-        pp[g][r >> 3][(r & 7) + 1] = (bf16)s[g][r + 1];
+      for (int h = 0; h < 2; ++h) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          bf16x2 p2;
+          p2[0] = (bf16)s[g][8 * h + 2 * e];
+          p2[1] = (bf16)s[g][8 * h + 2 * e + 1];
+          ps = __builtin_amdgcn_fdot2_f32_bf16(p2, ones, ps, false);
+          w[e] = __builtin_bit_cast(uint32_t, p2);
+        }
+        pp[g][h] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
       }
-      l_run[g] += ps0 + ps1;
+      ovf |= !(ps <= 0x1p64f);
+      l_run[g] += ps;
     }
   };
 
@@ -334,8 +349,12 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   // t + 2, then S, softmax and O += P V.  The LDS bases are re-pinned per step
   // so the compiler keeps one register per base rather than hoisting every
   // derived address out of the loop.
-  auto step = [&](int t, auto ks_t, auto vs_t, bool first, bool set_ref) __attribute__((always_inline)) {
-    constexpr int KS = decltype(ks_t)::value, VS = decltype(vs_t)::value;
+  //   MODE 0: softmax against m_ref and O += P V; on the first tile (t == 0)
+  //           the keys below the range are masked and, if set_ref, m_ref is
+  //           set to the first tile's maxima.
+  //   MODE 1: the maxima only (m_true), for a block whose first pass overflowed.
+  auto step = [&](int t, auto ks_t, auto vs_t, auto mode_t, bool set_ref) __attribute__((always_inline)) {
+    constexpr int KS = decltype(ks_t)::value, VS = decltype(vs_t)::value, MODE = decltype(mode_t)::value;
     __builtin_amdgcn_s_waitcnt(WAIT);       // this wave's copies of K tile t and V tile t have landed
     __builtin_amdgcn_s_barrier();           // ... and every wave's; the stages of tile t - 1 are free
     __builtin_amdgcn_sched_barrier(0);
@@ -345,30 +364,46 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     f32x16 sc[NG];
     scores(KS, sc);
-    bf16x8 pp[NG][2];
-    softmax(sc, pp, first, set_ref);
-    __builtin_amdgcn_sched_barrier(0);
-    pv_acc(VS, pp);
+    if (t == 0) mask_first(sc);
+    if constexpr (MODE == 1) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) m_true[g] = fmaxf(m_true[g], tile_max(sc[g]));
+    } else {
+      if (t == 0 && set_ref) {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const float tmax = tile_max(sc[g]);
+          m_ref[g] = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+        }
+      }
+      bf16x8 pp[NG][2];
+      softmax(sc, pp);
+      __builtin_amdgcn_sched_barrier(0);
+      pv_acc(VS, pp);
+    }
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
-  for (int pass = 0; pass < 2; ++pass) {
-    const bool pass0 = pass == 0;
+  // One pass over the item's key tiles in the given mode.
+  auto key_pass = [&](auto mode_t, bool set_ref, bool first_pass) __attribute__((always_inline)) {
+    constexpr int MODE = decltype(mode_t)::value;
+    if constexpr (MODE == 0) {
 #pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      l_run[g] = 0.f;
+      for (int g = 0; g < NG; ++g) {
+        l_run[g] = 0.f;
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[g][n][r] = 0.f;
+          for (int r = 0; r < 16; ++r) o[g][n][r] = 0.f;
+      }
     }
     // Prologue: K tile 0, V tile 0, K tile 1 (then Q on the first pass, all in
     // flight together).
     copy_tile(0, pk, ak, kstage(0));
     copy_tile(0, pv, av, vstage(0));
     copy_tile(1, pk, ak, kstage(1));
-    if (pass0) {
+    if (first_pass) {
       load_q();
       // Wait here for Q (and so for the copies issued before it): the key
       // loop then holds no wait for loads the compiler knows of, which would
@@ -378,35 +413,43 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < NS; ++i) asm volatile("" : "+v"(qf[g][i]));
     }
-    step(0, I0{}, I0{}, true, pass0);
+    step(0, I0{}, I0{}, mode_t, set_ref);
     // Steps 1 .. nkt - 1, six per round (the period of the two rings).
     for (int t = 1; t < nkt;) {
-      step(t, I1{}, I1{}, false, false);
+      step(t, I1{}, I1{}, mode_t, false);
       if (++t >= nkt) break;
-      step(t, I2{}, I0{}, false, false);
+      step(t, I2{}, I0{}, mode_t, false);
       if (++t >= nkt) break;
-      step(t, I0{}, I1{}, false, false);
+      step(t, I0{}, I1{}, mode_t, false);
       if (++t >= nkt) break;
-      step(t, I1{}, I0{}, false, false);
+      step(t, I1{}, I0{}, mode_t, false);
       if (++t >= nkt) break;
-      step(t, I2{}, I1{}, false, false);
+      step(t, I2{}, I1{}, mode_t, false);
       if (++t >= nkt) break;
-      step(t, I0{}, I0{}, false, false);
+      step(t, I0{}, I0{}, mode_t, false);
       ++t;
     }
     __builtin_amdgcn_s_waitcnt(at::waitcnt_vm(0));   // no copy may outlive the pass (or the block's LDS)
     __syncthreads();                                 // every wave's copies have landed and its reads are done
-    if (!pass0) break;
-    // Block-wide vote on the second pass, through the (now idle) ring memory.
+  };
+
+  // First pass against the first tile's maxima.  If any wave saw a sum
+  // overflow, the block takes the true maxima in a second pass and runs the
+  // item again against them (every P <= 1 then).
+  key_pass(I0{}, true, true);
+  {
     uint32_t *vote = reinterpret_cast<uint32_t *>(smem);
     const bool any = __ballot(ovf != 0) != 0;
     if (lane == 0) vote[wave] = any ? 1u : 0u;
     __syncthreads();
     const uint32_t again = vote[0] | vote[1] | vote[2] | vote[3];
     __syncthreads();                                 // the votes are read before the copies refill the rings
-    if (!again) break;
+    if (again) {
+      key_pass(I1{}, false, false);
 #pragma unroll
-    for (int g = 0; g < NG; ++g) m_ref[g] = fmaxf(m_true[g], __shfl_xor(m_true[g], 32, 64));
+      for (int g = 0; g < NG; ++g) m_ref[g] = fmaxf(m_true[g], __shfl_xor(m_true[g], 32, 64));
+      key_pass(I0{}, false, false);
+    }
   }
 
   // Accumulator layout: lane holds query (lane & 31) of the group; register r
