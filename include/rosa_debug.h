@@ -37,6 +37,24 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
 rosa_status rosa_debug_plan_lanes(const rosa_model_config *cfg, const rosa_capacity *cap,
                                   const rosa_request *reqs, int32_t n, int32_t lanes, int32_t *lane_of);
 
+/* Host-only attention launch lists (bf16 configs; no GPU needed, nothing
+ * enqueued): the persistent-block lists of the first attention launch of a
+ * one-lane call over this set (step 0, every request active, the first
+ * layer's attention set).
+ *   n_blocks      : blocks launched; block b starts at entry b
+ *   n_entries     : table entries (>= n_blocks)
+ *   item_of[e]    : plan attention item of entry e (-1: an idle block)
+ *   next[e]       : the same block's next entry, -1 after its last
+ *   item_cost[i]  : 32-key steps of plan attention item i (counts[1] items of
+ *                   rosa_debug_plan, first attention set)
+ * item_of / next hold max_entries; ROSA_E_CAPACITY (counts still written)
+ * when the table is longer.  Any array pointer may be NULL.  ROSA_E_UNSUPPORTED
+ * for fp32 configs. */
+rosa_status rosa_debug_attn_lists(const rosa_model_config *cfg, const rosa_capacity *cap,
+                                  const rosa_request *reqs, int32_t n, int32_t max_entries,
+                                  int32_t *n_blocks, int32_t *n_entries, int32_t *item_of,
+                                  int32_t *next, int32_t *item_cost);
+
 /* Time conditioning alone: for n flow times taus (HOST fp32), write the
  * modulation table rows to out (DEVICE fp32 [n][L*6d + 2d]): per layer l the
  * six d-wide vectors [shift_a|scale_a|gate_a|shift_m|scale_m|gate_m] at offset

@@ -122,26 +122,46 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[T::LDSB];
   static_assert(T::RINGB <= 65536 + TILEB, "stage offsets must fit the LDS immediate");
 
-  const AttnItem it = a.ordered[blockIdx.x];
-  if (it.nq <= 0) return;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
-  const int half = lane >> 5;
+  // The block is persistent: it runs the items of its list (a.ordered[b],
+  // then each entry's `next`) one after another.
+  if (a.ordered[blockIdx.x].nq <= 0) return;
   const int G = a.nq / a.nkv;
   const bf16 *qkv = reinterpret_cast<const bf16 *>(a.qkv);
-
   const size_t prow = (size_t)a.nkv * HD;   // prefix row stride (elements)
+  const long ldq = a.ldqkv;
+  const uint32_t lds0 = lds_u32(smem);
+
+  for (int e = blockIdx.x; e >= 0;) {
+  // The item's words pass through readfirstlane: the kernel's own stores
+  // keep the compiler from proving the table unchanged (so from loading it
+  // with scalar loads), and every field must be wave-uniform.
+  AttnItem it;
+  {
+    static_assert(sizeof(AttnItem) % 4 == 0, "item is whole words");
+    const uint32_t *src = reinterpret_cast<const uint32_t *>(a.ordered + e);
+    uint32_t w[sizeof(AttnItem) / 4];
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(AttnItem) / 4); ++i) w[i] = __builtin_amdgcn_readfirstlane(src[i]);
+    __builtin_memcpy(&it, w, sizeof(AttnItem));
+  }
+  e = it.next;
+  // The thread index is taken through an opaque copy per item, so the
+  // compiler does not hoist the per-lane addresses derived from it out of the
+  // item loop (they would hold registers across every item).
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3;   // wave-uniform, in an SGPR
+  const int half = lane >> 5;
   const bf16 *pk = reinterpret_cast<const bf16 *>(it.pk) + (size_t)a.layer * it.P * prow + (size_t)it.kvh * HD;
   const bf16 *pv = reinterpret_cast<const bf16 *>(it.pv) + (size_t)a.layer * it.P * prow + (size_t)it.kvh * HD;
   const bf16 *ak = qkv + (size_t)it.tok_off * a.ldqkv + (size_t)(a.nq + it.kvh) * HD;
   const bf16 *av = qkv + (size_t)it.tok_off * a.ldqkv + (size_t)(a.nq + a.nkv + it.kvh) * HD;
-  const long ldq = a.ldqkv;
   // Tile t covers keys [k0 + 32 t, k0 + 32 t + 32) with k0 = kend - 32 nkt:
   // only tile 0 can reach below kbeg (those keys are masked), so the key
   // loop itself never masks.
   const int nkt = (it.kend - it.kbeg + TK - 1) / TK;
   const int k0 = it.kend - TK * nkt;
-  const uint32_t lds0 = lds_u32(smem);
 
   // Copies: 1 KB units, unit u of a tile by wave u % 4; lane i fills physical
   // chunk i % CPR of row u * RPU + i / CPR, which holds logical chunk
@@ -519,6 +539,8 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
         pm[1] = l_all;
       }
     }
+  }
+  __syncthreads();                          // the staging reads are done before the next item's copies
   }
 }
 

@@ -9,6 +9,7 @@
 #include <mutex>
 #include <string>
 #include <thread>
+#include <queue>
 #include <vector>
 
 #include "../../include/rosa.h"
@@ -17,49 +18,88 @@
 
 using namespace rosa;
 
-// Attention launch order.  Blocks reach the 8 XCDs round-robin (block b on
-// XCD b % 8) and each XCD starts its blocks in order as CUs free up, so:
-// requests (each a contiguous range of items) go whole to an XCD (their query
-// blocks share its L2), longest first to the least-loaded XCD, and each XCD's
-// items run longest first.  Item cost = 32-key steps + a fixed overhead.
-// Appends the block -> item table (block b = x + 8 q runs XCD x's q-th item,
-// -1: the block exits) and returns the block count.  The order never changes
-// what an item computes.
+// Attention launch order.  The kernel's blocks are persistent: block b runs
+// the items of its own list one after another, and blocks reach the 8 XCDs
+// round-robin (block b on XCD b % 8).  Two levels of longest-processing-time
+// packing (largest first onto the least loaded), so the blocks finish
+// together:
+//   - onto XCDs: a request's items go to one XCD as a unit (its query blocks
+//     read the same keys through that XCD's L2); a request holding more than
+//     1/16 of the launch's work goes item by item instead;
+//   - on each XCD: its items onto its blocks, one block per item while the
+//     busiest XCD has no more items than kAttnBlocks / 8.
+// Item cost = 32-key steps + a fixed overhead.  Appends the block lists to
+// out (item index per entry) and next (the index, relative to this table, of
+// the same block's next entry, -1 after its last): entries 0 .. n_blocks-1
+// are the blocks' first items (-1: an idle block), the others follow block
+// by block.  Returns n_blocks.  The order never changes what an item computes.
 namespace rosa {
 int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std::pair<int, int>> &ranges,
-                      std::vector<int32_t> &out) {
-  constexpr int kItemOverheadSteps = 12;   // measured fixed cost of an item, in 32-key steps
+                      std::vector<int32_t> &out, std::vector<int32_t> &next) {
+  constexpr int64_t kItemOverheadSteps = 6;   // fixed cost of an item in a persistent block, in 32-key steps
   auto icost = [&](int it) -> int64_t { return (items[it].kend - items[it].kbeg + 31) / 32 + kItemOverheadSteps; };
-  struct RC { int lo, hi; int64_t cost; };
-  std::vector<RC> rc;
+  struct Unit { int lo, hi; int64_t cost; };   // items [lo, hi) placed together
+  int64_t total = 0;
+  for (const auto &r : ranges)
+    for (int j = r.first; j < r.second; ++j) total += icost(j);
+  std::vector<Unit> units;
   for (const auto &r : ranges) {
     int64_t c = 0;
     for (int j = r.first; j < r.second; ++j) c += icost(j);
-    rc.push_back({r.first, r.second, c});
+    if (16 * c > total) {
+      for (int j = r.first; j < r.second; ++j) units.push_back({j, j + 1, icost(j)});
+    } else {
+      units.push_back({r.first, r.second, c});
+    }
   }
-  std::stable_sort(rc.begin(), rc.end(), [](const RC &a, const RC &b2) { return a.cost > b2.cost; });
+  std::stable_sort(units.begin(), units.end(), [](const Unit &a, const Unit &b2) { return a.cost > b2.cost; });
   int64_t xload[8] = {};
   std::vector<std::vector<int>> xitems(8);
-  for (const RC &r : rc) {
+  for (const Unit &u : units) {
     int best = 0;
     for (int x = 1; x < 8; ++x)
       if (xload[x] < xload[best]) best = x;
-    xload[best] += r.cost;
-    for (int it = r.lo; it < r.hi; ++it) xitems[best].push_back(it);
+    xload[best] += u.cost;
+    for (int it = u.lo; it < u.hi; ++it) xitems[best].push_back(it);
   }
-  size_t most = 0;
+  size_t most = 1;
+  for (int x = 0; x < 8; ++x) most = std::max(most, xitems[x].size());
+  const int per_x = std::min(kAttnBlocks / 8, (int)most);
+  const int nb = 8 * per_x;
+  std::vector<std::vector<int>> bins(nb);
+  using LB = std::pair<int64_t, int>;       // (load, bin) min-heap per XCD
   for (int x = 0; x < 8; ++x) {
     std::stable_sort(xitems[x].begin(), xitems[x].end(), [&](int a, int b2) { return icost(a) > icost(b2); });
-    most = std::max(most, xitems[x].size());
+    std::priority_queue<LB, std::vector<LB>, std::greater<LB>> heap;
+    for (int j = 0; j < per_x; ++j) heap.push({0, j});
+    for (int it : xitems[x]) {
+      LB lb = heap.top();
+      heap.pop();
+      bins[x + 8 * lb.second].push_back(it);
+      lb.first += icost(it);
+      heap.push(lb);
+    }
   }
   const size_t at = out.size();
-  out.resize(at + 8 * most, -1);
-  for (int x = 0; x < 8; ++x)
-    for (size_t q = 0; q < xitems[x].size(); ++q) out[at + x + 8 * q] = xitems[x][q];
-  return (int)(8 * most);
+  out.resize(at + nb, -1);
+  next.resize(at + nb, -1);
+  for (int b = 0; b < nb; ++b) {
+    if (bins[b].empty()) continue;
+    out[at + b] = bins[b][0];
+    int32_t prev = b;                       // relative index of the entry to link from
+    for (size_t q = 1; q < bins[b].size(); ++q) {
+      const int32_t e = (int32_t)(out.size() - at);
+      out.push_back(bins[b][q]);
+      next.push_back(-1);
+      next[at + prev] = e;
+      prev = e;
+    }
+  }
+  return nb;
 }
 
-void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, size_t n, AttnItem *dst) {
+void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, const int32_t *next, size_t n,
+                      AttnItem *dst) {
   for (size_t e = 0; e < n; ++e) {
     if (order[e] >= 0) {
       dst[e] = items[order[e]];
@@ -67,6 +107,7 @@ void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, 
       dst[e] = AttnItem{};
       dst[e].nq = 0;
     }
+    dst[e].next = next[e];
   }
 }
 
@@ -151,13 +192,14 @@ struct Plan {
     int req_lo = 0, req_hi = 0, row_lo = 0, row_hi = 0;
     std::vector<int32_t> n_act, m;
     // Per attention set and step: offset of the attention launch order in
-    // attn_lists, and the launch's block count (8 x the longest per-XCD item list).
+    // attn_lists, and the launch's block count.
     std::vector<int32_t> list_at[2], list_blocks[2];
   };
   std::vector<Lane> lanes;
   // Attention launch orders, one per distinct set of active requests of a
-  // lane: the item index of each block (-1: the block exits).
-  std::vector<int32_t> attn_lists;
+  // lane: the persistent blocks' item lists (item index per entry, -1: an
+  // idle block) and each entry's link to its block's next entry.
+  std::vector<int32_t> attn_lists, attn_next;
 };
 
 }  // namespace
@@ -488,7 +530,7 @@ rosa_status build_plan(const rosa_model_config *cfg, const rosa_capacity *cap, c
           ranges.push_back({i > 0 ? S.items_upto[i - 1] : 0, S.items_upto[i]});
         const size_t at = p.attn_lists.size();
         ln.list_at[v][k] = (int)at;
-        ln.list_blocks[v][k] = attn_launch_order(S.items, ranges, p.attn_lists);
+        ln.list_blocks[v][k] = attn_launch_order(S.items, ranges, p.attn_lists, p.attn_next);
         for (size_t e = at; e < p.attn_lists.size(); ++e)
           if (p.attn_lists[e] >= 0) p.attn_lists[e] += S.item_base;
       }
@@ -586,7 +628,7 @@ hipError_t upload_plan(rosa_batch *b, const Plan &p, const rosa_request *reqs, i
   {
     std::vector<AttnItem> all(S0.items);
     all.insert(all.end(), S1.items.begin(), S1.items.end());
-    attn_order_items(all, p.attn_lists.data(), p.attn_lists.size(), (AttnItem *)(hp + b->off_lists));
+    attn_order_items(all, p.attn_lists.data(), p.attn_next.data(), p.attn_lists.size(), (AttnItem *)(hp + b->off_lists));
   }
   const size_t used = b->off_lists + p.attn_lists.size() * sizeof(AttnItem);
   hipError_t e = hipMemcpyAsync(b->d_plan, hp, used, hipMemcpyHostToDevice, b->stream);
@@ -814,9 +856,9 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->off_items = align(b->off_taus + kMaxTau * 4);
     b->off_groups = align(b->off_items + (size_t)b->max_items * sizeof(AttnItem));
     b->off_lists = align(b->off_groups + (size_t)b->max_slots * sizeof(AttnGroup));
-    // one launch order per step and lane at most: the lane's items plus at most
-    // 7 empty slots per XCD row of blocks
-    b->max_list_ints = (size_t)cap->max_steps * (8 * (size_t)b->max_items + 8 * kMaxLanes * n_sets);
+    // one launch order per step and lane at most: its items plus at most as
+    // many idle first entries (n_blocks <= items + 7)
+    b->max_list_ints = (size_t)cap->max_steps * (2 * (size_t)b->max_items + 8 * kMaxLanes * n_sets);
     b->plan_bytes = align(b->off_lists + b->max_list_ints * sizeof(AttnItem));
     b->d_plan = dalloc<uint8_t>(b, b->plan_bytes, e);
     if (e != hipSuccess) {
@@ -1061,6 +1103,47 @@ rosa_status rosa_debug_plan(const rosa_model_config *cfg, const rosa_capacity *c
   }
 }
 
+rosa_status rosa_debug_attn_lists(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
+                                  int32_t n, int32_t max_entries, int32_t *n_blocks, int32_t *n_entries,
+                                  int32_t *item_of, int32_t *next, int32_t *item_cost) {
+  try {
+    if (!cfg || !cap || !n_blocks || !n_entries || max_entries < 0) return ROSA_E_INVALID;
+    if (cfg->dtype != ROSA_BF16) return ROSA_E_UNSUPPORTED;
+    rosa_status st = check_config(cfg);
+    if (st != ROSA_OK) return st;
+    st = check_capacity(cap);
+    if (st != ROSA_OK) return st;
+    Plan p;
+    std::string err;
+    st = build_plan(cfg, cap, reqs, n, true, true, 1, p, err);
+    if (st != ROSA_OK) return st;
+    *n_blocks = 0;
+    *n_entries = 0;
+    if (p.lanes.empty() || p.Kmax == 0 || p.lanes[0].list_at[0].empty() || p.lanes[0].list_at[0][0] < 0) return ROSA_OK;
+    const Plan::Lane &ln = p.lanes[0];
+    const size_t lo = (size_t)ln.list_at[0][0];
+    size_t hi = p.attn_lists.size();
+    for (int k = 1; k < p.Kmax; ++k)
+      if (ln.list_at[0][k] > (int)lo) { hi = (size_t)ln.list_at[0][k]; break; }
+    if (p.n_sets > 1 && !ln.list_at[1].empty() && ln.list_at[1][0] > (int)lo) hi = std::min(hi, (size_t)ln.list_at[1][0]);
+    *n_blocks = ln.list_blocks[0][0];
+    *n_entries = (int32_t)(hi - lo);
+    if ((int64_t)(hi - lo) > max_entries) return ROSA_E_CAPACITY;
+    for (size_t e = lo; e < hi; ++e) {
+      if (item_of) item_of[e - lo] = p.attn_lists[e];
+      if (next) next[e - lo] = p.attn_next[e];
+    }
+    if (item_cost)
+      for (size_t i = 0; i < p.sets[0].items.size(); ++i) {
+        const AttnItem &it = p.sets[0].items[i];
+        item_cost[i] = (it.kend - it.kbeg + 31) / 32;
+      }
+    return ROSA_OK;
+  } catch (...) {
+    return ROSA_E_NOMEM;
+  }
+}
+
 rosa_status rosa_debug_plan_lanes(const rosa_model_config *cfg, const rosa_capacity *cap, const rosa_request *reqs,
                                   int32_t n, int32_t lanes, int32_t *lane_of) {
   try {
@@ -1176,7 +1259,8 @@ rosa_status rosa_attention_noalloc(const rosa_model_config *cfg, const rosa_requ
     std::memcpy(img.data() + kNaOffGroups, S0.groups.data(), S0.groups.size() * sizeof(AttnGroup));
     std::memcpy(img.data() + kNaOffGroups + S0.groups.size() * sizeof(AttnGroup), S1.groups.data(),
                 S1.groups.size() * sizeof(AttnGroup));
-    attn_order_items(all, p.attn_lists.data(), p.attn_lists.size(), reinterpret_cast<AttnItem *>(img.data() + kNaOffLists));
+    attn_order_items(all, p.attn_lists.data(), p.attn_next.data(), p.attn_lists.size(),
+                     reinterpret_cast<AttnItem *>(img.data() + kNaOffLists));
 
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);

@@ -34,7 +34,9 @@ static_assert(sizeof(ReqDesc) == 64, "ReqDesc is 64 bytes");
 struct AttnItem {
   const void *pk, *pv;   // the request's prefix K and V, [L][P][n_kv][hd]
   int32_t req, kvh, q0, nq, kbeg, kend, slot;
-  int32_t P, tok_off, pad0, pad1, pad2;
+  int32_t P, tok_off;
+  int32_t next;          // launch lists: the block's next entry, -1 after its last
+  int32_t pad1, pad2;
 };
 static_assert(sizeof(AttnItem) == 64, "AttnItem is 64 bytes");
 
@@ -54,6 +56,9 @@ constexpr int attn_groups_per_wave(int hd) { return hd <= 64 ? 2 : 1; }
 // launch has fewer than kAttnSplitTarget items; a split item holds at least
 // kAttnMinSplitKeys keys; at most kAttnMaxSlots partial-result slots per launch.
 constexpr int kAttnSplitTarget = 256;
+// Persistent blocks of the bf16 attention kernel per launch: two per compute
+// unit of a 256-CU MI355X.
+constexpr int kAttnBlocks = 512;
 constexpr int kAttnMinSplitKeys = 256;
 constexpr int kAttnMaxSlots = 2 * kAttnSplitTarget;
 constexpr int kMaxTau = 128;       // distinct flow times per call
@@ -151,8 +156,9 @@ hipError_t launch_prefill_kv_scatter(const PrefillJob *jobs, const int32_t *row_
 // Attention of one layer.
 struct AttnArgs {
   const AttnItem *items; int n_items;
-  // bf16: the items in launch order.  Block b runs ordered[b], or exits if
-  // its nq is 0; n_blocks blocks.  items and n_items are then unused.
+  // bf16: the persistent blocks' item lists.  Block b runs ordered[b], then
+  // the entry its `next` names, and so on until next is -1 (an idle block's
+  // entry has nq 0); n_blocks blocks.  items and n_items are then unused.
   const AttnItem *ordered; int n_blocks;
   const ReqDesc *reqs;
   int layer;
@@ -163,19 +169,22 @@ struct AttnArgs {
   float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
 };
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
-// Host: XCD-balanced, longest-first block -> item table for the items of the
-// given requests (contiguous item ranges); appended to out (-1: an idle
-// block); returns the block count.
+// Host: XCD-balanced item lists of persistent blocks for the items of the
+// given requests (contiguous item ranges): appends entries to out (item
+// index; entries 0 .. n_blocks-1 are the blocks' first items, -1: idle) and
+// next (the index within this table of the block's next entry, -1 after its
+// last); returns n_blocks.
 int attn_launch_order(const std::vector<AttnItem> &items, const std::vector<std::pair<int, int>> &ranges,
-                      std::vector<int32_t> &out);
+                      std::vector<int32_t> &out, std::vector<int32_t> &next);
 // Host: round-to-nearest-even fp32 -> bf16 bits (NaN stays a quiet NaN).
 uint16_t f32_to_bf16_rne(float f);
 // Host: upload L stacked [K][N] fp32 matrices as [L][N][K] (K contiguous), in
 // bf16 or fp32; synchronous.
 hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16);
-// Host: the items of a block -> item table in block order (an idle block
-// gets an item with nq = 0), written to dst.
-void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, size_t n, AttnItem *dst);
+// Host: the block lists as item records (an idle block gets an item with
+// nq = 0), each with its `next` link, written to dst.
+void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, const int32_t *next, size_t n,
+                      AttnItem *dst);
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16, hipStream_t s);

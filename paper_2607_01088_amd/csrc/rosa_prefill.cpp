@@ -38,7 +38,7 @@ struct PrefillPlan {
   std::vector<int32_t> row_job;
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
-  std::vector<int32_t> list;      // bf16 launch order
+  std::vector<int32_t> list, list_next;   // bf16 launch order (block item lists)
   int n_blocks = 0;
   int64_t M = 0;
 };
@@ -268,7 +268,7 @@ rosa_status build_prefill_plan(const rosa_prefill *h, const rosa_prefix_job *job
     err = "internal: attention work items exceeded";
     return ROSA_E_CAPACITY;
   }
-  if (h->bf16 && !p.items.empty()) p.n_blocks = attn_launch_order(p.items, ranges, p.list);
+  if (h->bf16 && !p.items.empty()) p.n_blocks = attn_launch_order(p.items, ranges, p.list, p.list_next);
   if (p.list.size() > h->max_list) { err = "internal: attention launch order exceeded"; return ROSA_E_CAPACITY; }
   return ROSA_OK;
 }
@@ -286,7 +286,7 @@ hipError_t upload_prefill_plan(rosa_prefill *h, const PrefillPlan &p) {
   std::memcpy(hp + h->off_rows, p.row_job.data(), p.row_job.size() * 4);
   std::memcpy(hp + h->off_items, p.items.data(), p.items.size() * sizeof(AttnItem));
   std::memcpy(hp + h->off_groups, p.groups.data(), p.groups.size() * sizeof(AttnGroup));
-  attn_order_items(p.items, p.list.data(), p.list.size(), (AttnItem *)(hp + h->off_list));
+  attn_order_items(p.items, p.list.data(), p.list_next.data(), p.list.size(), (AttnItem *)(hp + h->off_list));
   const size_t used = h->off_list + p.list.size() * sizeof(AttnItem);
   hipError_t e = hipMemcpyAsync(h->d_plan, hp, used, hipMemcpyHostToDevice, h->stream);
   if (e != hipSuccess) return e;
@@ -361,7 +361,7 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     const int G = h->nq / h->nkv;
     const int64_t qb_bound = (int64_t)h->nkv * (((int64_t)T * G + 127) / 128 + 2 * (int64_t)max_jobs);
     h->max_items = (int)(qb_bound + kAttnMaxSlots);
-    h->max_list = 8 * (size_t)h->max_items + 8;
+    h->max_list = 2 * (size_t)h->max_items + 8;
     auto align = [](size_t v) { return (v + 255) / 256 * 256; };
     h->off_jobs = 0;
     h->off_reqs = align(h->off_jobs + (size_t)max_jobs * sizeof(PrefillJob));

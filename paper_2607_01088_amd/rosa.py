@@ -150,6 +150,10 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.rosa_debug_plan_lanes.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32, i32,
                                           C.POINTER(i32)]
     lib.rosa_debug_plan_lanes.restype = C.c_int
+    lib.rosa_debug_attn_lists.argtypes = [C.POINTER(ModelConfig), C.POINTER(Capacity), C.POINTER(Request), i32, i32,
+                                          C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32),
+                                          C.POINTER(i32)]
+    lib.rosa_debug_attn_lists.restype = C.c_int
     lib.rosa_debug_time_conditioning.argtypes = [vp, C.POINTER(C.c_float), i32, vp]
     lib.rosa_debug_time_conditioning.restype = C.c_int
     lib.rosa_debug_attention.argtypes = [vp, C.POINTER(Request), i32, i32, vp, vp]
@@ -265,6 +269,24 @@ def plan_lanes(shape, dtype: str, cap: Capacity, reqs: Sequence[Request], lanes:
     out = (C.c_int32 * max(1, n))()
     st = lib.rosa_debug_plan_lanes(C.byref(cfg), C.byref(cap), request_array(reqs), n, lanes, out)
     return st, list(out)[:n]
+
+
+def attn_lists(shape, cap: Capacity, reqs: Sequence[Request], n_items: int):
+    """Host-only attention launch lists of a bf16 call (rosa_debug_attn_lists):
+    (status, n_blocks, item of each entry, next of each entry, cost of each item)."""
+    lib = load()
+    cfg = model_config(shape, "bf16")
+    n = len(reqs)
+    arr = request_array(reqs)
+    nb, ne = C.c_int32(0), C.c_int32(0)
+    st = lib.rosa_debug_attn_lists(C.byref(cfg), C.byref(cap), arr, n, 0, C.byref(nb), C.byref(ne), None, None, None)
+    if st not in (ROSA_OK, ROSA_E_CAPACITY):
+        return st, 0, [], [], []
+    m = max(1, ne.value)
+    item_of, nxt = (C.c_int32 * m)(), (C.c_int32 * m)()
+    cost = (C.c_int32 * max(1, n_items))()
+    st = lib.rosa_debug_attn_lists(C.byref(cfg), C.byref(cap), arr, n, m, C.byref(nb), C.byref(ne), item_of, nxt, cost)
+    return st, nb.value, list(item_of)[:ne.value], list(nxt)[:ne.value], list(cost)[:n_items]
 
 
 def s1_simulate(robots: int, batch: int, batch_ms: float, t_act_ms: float, n_batches: int = 256) -> Dict[str, float]:

@@ -106,6 +106,61 @@ def test_plan_lanes_balance_and_cover_every_request():
     assert st == rosa.ROSA_OK and set(lanes) == {0}
 
 
+def _walk_lists(nb, item_of, nxt):
+    """Follow each block's chain; returns the item lists per block."""
+    seen = [False] * len(item_of)
+    blocks = []
+    for b in range(nb):
+        lst, e = [], b
+        while e >= 0:
+            assert 0 <= e < len(item_of) and not seen[e], (b, e)
+            seen[e] = True
+            if item_of[e] < 0:
+                assert e == b and nxt[e] == -1      # idle: a first entry with no successor
+                break
+            lst.append(item_of[e])
+            e = nxt[e]
+        blocks.append(lst)
+    assert all(seen), "every table entry belongs to one block's chain"
+    return blocks
+
+
+@pytest.mark.parametrize("case", ["factory", "one_request", "few_requests"])
+def test_attention_launch_lists_cover_every_item_once_and_balance(case):
+    """Persistent attention launch lists (rosa_debug_attn_lists): every work
+    item of the launch is on exactly one block's chain, the grid is a multiple
+    of the 8 XCDs and at most 512 blocks, block loads are within one item of
+    the mean (longest-processing-time bound), and while there are no more
+    items than blocks no block runs two."""
+    import numpy as np
+    rng = np.random.default_rng(5)
+    if case == "factory":
+        reqs = [req(int(rng.integers(512, 1281)), int(rng.choice([16, 50])), int(rng.choice([5, 10])))
+                for _ in range(256)]
+    elif case == "one_request":
+        reqs = [req(1024, 50, 10)]
+    else:
+        reqs = [req(int(rng.integers(600, 1025)), 50, 10) for _ in range(5)]
+    cap = rosa.capacity(len(reqs), 50, len(reqs) * 50, 10, len(reqs) * 1280)
+    st, _, _, _, counts = rosa.plan(PI0_SHAPE, "bf16", cap, reqs)
+    assert st == rosa.ROSA_OK
+    n_items = counts[1]
+    st, nb, item_of, nxt, cost = rosa.attn_lists(PI0_SHAPE, cap, reqs, n_items)
+    assert st == rosa.ROSA_OK
+    assert nb % 8 == 0 and 8 <= nb <= 512
+    blocks = _walk_lists(nb, item_of, nxt)
+    flat = sorted(i for lst in blocks for i in lst)
+    assert flat == list(range(n_items))
+    over = 6                                  # fixed per-item overhead the packing charges, in steps
+    loads = [sum(cost[i] + over for i in lst) for lst in blocks]
+    biggest = max(cost) + over
+    assert max(loads) <= sum(loads) / nb + biggest
+    if n_items <= nb:
+        assert max(len(lst) for lst in blocks) == 1
+    st, *_ = rosa.attn_lists(PI0_SHAPE, cap, reqs[:0], 0)
+    assert st == rosa.ROSA_OK
+
+
 @pytest.mark.parametrize("bad,status", [
     (dict(P=-1), rosa.ROSA_E_INVALID),
     (dict(H=0), rosa.ROSA_E_INVALID),
