@@ -172,6 +172,157 @@ def _summarize_prefill(out):
     open(os.path.join(PROFILES, "kernel_stats_vlm_prefill_b32.md"), "w").write("\n".join(lines) + "\n")
 
 
+PMC_UTIL = ("MfmaUtil VALUBusy LdsUtil LDSBankConflict SQ_WAIT_INST_LDS SQ_WAVE_CYCLES SQ_BUSY_CYCLES "
+            "SQ_LDS_DATA_FIFO_FULL GRBM_GUI_ACTIVE")
+PMC_INST = ("SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_INSTS_SALU SQ_WAIT_ANY SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+            "SQ_LDS_CMD_FIFO_FULL SQ_ACTIVE_INST_LDS GRBM_GUI_ACTIVE")
+PROJ_ORDER = ("gemm_qkv", "attention", "gemm_o", "gemm_up", "gemm_down")
+
+
+def _classify_dispatches(rows):
+    """Dispatch id -> kernel role for a one-lane bf16 generate run.  Per layer
+    the expert launches modnorm, the QKV projection, attention (and, for split
+    keys, the merge), the output projection, modnorm, MLP up, MLP down; a split
+    product's reduce kernel belongs to the projection before it."""
+    names = {}
+    for r in rows:
+        names[int(r["Dispatch_Id"])] = r["Kernel_Name"]
+    role, prev, last_gemm = {}, "", ""
+    for d in sorted(names):
+        n = names[d]
+        if "attention_bf16" in n:
+            cur = "attention"
+        elif "gemm_split_reduce" in n:
+            cur = prev if prev.startswith("gemm_") else "other"
+        elif "gemm_bf16_kernel" in n:
+            if prev in ("attention", "attn_merge"):
+                cur = "gemm_o"
+            elif prev == "gemm_up":
+                cur = "gemm_down"
+            elif prev == "modnorm":
+                cur = "gemm_up" if last_gemm == "gemm_o" else "gemm_qkv"
+            else:
+                cur = "other"
+            last_gemm = cur
+        elif "attn_merge" in n:
+            cur = "attn_merge"
+        elif "modnorm" in n:
+            cur = "modnorm"
+        else:
+            cur = "other"
+        role[d] = cur
+        prev = cur
+    return role
+
+
+def _pmc_by_role(rows, role):
+    """{role: {counter: [values per dispatch]}} and {role: {dispatch: GRBM_GUI_ACTIVE}}."""
+    agg, grbm = {}, {}
+    for r in rows:
+        k = role.get(int(r["Dispatch_Id"]), "other")
+        v = float(r["Counter_Value"])
+        agg.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(v)
+        if r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+            grbm.setdefault(k, {})[int(r["Dispatch_Id"])] = v
+    return agg, grbm
+
+
+def _summarize_pmc(out):
+    """Utilisation counters per kernel role (pmc_util/, pmc_inst/ runs)."""
+    util = _csv_rows(f"{out}/pmc_util/**/*counter_collection.csv")
+    inst = _csv_rows(f"{out}/pmc_inst/**/*counter_collection.csv")
+    ua, ug = _pmc_by_role(util, _classify_dispatches(util))
+    ia, _ = _pmc_by_role(inst, _classify_dispatches(inst))
+
+    def wavg(agg, grbm, role, name):
+        # time-weighted over dispatches (weights: GRBM_GUI_ACTIVE of the dispatch)
+        rows = [r for r in util if r["Counter_Name"] == name]
+        role_of = _classify_dispatches(util)
+        num = den = 0.0
+        for r in rows:
+            d = int(r["Dispatch_Id"])
+            if role_of.get(d) != role:
+                continue
+            w = grbm.get(role, {}).get(d, 0.0)
+            num += w * float(r["Counter_Value"])
+            den += w
+        return num / den if den else float("nan")
+
+    def tot(agg, role, name):
+        return sum(agg.get(role, {}).get(name, [0.0]))
+
+    lines = ["# Utilisation counters per kernel, factory_b256 workload", "",
+             "Commands (one MI355X, repository root, library built in-tree; one lane, so every dispatch runs "
+             "alone; two counter sets, each in its own run):", "", "```", "export TMPDIR=/tmp",
+             f"timeout -s KILL 300 rocprofv3 --pmc {PMC_UTIL} --output-format csv -d {out}/pmc_util -o u -- "
+             "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
+             f"timeout -s KILL 300 rocprofv3 --pmc {PMC_INST} --output-format csv -d {out}/pmc_inst -o i -- "
+             "python -u bench.py --steps 1 --warmup 0 --no-cpu-baseline --lanes 1",
+             f"python bench.py --summarize-profiles {out}", "```", "",
+             "Dispatches are assigned to projections by their place in the per-layer launch sequence "
+             "(modnorm, QKV, attention, output projection, modnorm, MLP up, MLP down).  MfmaUtil, VALUBusy, "
+             "LdsUtil and LDSBankConflict are rocprofv3's derived metrics (percent of the kernel's active GPU "
+             "cycles: MFMA busy cycles per SIMD, VALU issue per CU, LDS indexed-access cycles per CU, LDS "
+             "bank-conflict stall cycles per CU), averaged over dispatches weighted by GRBM_GUI_ACTIVE.  "
+             "LDS wait = SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES (share of resident-wave time spent waiting to issue "
+             "an LDS instruction); any wait = SQ_WAIT_ANY / SQ_WAVE_CYCLES.  Instruction counts are per MFMA "
+             "instruction (every MFMA here is a 32x32x16 bf16 one, 32 busy cycles).", "",
+             "| Kernel | Dispatches | MfmaUtil % | VALUBusy % | LdsUtil % | LDS bank conflict % | LDS wait | "
+             "any wait | VALU / MFMA | LDS / MFMA | SALU / MFMA | LDS data FIFO full / active cycle | "
+             "GFLOP / dispatch |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    res = {}
+    for role in PROJ_ORDER:
+        if role not in ua:
+            continue
+        n = len(ug.get(role, {}))
+        mf = wavg(ua, ug, role, "MfmaUtil")
+        vb = wavg(ua, ug, role, "VALUBusy")
+        lu = wavg(ua, ug, role, "LdsUtil")
+        bc = wavg(ua, ug, role, "LDSBankConflict")
+        wc = tot(ua, role, "SQ_WAVE_CYCLES")
+        lw = tot(ua, role, "SQ_WAIT_INST_LDS") / wc if wc else float("nan")
+        mfma = tot(ia, role, "SQ_INSTS_MFMA")
+        aw_wc = tot(ia, role, "SQ_WAIT_ANY")
+        # SQ_WAIT_ANY comes from the second run; its wave cycles are taken as the first run's
+        any_w = aw_wc / wc if wc else float("nan")
+        per = lambda c: tot(ia, role, c) / mfma if mfma else float("nan")
+        fifo = tot(ua, role, "SQ_LDS_DATA_FIFO_FULL") / max(tot(ua, role, "SQ_BUSY_CYCLES"), 1.0)
+        gfl = tot(ia, role, "SQ_INSTS_VALU_MFMA_MOPS_BF16") * 512 / max(len(ia.get(role, {}).get("SQ_INSTS_MFMA", [1])), 1) / 1e9
+        res[role] = dict(dispatches=n, mfma_util=round(mf, 1), valu_busy=round(vb, 1), lds_util=round(lu, 1),
+                         lds_bank_conflict=round(bc, 2), lds_wait=round(lw, 3), any_wait=round(any_w, 3),
+                         valu_per_mfma=round(per("SQ_INSTS_VALU"), 2), lds_per_mfma=round(per("SQ_INSTS_LDS"), 3),
+                         salu_per_mfma=round(per("SQ_INSTS_SALU"), 3), gflop_per_dispatch=round(gfl, 2))
+        lines.append(f"| {role} | {n} | {mf:.1f} | {vb:.1f} | {lu:.1f} | {bc:.2f} | {lw:.3f} | {any_w:.3f} | "
+                     f"{per('SQ_INSTS_VALU'):.2f} | {per('SQ_INSTS_LDS'):.3f} | {per('SQ_INSTS_SALU'):.3f} | "
+                     f"{fifo:.3f} | {gfl:.2f} |")
+    srcs = {f: hashlib.sha256(open(os.path.join(ROOT, "paper_2607_01088_amd", "csrc", f), "rb").read()).hexdigest()[:16]
+            for f in ("k_attn.hip", "k_gemm.hip")}
+    lines += ["", "Kernel source sha256 (first 16 hex digits) when measured: " +
+              ", ".join(f"`{f}` `{h}`" for f, h in srcs.items()) + "."]
+    open(os.path.join(PROFILES, "pmc_factory_b256.md"), "w").write("\n".join(lines) + "\n")
+    json.dump({"workload": "factory_b256", "sources": srcs, "kernels": res},
+              open(os.path.join(PROFILES, "pmc_factory_b256.json"), "w"), indent=1)
+
+
+def _traffic_rows(out, ff, wf):
+    """Per-projection rows of the traffic table (dispatches assigned by launch order)."""
+    fr = _csv_rows(f"{out}/pmc_fetch/**/*counter_collection.csv")
+    wr_ = _csv_rows(f"{out}/pmc_write/**/*counter_collection.csv")
+    fa, _ = _pmc_by_role(fr, _classify_dispatches(fr))
+    wa, _ = _pmc_by_role(wr_, _classify_dispatches(wr_))
+    rows = []
+    for role in ("gemm_qkv", "gemm_o", "gemm_up", "gemm_down"):
+        f = fa.get(role, {}).get("FETCH_SIZE", [])
+        w = wa.get(role, {}).get("WRITE_SIZE", [])
+        if not f or not w:
+            continue
+        fk, wk = sum(f) / len(f), sum(w) / len(w)
+        rows.append(f"| {role} (all tile configurations) | {len(f)} | {fk:.1f} | {wk:.1f} | "
+                    f"{fk * ff * 1024 / 1e6:.1f} | {wk * wf * 1024 / 1e6:.1f} |")
+    return rows
+
+
 def summarize_profiles(out):
     """Turn rocprofv3 outputs of this script into the summaries under
     profiles/ (kernel-time table, calibrated HBM traffic of the attention
@@ -182,6 +333,8 @@ def summarize_profiles(out):
     import glob
     if glob.glob(f"{out}/prof_prefill/**/*kernel_stats.csv", recursive=True):
         _summarize_prefill(out)
+    if glob.glob(f"{out}/pmc_util/**/*counter_collection.csv", recursive=True):
+        _summarize_pmc(out)
     if not glob.glob(f"{out}/prof_factory/**/*kernel_stats.csv", recursive=True):
         return
     stats = _csv_rows(f"{out}/prof_factory/**/*kernel_stats.csv")
@@ -231,6 +384,7 @@ def summarize_profiles(out):
           "| Kernel | Dispatches | FETCH_SIZE (KiB, avg) | WRITE_SIZE (KiB, avg) | HBM read (MB) | HBM write (MB) |",
           "|---|---:|---:|---:|---:|---:|",
           f"| `rosa::attention_bf16_kernel<256, 1>` | {nf} | {fetch:.1f} | {write:.1f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} |",
+          *_traffic_rows(out, ff, wf),
           "", f"Per launch: {(rd + wr) / 1e6:.1f} MB of HBM traffic.  Algorithmic bytes per launch (each active "
           "request's prefix K and V of the layer read once) are 174 MB averaged over the 180 launches of one call; "
           "queries, action keys and the output add about 26 MB written and 30 MB read.", "",

@@ -44,39 +44,8 @@ constexpr int waitcnt_lgkm0 = 15 | (3 << 14) | (7 << 4);   // lgkmcnt(0), others
 __device__ __forceinline__ int swz(int r, int cpr) { return (((r & 3) << 2) | ((r >> 2) & 3)) & (cpr - 1); }
 }  // namespace at
 
-#define ROSA_LDS_A(p) ((__attribute__((address_space(3))) void *)(p))
 
 
-// One 1 KB global -> LDS copy (lane i: 16 bytes from its own source to
-// lds + 16 i), written as inline assembly so the compiler does not track it:
-// its model of this copy makes it wait for every outstanding LDS read before
-// the next MFMA, which would cap the LDS reads in flight at one.  The kernel
-// waits for the copies itself (vmcnt) and sets M0, which nothing else in these
-// kernels uses; the s_nop is the wait state the M0 write needs before the copy.
-// dma_1k_s takes a wave-uniform 64-bit base (SGPRs) plus a 32-bit per-lane
-// byte offset; dma_1k a full per-lane address.
-__device__ __forceinline__ void dma_1k(const void *src, uint32_t lds) {
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
-#pragma clang diagnostic pop
-}
-__device__ __forceinline__ void dma_1k_s(const void *base, uint32_t off, uint32_t lds) {
-  // The base is wave-uniform by construction; reading it through readfirstlane
-  // keeps it in SGPRs even where the compiler cannot prove that.
-  const uint64_t b64 = (uint64_t)(size_t)base;
-  const uint64_t ub = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b64 >> 32)) << 32) |
-                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b64);
-  const void *bs = (const void *)(size_t)ub;
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(bs), "s"(lds)
-               : "memory", "m0");
-#pragma clang diagnostic pop
-}
-__device__ __forceinline__ uint32_t lds_u32(const uint8_t *p) {
-  return (uint32_t)(size_t)ROSA_LDS_A(p);
-}
 typedef __attribute__((address_space(3))) const uint8_t lds_u8;
 __device__ __forceinline__ const lds_u8 *lds_ptr(uint32_t a) { return (const lds_u8 *)(size_t)a; }
 __device__ __forceinline__ bf16x8 lds_tr_pair(const lds_u8 *p0, const lds_u8 *p1) {

@@ -10,6 +10,7 @@
 // slices in order and applies the epilogue.
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 
 #include "rosa_device.h"
 #include "rosa_internal.h"
@@ -20,12 +21,16 @@ namespace rosa {
 // Block tile BM x BN = (32 MB) x (32 TN WN), WM x WN waves, each wave
 // (32 MB / WM) x (32 TN) made of 32 x 32 v_mfma_f32_32x32x16_bf16 tiles.
 //
-// Main loop: K is consumed 32 at a time through a ring of four LDS stages
-// filled by global_load_lds_dwordx4 (global -> LDS without staging
-// registers): while the waves multiply stage s, stages s+1 and s+2 are landing
-// and stage s+3 is being requested.  One barrier per stage.  Each stage buffer
-// is its own LDS object and the barrier is a bare s_barrier, so the only wait
-// on the asynchronous copies is the explicit vmcnt before it.
+// Main loop: K is consumed BK (32 or 64) at a time through a ring of NST = 4
+// LDS stages filled by global_load_lds_dwordx4 (global -> LDS without
+// staging registers): while the waves multiply stage s, stage s+1 has landed
+// and stages s+2 .. s+NST-1 are landing or being requested, so NST - 2 stages
+// of copies cover the memory latency.  One barrier per stage, crossed before the stage's last
+// k-step of MFMAs so that the next stage's first operand reads overlap them;
+// within a stage each k-step's operands are read while the previous k-step's
+// MFMAs run.  The copies are issued as
+// inline assembly the compiler does not track and the barrier is a bare
+// s_barrier, so the only wait on them is the explicit vmcnt before it.
 //
 // LDS rows are 64 bytes (32 bf16 of K); the four 16-byte chunks of row r are
 // stored XOR-swizzled by (r / 4) % 4, so the 16 rows a 16-lane group reads at
@@ -43,9 +48,16 @@ namespace rosa {
 // column tiles of one row panel share an XCD's L2.
 namespace gb {
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// f(integral_constant<int, i>) for i = 0 .. N - 1, in order.
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
 }  // namespace gb
 
-#define ROSA_LDS(p) ((__attribute__((address_space(3))) void *)(p))
 
 // Chunk swizzle of an LDS row of CPR 16-byte chunks: chunk c of row r is
 // stored at c ^ gswz(r).  64-byte rows (CPR 4): (r / 4) % 4; 128-byte rows
@@ -57,30 +69,30 @@ __device__ __forceinline__ int gswz(int r) { return CPR == 4 ? (r >> 2) & 3 : (r
 template <int MB_, int TN_, int WM_, int WN_, int BK_ = 32>
 struct GemmTile {
   static constexpr int MB = MB_, TN = TN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
-  static constexpr int NST = 4;                                         // LDS ring depth
   static constexpr int MBW = MB / WM;                                   // 32-row blocks per wave
   static constexpr int BM = 32 * MB, BN = 32 * TN * WN;
   static constexpr int BK = BK_;                                        // K per stage
   static constexpr int ROWB = BK * 2, CPR = ROWB / 16, RPU = 1024 / ROWB;   // row bytes, chunks per row, rows per 1 KB
   static constexpr int ABYTES = BM * BK * 2, SBYTES = ABYTES + BN * BK * 2;
+  // LDS ring depth (deeper rings measured no faster on these shapes).
+  static constexpr int NST = 4;
+  static_assert(NST * SBYTES <= 160 * 1024, "LDS");
   static constexpr int U = (BM + BN) / RPU;                             // 1 KB copies per stage
   static_assert(BK == 32 || BK == 64, "stage K");
   static constexpr int CHI = (U + NW - 1) / NW, CLO = U / NW;           // copies per wave
   static constexpr int NHI = U % NW == 0 ? NW : U % NW;                 // waves with CHI copies
-  static constexpr int PERB = SBYTES / 4096;                            // 4 KB epilogue slots per stage
   static_assert(MBW * WM == MB, "row split");
-  static_assert(NST * PERB >= NW, "epilogue staging space");
+  static_assert(NW * 4096 <= NST * SBYTES, "epilogue staging space (4 KB per wave)");
 };
 
 // K stages [kt0, kt0 + nk) of the tile at (m0, n0) into acc (zeroed first).
 // Ends with every copy landed and every wave past its last LDS read.
 template <typename T>
-__device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0, int kt0, int nk, uint8_t *L0,
-                                              uint8_t *L1, uint8_t *L2, uint8_t *L3,
+__device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0, int kt0, int nk, uint8_t *L,
                                               f32x16 (&acc)[T::MBW][T::TN]) {
   using namespace gb;
   constexpr int NW = T::NW, MBW = T::MBW, TN = T::TN, CHI = T::CHI, CLO = T::CLO, NST = T::NST;
-  constexpr int ABYTES = T::ABYTES;
+  constexpr int ABYTES = T::ABYTES, SBYTES = T::SBYTES;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % NW;   // wave-uniform, in an SGPR
   const int wm = wave / T::WN, wn = wave % T::WN;
@@ -108,12 +120,14 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
   }
   const bool hi = wave < T::NHI;
   constexpr int BK = T::BK, ROWB = T::ROWB;
-  auto issue = [&](uint8_t *st, int kt) {
+  // Copy j (of CHI) of this wave for stage kt into buffer st.
+  auto issue_one = [&](uint8_t *st, int kt, int j) __attribute__((always_inline)) {
     const int k0 = (kt0 + min(kt, nk - 1)) * BK;   // past the end: repeat the last stage (never read)
+    if (j < CLO || hi) dma_1k(src[j] + k0, lds_u32(st) + (uint32_t)((j * NW + wave) * 1024));
+  };
+  auto issue = [&](uint8_t *st, int kt) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < CHI; ++j)
-      if (j < CLO || hi)
-        __builtin_amdgcn_global_load_lds((const void *)(src[j] + k0), ROSA_LDS(st + (j * NW + wave) * 1024), 16, 0, 0);
+    for (int j = 0; j < CHI; ++j) issue_one(st, kt, j);
   };
 
 #pragma unroll
@@ -133,50 +147,84 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
   for (int ks = 0; ks < NKS; ++ks) ph[ks] = ((2 * ks + (lane >> 5)) ^ swz) * 16;
   const int arow = (wm * MBW * 32 + (lane & 31)) * ROWB;
   const int brow = ABYTES + (wn * TN * 32 + (lane & 31)) * ROWB;
-  auto compute = [&](const uint8_t *st) {
+  // Fragments of one k-step (MBW A tiles, TN W tiles), double-buffered.
+  bf16x8 fa[2][MBW], fb[2][TN];
+  auto read_frags = [&](const uint8_t *st, int ks, int f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[f][j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * ROWB + ph[ks]);
+#pragma unroll
+    for (int i = 0; i < MBW; ++i) fa[f][i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * ROWB + ph[ks]);
+  };
+  // The k-step's MFMAs; after MFMA number q, between(q) (the refill copies,
+  // spread over the k-step so that no wave stalls on a burst of copies while
+  // its MFMAs wait to issue).
+  auto mfmas = [&](int f, auto &&between) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < MBW; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[f][j], fa[f][i], acc[i][j], 0, 0, 0);
+        between(i * TN + j);
+      }
+  };
+  constexpr int NMF = MBW * TN;            // MFMAs per k-step
+  // Stage kt in buffer kt % NST (`cur`), whose k-step 0 fragments are
+  // already in registers.  Each k-step first reads the next k-step's
+  // fragments, then issues its own MFMAs, so LDS latency hides behind a
+  // k-step of MFMAs.  Before the last k-step's MFMAs the block crosses the
+  // stage boundary: wait until this wave's copies of stage kt + 1 have landed
+  // (stages kt + 2 .. kt + NST - 2 may still be in flight), barrier (every
+  // wave's copies have landed, and every wave has finished reading stage
+  // kt - 1), refill stage kt - 1's buffer with stage kt + NST - 1, and read
+  // stage kt + 1's first fragments.
+  auto stage = [&](auto cur_t, int kt) __attribute__((always_inline)) {
+    constexpr int cur = decltype(cur_t)::value;
+    constexpr int nxt = cur + 1 == NST ? 0 : cur + 1, old = cur == 0 ? NST - 1 : cur - 1;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) {
-      bf16x8 af[MBW], bfr[TN];
+      if (ks + 1 < NKS) {
+        read_frags(L + cur * SBYTES, ks + 1, (ks + 1) & 1);
+      } else {
+        if (hi) __builtin_amdgcn_s_waitcnt(waitcnt_vm((NST - 3) * CHI));
+        else __builtin_amdgcn_s_waitcnt(waitcnt_vm((NST - 3) * CLO));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(L + nxt * SBYTES, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (ks + 1 < NKS) {
+        mfmas(ks & 1, [](int) {});
+      } else {
+        // copy j after MFMA (j * NMF) / CHI: spread evenly over the k-step
+        mfmas(ks & 1, [&](int q) __attribute__((always_inline)) {
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[j] = *reinterpret_cast<const bf16x8 *>(st + brow + j * 32 * ROWB + ph[ks]);
-#pragma unroll
-      for (int i = 0; i < MBW; ++i) af[i] = *reinterpret_cast<const bf16x8 *>(st + arow + i * 32 * ROWB + ph[ks]);
-#pragma unroll
-      for (int i = 0; i < MBW; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < CHI; ++j)
+            if ((j * NMF) / CHI == q) issue_one(L + old * SBYTES, kt + NST - 1, j);
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // A wave copies CHI or CLO units per stage, so waiting until at most two
-  // stages of its copies are outstanding means stage kt has landed.
-  auto step = [&](uint8_t *cur, uint8_t *refill, int kt) {
-    if (hi) __builtin_amdgcn_s_waitcnt(waitcnt_vm(CHI * (NST - 2)));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(CLO * (NST - 2)));
-    __builtin_amdgcn_s_barrier();           // ... every wave's too; stage kt-1 is no longer read
-    __builtin_amdgcn_sched_barrier(0);
-    issue(refill, kt + NST - 1);
-    compute(cur);
-  };
+  static_assert(NKS % 2 == 0, "the next stage's first fragments go to buffer 0");
 
-  // Stage s (relative to kt0) lives in L(s % 4).
-  issue(L0, 0);
-  issue(L1, 1);
-  issue(L2, 2);
+  // Prologue: stages 0 .. NST - 2 requested, stage 0 landed.
+#pragma unroll
+  for (int st = 0; st < NST - 1; ++st) issue(L + st * SBYTES, st);
+  if (hi) __builtin_amdgcn_s_waitcnt(waitcnt_vm((NST - 2) * CHI));
+  else __builtin_amdgcn_s_waitcnt(waitcnt_vm((NST - 2) * CLO));
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  read_frags(L, 0, 0);
+  // Groups of NST stages, unrolled so that every buffer offset is an
+  // immediate, then the remaining stages.
   int kt = 0;
-  for (; kt + 4 <= nk; kt += 4) {
-    step(L0, L3, kt);
-    step(L1, L0, kt + 1);
-    step(L2, L1, kt + 2);
-    step(L3, L2, kt + 3);
-  }
-  if (kt < nk) {
-    step(L0, L3, kt);
-    if (kt + 1 < nk) {
-      step(L1, L0, kt + 1);
-      if (kt + 2 < nk) step(L2, L1, kt + 2);
-    }
-  }
+  for (; kt + NST <= nk; kt += NST)
+    static_for<NST>([&](auto r) { stage(r, kt + decltype(r)::value); });
+  static_for<NST - 1>([&](auto r) {
+    if (kt + decltype(r)::value < nk) stage(r, kt + decltype(r)::value);
+  });
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();                          // every wave is past its last stage read: LDS is free
 }
@@ -184,8 +232,8 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
 // Epilogue of the tile at (m0, n0) from acc; stages through the ring's LDS,
 // which must be free (gemm_mainloop ends that way).
 template <typename T, int EPI>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0, uint8_t *L0, uint8_t *L1,
-                                              uint8_t *L2, uint8_t *L3, f32x16 (&acc)[T::MBW][T::TN]) {
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0, uint8_t *L,
+                                              f32x16 (&acc)[T::MBW][T::TN]) {
   constexpr int MBW = T::MBW, TN = T::TN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) % T::NW;
@@ -199,8 +247,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
     // Each wave stages one 32 x 32 tile at a
     // time in its own 4 KB slot (fp32: 32 rows x 8 chunks of 16 B, chunk c of
     // row r at c ^ ((r / 2) % 8)), then reads it back row-contiguous.
-    const int sb = wave / T::PERB;
-    uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+    uint8_t *stg = L + wave * 4096;
     float *H = reinterpret_cast<float *>(g.out);
     // Gate rows of every row this lane touches, loaded once up front so that
     // no gate load waits for its row's modulation index (32-bit offsets: the
@@ -217,53 +264,73 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           goff[i][p] = g.rowmod[row] * g.gate_stride;
         }
     }
+    // Pass p of 32 x 32 tile q = i TN + j: rows 8 p + lane / 8, columns
+    // 4 (lane % 8) .. + 3.  The residual and gate rows of tile q + 1 are
+    // requested before tile q is combined, so each tile's global loads wait
+    // behind the previous tile's work instead of stalling on their own
+    // (two register sets; 16-wave tiles, and tiles small enough to run two
+    // blocks per CU, have no registers to spare and load each tile's rows
+    // just before use).
+    constexpr int Q = MBW * TN;
+    constexpr bool kTwoBlocks = T::NST * T::SBYTES <= 80 * 1024;
+    constexpr int NB = (EPI == kEpiGatedResidual && T::NW < 16 && !kTwoBlocks) ? 2 : 1;
+    float4 hv[NB][4], gt[NB][4];
+    const int col0 = (lane & 7) * 4;
+    auto load_rows = [&](int q, int buf) __attribute__((always_inline)) {
+      const int i = q / TN, j = q % TN;
+      const int rb = m0 + (wm * MBW + i) * 32, col = n0 + (wn * TN + j) * 32 + col0;
 #pragma unroll
-    for (int i = 0; i < MBW; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-          const int c = (2 * gq + half) ^ ((r32 >> 1) & 7);
-          *reinterpret_cast<float4 *>(stg + r32 * 128 + c * 16) =
-              make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+      for (int p = 0; p < 4; ++p) {
+        const int row = rb + 8 * p + (lane >> 3);
+        if (row < g.M && col < g.N) {
+          hv[buf][p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
+          if constexpr (kHoist) gt[buf][p] = *reinterpret_cast<const float4 *>(g.gate + goff[i][p] + col);
+          else gt[buf][p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
         }
-        // Pass p: rows 8 p + lane / 8, columns 4 (lane % 8) .. + 3.  All loads first.
-        float4 v[4], hv[4], gt[4];
-        const int col = cb + (lane & 7) * 4;
+      }
+    };
+    if constexpr (EPI == kEpiGatedResidual && NB == 2) load_rows(0, 0);
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int rr = 8 * p + (lane >> 3), c = lane & 7;
-          v[p] = *reinterpret_cast<const float4 *>(stg + rr * 128 + ((c ^ ((rr >> 1) & 7)) * 16));
-          const int row = rb + rr;
-          if (EPI == kEpiGatedResidual && row < g.M && col < g.N) {
-            hv[p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
-            if constexpr (kHoist) gt[p] = *reinterpret_cast<const float4 *>(g.gate + goff[i][p] + col);
-            else gt[p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
-          }
-        }
+    for (int q = 0; q < Q; ++q) {
+      const int i = q / TN, j = q % TN, buf = NB == 2 ? (q & 1) : 0;
+      if constexpr (EPI == kEpiGatedResidual) {
+        if (NB == 1) load_rows(q, 0);
+        else if (q + 1 < Q) load_rows(q + 1, (q + 1) & 1);
+      }
+      const int rb = m0 + (wm * MBW + i) * 32, col = n0 + (wn * TN + j) * 32 + col0;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int row = rb + 8 * p + (lane >> 3);
-          if (row < g.M && col < g.N) {
-            if constexpr (EPI == kEpiPartial) {
-              *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = v[p];
-            } else {
-              float4 h = hv[p];
-              h.x = h.x + gt[p].x * v[p].x;
-              h.y = h.y + gt[p].y * v[p].y;
-              h.z = h.z + gt[p].z * v[p].z;
-              h.w = h.w + gt[p].w * v[p].w;
-              *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
-            }
+      for (int gq = 0; gq < 4; ++gq) {
+        const int c = (2 * gq + half) ^ ((r32 >> 1) & 7);
+        *reinterpret_cast<float4 *>(stg + r32 * 128 + c * 16) =
+            make_float4(acc[i][j][4 * gq], acc[i][j][4 * gq + 1], acc[i][j][4 * gq + 2], acc[i][j][4 * gq + 3]);
+      }
+      float4 v[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int rr = 8 * p + (lane >> 3), c = lane & 7;
+        v[p] = *reinterpret_cast<const float4 *>(stg + rr * 128 + ((c ^ ((rr >> 1) & 7)) * 16));
+      }
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int row = rb + 8 * p + (lane >> 3);
+        if (row < g.M && col < g.N) {
+          if constexpr (EPI == kEpiPartial) {
+            *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = v[p];
+          } else {
+            float4 h = hv[buf][p];
+            h.x = h.x + gt[buf][p].x * v[p].x;
+            h.y = h.y + gt[buf][p].y * v[p].y;
+            h.z = h.z + gt[buf][p].z * v[p].z;
+            h.w = h.w + gt[buf][p].w * v[p].w;
+            *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
           }
         }
       }
+    }
   } else {
     // Each wave stages one 32 x 32 tile at a time in its own 4 KB slot, then
     // reads it back row-contiguous.
-    const int sb = wave / T::PERB;
-    uint8_t *stg = (sb == 0 ? L0 : sb == 1 ? L1 : sb == 2 ? L2 : L3) + (wave % T::PERB) * 4096;
+    uint8_t *stg = L + wave * 4096;
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
@@ -298,10 +365,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
 template <typename T, int EPI>
 __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct, int ksplit) {
   constexpr int SBYTES = T::SBYTES;
-  __shared__ __attribute__((aligned(1024))) uint8_t L0[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L1[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L2[SBYTES];
-  __shared__ __attribute__((aligned(1024))) uint8_t L3[SBYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t L[T::NST * SBYTES];
 
   // Work unit of this block: XCD x = b % 8 takes the x-th eighth of the unit
   // list; unit u is K slice u / n_tiles of tile u % n_tiles (one slice
@@ -315,14 +379,14 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
   const int m0 = (tile / nct) * T::BM, n0 = (tile % nct) * T::BN;
   const int nks = g.K / T::BK / ksplit;
   f32x16 acc[T::MBW][T::TN];
-  gemm_mainloop<T>(g, m0, n0, slice * nks, nks, L0, L1, L2, L3, acc);
+  gemm_mainloop<T>(g, m0, n0, slice * nks, nks, L, acc);
   if constexpr (EPI == kEpiPartial) {
     GemmArgs gp = g;
     gp.out = g.part + (size_t)slice * g.M * g.N;
     gp.ldo = g.N;
-    gemm_epilogue<T, EPI>(gp, m0, n0, L0, L1, L2, L3, acc);
+    gemm_epilogue<T, EPI>(gp, m0, n0, L, acc);
   } else {
-    gemm_epilogue<T, EPI>(g, m0, n0, L0, L1, L2, L3, acc);
+    gemm_epilogue<T, EPI>(g, m0, n0, L, acc);
   }
 }
 
@@ -335,17 +399,17 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
 // more slowly, by an amount that differs between tiles).
 struct GemmCfg { int bm, bn, bk; float a, a2, b[3]; };
 static constexpr GemmCfg kCfgs[kGemmConfigs] = {
-    {384, 128, 32, 15.5f, 19.2f, {9.7f, 13.1f, 19.8f}},  // 0: 8 waves, 96 x 64 each
-    {256, 256, 32, 20.1f, 13.8f, {8.8f, 12.5f, 16.0f}},  // 1: 16 waves, 64 x 64 each
-    {128, 256, 32, 12.5f, 13.0f, {7.5f, 7.9f, 13.8f}},   // 2: 8 waves, 64 x 64 each
-    {192, 128, 32, 12.3f, 3.2f, {5.3f, 4.2f, 9.1f}},     // 3: 8 waves, 96 x 32 each
-    {288, 128, 32, 17.1f, 15.3f, {7.5f, 9.9f, 13.6f}},   // 4: 12 waves, 96 x 32 each
-    {128, 64, 64, 4.6f, 5.0f, {3.0f, 3.2f, 6.9f}},       // 5: 4 waves, 64 x 32 each
-    {192, 128, 64, 8.9f, 6.8f, {6.8f, 8.4f, 13.1f}},     // 6: 8 waves, 96 x 32 each
-    {128, 128, 64, 6.8f, 6.0f, {4.5f, 6.2f, 11.5f}},     // 7: 4 waves, 64 x 64 each
-    {160, 128, 64, 9.5f, 3.4f, {4.6f, 6.5f, 15.1f}},     // 8: 4 waves, 160 x 32 each
-    {96, 128, 64, 6.5f, 4.2f, {3.5f, 4.8f, 9.0f}},       // 9: 4 waves, 96 x 32 each
-    {256, 64, 64, 7.1f, 7.4f, {4.0f, 5.0f, 9.2f}},       // 10: 8 waves, 64 x 32 each
+    {384, 128, 32, 15.5f, 19.2f, {9.5f, 12.8f, 15.3f}},  // 0: 8 waves, 96 x 64 each
+    {256, 256, 32, 18.8f, 13.8f, {9.2f, 12.3f, 16.7f}},  // 1: 16 waves, 64 x 64 each
+    {128, 256, 32, 12.5f, 13.0f, {6.5f, 7.9f, 11.1f}},   // 2: 8 waves, 64 x 64 each
+    {192, 128, 32, 10.7f, 3.2f, {4.9f, 5.5f, 9.4f}},     // 3: 8 waves, 96 x 32 each
+    {288, 128, 32, 13.7f, 15.3f, {8.8f, 10.9f, 13.7f}},  // 4: 12 waves, 96 x 32 each
+    {128, 64, 64, 4.7f, 5.0f, {3.1f, 3.4f, 6.0f}},       // 5: 4 waves, 64 x 32 each
+    {192, 128, 64, 8.8f, 6.8f, {6.2f, 8.2f, 10.9f}},     // 6: 8 waves, 96 x 32 each
+    {128, 128, 64, 6.5f, 6.0f, {4.7f, 6.3f, 9.9f}},      // 7: 4 waves, 64 x 64 each
+    {160, 128, 64, 8.1f, 3.4f, {4.5f, 7.1f, 14.7f}},     // 8: 4 waves, 160 x 32 each
+    {96, 128, 64, 5.5f, 4.2f, {4.3f, 6.0f, 8.9f}},       // 9: 4 waves, 96 x 32 each
+    {256, 64, 64, 6.9f, 7.4f, {4.0f, 4.8f, 8.8f}},       // 10: 8 waves, 64 x 32 each
 };
 using Cfg0 = GemmTile<12, 2, 4, 2>;
 using Cfg1 = GemmTile<8, 2, 4, 4>;

@@ -13,6 +13,37 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;    // 32x32 MFMA accu
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 
+// One 1 KB global -> LDS copy (lane i: 16 bytes from its own source to
+// lds + 16 i), written as inline assembly so the compiler does not track it:
+// its model of this copy makes it wait for every outstanding LDS read before
+// the next MFMA, which would cap the LDS reads in flight at one.  The kernels
+// wait for the copies themselves (vmcnt) and set M0, which nothing else in
+// them uses; the s_nop is the wait state the M0 write needs before the copy.
+// dma_1k_s takes a wave-uniform 64-bit base (SGPRs) plus a 32-bit per-lane
+// byte offset; dma_1k a full per-lane address.
+__device__ __forceinline__ void dma_1k(const void *src, uint32_t lds) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+__device__ __forceinline__ void dma_1k_s(const void *base, uint32_t off, uint32_t lds) {
+  // The base is wave-uniform by construction; reading it through readfirstlane
+  // keeps it in SGPRs even where the compiler cannot prove that.
+  const uint64_t b64 = (uint64_t)(size_t)base;
+  const uint64_t ub = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b64 >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b64);
+  const void *bs = (const void *)(size_t)ub;
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(bs), "s"(lds)
+               : "memory", "m0");
+#pragma clang diagnostic pop
+}
+__device__ __forceinline__ uint32_t lds_u32(const uint8_t *p) {
+  return (uint32_t)(size_t)(__attribute__((address_space(3))) void *)(p);
+}
+
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
 
