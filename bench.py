@@ -323,6 +323,50 @@ def _traffic_rows(out, ff, wf):
     return rows
 
 
+def _summarize_presets(out):
+    """One line per workload from `bench.py --workload W --no-cpu-baseline`
+    runs whose JSON lines were saved as bench_W.log under `out`."""
+    rows = []
+    for w in ("factory_b256", "factory_b256_alternating", "pi0_b1", "pi0_b32", "stress_b512"):
+        f = f"{out}/bench_{w}.log"
+        if not os.path.exists(f):
+            continue
+        try:
+            j = json.loads(open(f).read().strip().splitlines()[-1])
+        except (ValueError, IndexError):
+            continue
+        if j.get("config", {}).get("workload") == w:
+            rows.append((w, j))
+    if not rows:
+        return
+    lines = ["# Whole-call results per workload (one MI355X, bf16)", "",
+             "Commands (repository root, library built in-tree), one per workload:", "", "```",
+             "export TMPDIR=/tmp",
+             *[f"timeout -k 10 300 python -u bench.py --workload {w.replace('_alternating', '')} --no-cpu-baseline"
+               + (" --attention-layout alternating" if w.endswith("_alternating") else "") + f" > {out}/bench_{w}.log"
+               for w, _ in rows],
+             f"python bench.py --summarize-profiles {out}", "```", "",
+             "Each line: 3 warm-up + 20 timed calls; chunks/s = requests x calls / wall time; per-call kernel time "
+             "from the library's per-launch events (one extra pass).", "",
+             "| Workload | Requests | Action tokens | Prefix tokens | chunks/s | ms per call | p50 ms | p99 ms | "
+             "attention ms/call | GEMMs ms/call | attention GB/s (frac of 8 TB/s) | GEMM TFLOP/s (frac of 2.5 PF) |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for w, j in rows:
+        k = j.get("kernels", {})
+        att = k.get("attention", {})
+        gm = sum(v.get("ms_per_call", 0) for n, v in k.items() if n.startswith("gemm_"))
+        lines.append(f"| {w} | {j['config']['requests']} | {j['config']['action_tokens']} | "
+                     f"{j['config']['prefix_tokens']} | {j['value']} | {j['ms_per_step']} | {j['p50_ms']} | "
+                     f"{j['p99_ms']} | {att.get('ms_per_call', 0):.2f} | {gm:.2f} | "
+                     f"{att.get('achieved', 0):.0f} ({att.get('frac', 0):.3f}) | "
+                     f"{j['gemm_all']['achieved']} ({j['gemm_all']['frac']:.3f}) |")
+    srcs = {f: hashlib.sha256(open(os.path.join(ROOT, "paper_2607_01088_amd", "csrc", f), "rb").read()).hexdigest()[:16]
+            for f in ("k_attn.hip", "k_gemm.hip")}
+    lines += ["", "Kernel source sha256 (first 16 hex digits) when measured: " +
+              ", ".join(f"`{f}` `{h}`" for f, h in srcs.items()) + "."]
+    open(os.path.join(PROFILES, "bench_workloads.md"), "w").write("\n".join(lines) + "\n")
+
+
 def summarize_profiles(out):
     """Turn rocprofv3 outputs of this script into the summaries under
     profiles/ (kernel-time table, calibrated HBM traffic of the attention
@@ -335,6 +379,7 @@ def summarize_profiles(out):
         _summarize_prefill(out)
     if glob.glob(f"{out}/pmc_util/**/*counter_collection.csv", recursive=True):
         _summarize_pmc(out)
+    _summarize_presets(out)
     if not glob.glob(f"{out}/prof_factory/**/*kernel_stats.csv", recursive=True):
         return
     stats = _csv_rows(f"{out}/prof_factory/**/*kernel_stats.csv")
@@ -406,6 +451,28 @@ def copy_probe(torch):
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read_per_launch": n, "copy_probe_bytes_written_per_launch": n,
                       "launches": 5}), flush=True)
+
+
+def measured_peaks(torch, rosa):
+    """Attainable peaks on this GPU, taken after the timed region: a plain
+    512 MiB device-to-device copy (read + write bytes per second, best of 5)
+    and the library's MFMA-only loop (dense bf16, rosa_debug_mfma_peak)."""
+    n = 512 << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = 0.0
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = max(best, 2 * n / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    del src, dst
+    return {"hbm_copy_gbs": round(best, 1), "mfma_bf16_tflops": round(rosa.mfma_peak(torch.cuda.current_device()), 1),
+            "how": "best of 5 timed 512 MiB device-to-device copies (2 x bytes / time); "
+                   "rosa_debug_mfma_peak (back-to-back 32x32x16 bf16 MFMAs, 2 waves per SIMD on every CU)"}
 
 
 def batch_profile(torch, rosa, expert, db, reqs, preset, args):
@@ -918,6 +985,10 @@ def main():
     gemm_total_ms = sum(kernels[k]["ms_per_call"] for k in gemm_flops if k in kernels)
     gemm_all = sum(gemm_flops.values()) / (gemm_total_ms * 1e-3) / 1e12
 
+    peaks = measured_peaks(torch, rosa)
+    mpeak = peaks["hbm_copy_gbs"] if roofline["bound"] == "hbm" else peaks["mfma_bf16_tflops"]
+    roofline["frac_of_measured_peak"] = round(roofline["achieved"] / mpeak, 4) if mpeak else None
+
     B = len(reqs)
     ms_per_step = elapsed / args.steps * 1e3
     value = B * args.steps / elapsed
@@ -938,7 +1009,10 @@ def main():
         "p99_ms": round(float(np.percentile(lat, 99)), 3),
         "roofline": roofline,
         "gemm_all": {"achieved": round(gemm_all, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
-                     "frac": round(gemm_all / MFMA_BF16_PEAK_TFS, 4)},
+                     "frac": round(gemm_all / MFMA_BF16_PEAK_TFS, 4),
+                     "frac_of_measured_peak": round(gemm_all / peaks["mfma_bf16_tflops"], 4)
+                     if peaks["mfma_bf16_tflops"] else None},
+        "measured_peaks": peaks,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kernels.items()},
         "prefix_kv_gb": round(kv_bytes / 1e9, 3),

@@ -55,6 +55,15 @@ rosa_status rosa_debug_attn_lists(const rosa_model_config *cfg, const rosa_capac
                                   int32_t *n_blocks, int32_t *n_entries, int32_t *item_of,
                                   int32_t *next, int32_t *item_cost);
 
+/* Attainable dense bf16 MFMA throughput of GPU `device`: times a kernel that
+ * issues nothing but back-to-back v_mfma_f32_32x32x16_bf16 (eight
+ * independent accumulators per wave, two waves per SIMD on every CU) and
+ * writes the rate in TFLOP/s to *tflops (the clock the chip holds under that
+ * load sets it, not the boost clock of the published peak).  Synchronous,
+ * about 10 ms; allocates and frees a small buffer and a stream.
+ * ROSA_E_DEVICE on any HIP error. */
+rosa_status rosa_debug_mfma_peak(int32_t device, double *tflops);
+
 /* Time conditioning alone: for n flow times taus (HOST fp32), write the
  * modulation table rows to out (DEVICE fp32 [n][L*6d + 2d]): per layer l the
  * six d-wide vectors [shift_a|scale_a|gate_a|shift_m|scale_m|gate_m] at offset

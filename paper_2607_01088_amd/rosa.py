@@ -154,6 +154,8 @@ def load(path: Optional[str] = None) -> C.CDLL:
                                           C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32),
                                           C.POINTER(i32)]
     lib.rosa_debug_attn_lists.restype = C.c_int
+    lib.rosa_debug_mfma_peak.argtypes = [i32, C.POINTER(C.c_double)]
+    lib.rosa_debug_mfma_peak.restype = C.c_int
     lib.rosa_debug_time_conditioning.argtypes = [vp, C.POINTER(C.c_float), i32, vp]
     lib.rosa_debug_time_conditioning.restype = C.c_int
     lib.rosa_debug_attention.argtypes = [vp, C.POINTER(Request), i32, i32, vp, vp]
@@ -287,6 +289,16 @@ def attn_lists(shape, cap: Capacity, reqs: Sequence[Request], n_items: int):
     cost = (C.c_int32 * max(1, n_items))()
     st = lib.rosa_debug_attn_lists(C.byref(cfg), C.byref(cap), arr, n, m, C.byref(nb), C.byref(ne), item_of, nxt, cost)
     return st, nb.value, list(item_of)[:ne.value], list(nxt)[:ne.value], list(cost)[:n_items]
+
+
+def mfma_peak(device: int = 0) -> float:
+    """Attainable dense bf16 MFMA rate of the GPU in TFLOP/s (rosa_debug_mfma_peak)."""
+    lib = load()
+    v = C.c_double(0.0)
+    st = lib.rosa_debug_mfma_peak(device, C.byref(v))
+    if st != ROSA_OK:
+        raise RosaError(st, "rosa_debug_mfma_peak failed")
+    return v.value
 
 
 def s1_simulate(robots: int, batch: int, batch_ms: float, t_act_ms: float, n_batches: int = 256) -> Dict[str, float]:
