@@ -759,7 +759,11 @@ hipError_t noalloc_scratch(int dev, uint8_t **out) {
 extern "C" {
 
 const char *rosa_status_string(rosa_status s) {
-  switch (s) {
+  // A C caller may pass any int; read it as one (loading an out-of-range
+  // value through the enum type is undefined in C++).
+  int v;
+  std::memcpy(&v, &s, sizeof v);
+  switch (v) {
     case ROSA_OK: return "ok";
     case ROSA_E_INVALID: return "invalid argument";
     case ROSA_E_CAPACITY: return "capacity exceeded";

@@ -119,11 +119,13 @@ _lib = None
 
 
 def load(path: Optional[str] = None) -> C.CDLL:
-    """Load the built library (raises if it has not been built)."""
+    """Load the built library (raises if it has not been built): `path`, else
+    $ROSA_LIB_PATH (another build, e.g. the sanitized one), else the in-tree
+    librosa.so."""
     global _lib
     if _lib is not None:
         return _lib
-    p = path or _LIB_PATH
+    p = path or os.environ.get("ROSA_LIB_PATH") or _LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"rosa HIP library not built: {p} is missing "
                            "(run python -m paper_2607_01088_amd.build)")
