@@ -482,9 +482,10 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
       if (base + r < it.nq) {
         const int qrow = it.q0 + base + r;
         const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * 2 * HD + ((c ^ (r & (CPRO - 1))) * 16));
-        bf16 *op = reinterpret_cast<bf16 *>(a.o) + (size_t)(it.tok_off + qrow / G) * a.ldo +
-                   (size_t)(it.kvh * G + qrow % G) * HD;
-        *reinterpret_cast<uint4 *>(op + c * 8) = v;
+        const size_t orow = (size_t)(it.tok_off + qrow / G), ocol = (size_t)(it.kvh * G + qrow % G) * HD + c * 8;
+        // row-major, or kb32 (the 16-byte chunk stays inside one 32-wide block)
+        const size_t off = a.o_rows > 0 ? kb32_offset(a.o_rows, orow, ocol) : orow * a.ldo + ocol;
+        *reinterpret_cast<uint4 *>(reinterpret_cast<bf16 *>(a.o) + off) = v;
       }
     }
   }
@@ -580,7 +581,7 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
                                                          const ReqDesc *__restrict__ reqs,
                                                          const float *__restrict__ part_o,
                                                          const float *__restrict__ part_ml, OutT *o,
-                                                         int ldo, int nq, int nkv, int hd) {
+                                                         int ldo, int nq, int nkv, int hd, int o_rows) {
   const AttnGroup gr = groups[blockIdx.y];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int qloc = blockIdx.x * 4 + wave;
@@ -628,14 +629,18 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
     }
   }
   const float inv = 1.0f / L;
-  OutT *op = o + (size_t)(tok_off + qt) * ldo + (size_t)qg * hd;
+  const size_t orow = (size_t)(tok_off + qt);
 #pragma unroll
   for (int j = 0; j < kMaxE; ++j)
-    if (lane + 64 * j < hd) op[lane + 64 * j] = from_f32<OutT>(acc[j] * inv);
+    if (lane + 64 * j < hd) {
+      const size_t col = (size_t)qg * hd + lane + 64 * j;
+      o[o_rows > 0 ? kb32_offset(o_rows, orow, col) : orow * ldo + col] = from_f32<OutT>(acc[j] * inv);
+    }
 }
 
 hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
+  if (a.o_rows > 0 && !bf16_mode) return hipErrorInvalidValue;
   if (bf16_mode) {
     if (a.n_blocks <= 0) return hipSuccess;
     dim3 grid(a.n_blocks);
@@ -661,16 +666,17 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
 
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
-                             int nkv, int hd, bool bf16_mode, hipStream_t s) {
+                             int nkv, int hd, bool bf16_mode, hipStream_t s, int o_rows) {
   if (n_groups <= 0) return hipSuccess;
   if (hd > 256) return hipErrorInvalidValue;   // a lane holds at most 4 head-dim elements
+  if (o_rows > 0 && !bf16_mode) return hipErrorInvalidValue;
   dim3 grid(kAttnQB / 4, n_groups);
   if (bf16_mode)
     hipLaunchKernelGGL(attn_merge_kernel<bf16>, grid, dim3(256), 0, s, groups, reqs, part_o, part_ml,
-                       (bf16 *)o, ldo, nq, nkv, hd);
+                       (bf16 *)o, ldo, nq, nkv, hd, o_rows);
   else
     hipLaunchKernelGGL(attn_merge_kernel<float>, grid, dim3(256), 0, s, groups, reqs, part_o, part_ml,
-                       (float *)o, ldo, nq, nkv, hd);
+                       (float *)o, ldo, nq, nkv, hd, 0);
   return hipGetLastError();
 }
 

@@ -101,10 +101,14 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
 
   // Copy sources: 1 KB unit u (A rows first, then W rows) is copied by wave
   // u % NW; lane i writes physical chunk i % CPR of row i / CPR of the unit,
-  // which holds logical chunk (i % CPR) ^ gswz(row).  Rows past M (or N)
+  // which holds logical chunk (i % CPR) ^ gswz(row).  Both operands are kb32
+  // (planes of R rows: a_rows for A, N for W), so logical chunk c of a row
+  // (k = k0 + 8 c) lies in plane k0 / 32 + c / 4 and a unit reads one (32 of
+  // K) or two (64 of K) contiguous 512 B - 1 KB runs.  Rows past M (or N)
   // re-read the last row; their results are never stored.
   constexpr int CPR = T::CPR, RPU = T::RPU;
   const bf16 *src[CHI];
+  size_t kstep[CHI];                        // elements per 32 of K: 32 R
 #pragma unroll
   for (int j = 0; j < CHI; ++j) {
     const int u = min(j * NW + wave, T::U - 1);
@@ -112,18 +116,20 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
     const int csrc = (lane % CPR) ^ gswz<CPR>(lrow);
     if (u < T::BM / RPU) {
       const int row = min(m0 + lrow, g.M - 1);
-      src[j] = A + (size_t)row * g.lda + csrc * 8;
+      kstep[j] = (size_t)g.a_rows * 32;
+      src[j] = A + ((size_t)(csrc >> 2) * g.a_rows + row) * 32 + (csrc & 3) * 8;
     } else {
       const int row = min(n0 + lrow - T::BM, g.N - 1);
-      src[j] = W + (size_t)row * g.K + csrc * 8;
+      kstep[j] = (size_t)g.N * 32;
+      src[j] = W + ((size_t)(csrc >> 2) * g.N + row) * 32 + (csrc & 3) * 8;
     }
   }
   const bool hi = wave < T::NHI;
   constexpr int BK = T::BK, ROWB = T::ROWB;
   // Copy j (of CHI) of this wave for stage kt into buffer st.
   auto issue_one = [&](uint8_t *st, int kt, int j) __attribute__((always_inline)) {
-    const int k0 = (kt0 + min(kt, nk - 1)) * BK;   // past the end: repeat the last stage (never read)
-    if (j < CLO || hi) dma_1k(src[j] + k0, lds_u32(st) + (uint32_t)((j * NW + wave) * 1024));
+    const int kb = (kt0 + min(kt, nk - 1)) * (BK / 32);   // past the end: repeat the last stage (never read)
+    if (j < CLO || hi) dma_1k(src[j] + (size_t)kb * kstep[j], lds_u32(st) + (uint32_t)((j * NW + wave) * 1024));
   };
   auto issue = [&](uint8_t *st, int kt) __attribute__((always_inline)) {
 #pragma unroll
@@ -355,8 +361,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           const int rr = 16 * p + (lane >> 2), c = lane & 3;
           const bf16x8 v = *reinterpret_cast<const bf16x8 *>(stg + rr * 64 + ((c ^ ((rr >> 2) & 3)) * 16));
           const int row = rb + rr, col = cb + c * 8;
-          if (row < g.M && col < g.N)
-            *reinterpret_cast<bf16x8 *>(reinterpret_cast<bf16 *>(g.out) + (size_t)row * g.ldo + col) = v;
+          if (row < g.M && col < g.N) {
+            const size_t off = g.out_rows > 0 ? kb32_offset(g.out_rows, row, col) : (size_t)row * g.ldo + col;
+            *reinterpret_cast<bf16x8 *>(reinterpret_cast<bf16 *>(g.out) + off) = v;
+          }
         }
       }
   }
@@ -459,7 +467,8 @@ __global__ void __launch_bounds__(256) gemm_split_reduce_kernel(GemmArgs g, int 
       }
       bf16x4 o;
       o[0] = (bf16)a0; o[1] = (bf16)a1; o[2] = (bf16)a2; o[3] = (bf16)a3;
-      *reinterpret_cast<bf16x4 *>(reinterpret_cast<bf16 *>(g.out) + (size_t)row * g.ldo + col) = o;
+      const size_t off = g.out_rows > 0 ? kb32_offset(g.out_rows, row, col) : (size_t)row * g.ldo + col;
+      *reinterpret_cast<bf16x4 *>(reinterpret_cast<bf16 *>(g.out) + off) = o;
     }
   }
 }
@@ -501,7 +510,7 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split
 
 static hipError_t launch_cfg(const GemmArgs &g, int cfg, hipStream_t s, bool allow_split) {
   if (g.M <= 0) return hipSuccess;
-  if (g.K % 128 != 0 || g.N % 8 != 0) return hipErrorInvalidValue;
+  if (g.K % 128 != 0 || g.N % 8 != 0 || g.a_rows < g.M) return hipErrorInvalidValue;
   switch (cfg) {
     case 0: return launch_tile<Cfg0>(g, s, allow_split);
     case 1: return launch_tile<Cfg1>(g, s, allow_split);

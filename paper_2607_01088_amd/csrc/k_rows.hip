@@ -101,7 +101,7 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
                                                       const float *__restrict__ modtab, int mod_stride,
                                                       int shift_off, int scale_off,
                                                       const int32_t *__restrict__ rowmod,
-                                                      OutT *__restrict__ u) {
+                                                      OutT *__restrict__ u, int u_rows) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
@@ -146,7 +146,9 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
         a = *reinterpret_cast<const float4 *>(scale + i);
         b = *reinterpret_cast<const float4 *>(shift + i);
       }
-      store4<OutT>(ur + i, v[c].x * r * (1.0f + a.x) + b.x, v[c].y * r * (1.0f + a.y) + b.y,
+      // row-major, or (u_rows > 0) kb32: the 4 values stay inside one 32-wide block
+      OutT *up = u_rows > 0 ? u + kb32_offset(u_rows, row, i) : ur + i;
+      store4<OutT>(up, v[c].x * r * (1.0f + a.x) + b.x, v[c].y * r * (1.0f + a.y) + b.y,
                    v[c].z * r * (1.0f + a.z) + b.z, v[c].w * r * (1.0f + a.w) + b.w);
     }
   }
@@ -154,25 +156,47 @@ __global__ void __launch_bounds__(256) modnorm_kernel(const float *__restrict__ 
 
 hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *modtab, int mod_stride,
                           int shift_off, int scale_off, const int32_t *rowmod, void *u, bool bf16_out,
-                          hipStream_t s) {
+                          hipStream_t s, int u_rows) {
   if (M <= 0) return hipSuccess;
   if (d % 4 || d > kNormChunks * 256) return hipErrorInvalidValue;
+  if (u_rows > 0 && (!bf16_out || d % 32 || u_rows < M)) return hipErrorInvalidValue;
   dim3 grid((M + 3) / 4);
   const int nc = (d + 255) / 256;
   auto go = [&](auto tag) {
     constexpr int NC = decltype(tag)::value;
     if (bf16_out)
       hipLaunchKernelGGL((modnorm_kernel<bf16, NC>), grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
-                         shift_off, scale_off, rowmod, (bf16 *)u);
+                         shift_off, scale_off, rowmod, (bf16 *)u, u_rows);
     else
       hipLaunchKernelGGL((modnorm_kernel<float, NC>), grid, dim3(256), 0, s, h, M, d, eps, modtab, mod_stride,
-                         shift_off, scale_off, rowmod, (float *)u);
+                         shift_off, scale_off, rowmod, (float *)u, 0);
   };
   if (nc <= 1) go(std::integral_constant<int, 1>{});
   else if (nc <= 2) go(std::integral_constant<int, 2>{});
   else if (nc <= 4) go(std::integral_constant<int, 4>{});
   else if (nc <= 8) go(std::integral_constant<int, 8>{});
   else go(std::integral_constant<int, 16>{});
+  return hipGetLastError();
+}
+
+// bf16 row-major [M][K] -> kb32 planes of R rows: one thread per 8 values
+// (16 bytes), consecutive threads along K within a row.
+__global__ void __launch_bounds__(256) kb32_pack_kernel(const bf16 *__restrict__ src, int M, int K, int lda,
+                                                        bf16 *__restrict__ dst, int R) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const int per_row = K / 8;
+  if (i >= (size_t)M * per_row) return;
+  const int m = (int)(i / per_row), k = (int)(i % per_row) * 8;
+  *reinterpret_cast<bf16x8 *>(dst + kb32_offset(R, m, k)) =
+      *reinterpret_cast<const bf16x8 *>(src + (size_t)m * lda + k);
+}
+
+hipError_t launch_kb32_pack(const void *src, int M, int K, int lda, void *dst, int R, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (K % 32 || R < M || lda < K) return hipErrorInvalidValue;
+  const size_t n = (size_t)M * (K / 8);
+  hipLaunchKernelGGL(kb32_pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, (const bf16 *)src, M, K,
+                     lda, (bf16 *)dst, R);
   return hipGetLastError();
 }
 
@@ -289,7 +313,7 @@ __global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restr
                                                              const bf16 *__restrict__ wt, const float *__restrict__ b_out,
                                                              int A, const int32_t *__restrict__ row_req,
                                                              const ReqDesc *__restrict__ reqs, int step,
-                                                             float *__restrict__ x, int row0) {
+                                                             float *__restrict__ x, int row0, int u_rows) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds_out[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
   const int cpr = KC / 8;                       // 16-byte chunks per LDS row
@@ -314,11 +338,13 @@ __global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restr
         }
         __syncthreads();
       }
-      const bf16 *ap = u + (size_t)arow * d + c * KC + half * 8;
       for (int k0 = 0; k0 < KC / 16; k0 += 8) {
         bf16x8 af[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) af[j] = *reinterpret_cast<const bf16x8 *>(ap + (k0 + j) * 16);
+        for (int j = 0; j < 8; ++j) {
+          const int k = c * KC + (k0 + j) * 16 + half * 8;   // 8 values inside one 32-wide block
+          af[j] = *reinterpret_cast<const bf16x8 *>(u + (u_rows > 0 ? kb32_offset(u_rows, arow, k) : (size_t)arow * d + k));
+        }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int ch = 2 * (k0 + j) + half;
@@ -360,9 +386,9 @@ size_t out_proj_lds_bytes(int d, int A) {
 
 hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, const float *b_out, int A,
                                  const int32_t *row_req, const ReqDesc *reqs, int step, float *x, int row0,
-                                 hipStream_t s) {
+                                 hipStream_t s, int u_rows) {
   if (M <= 0) return hipSuccess;
-  if (d % 128 || A < 1 || A > 64) return hipErrorInvalidValue;
+  if (d % 128 || A < 1 || A > 64 || (u_rows > 0 && u_rows < M)) return hipErrorInvalidValue;
   const int nb = A <= 32 ? 1 : 2;
   const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
   const size_t lds = (size_t)nb * 32 * kc * 2;
@@ -376,9 +402,11 @@ hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, co
   const int nrb = (M + 31) / 32;
   const int blocks = std::min((nrb + 3) / 4, 256);
   if (nb == 1)
-    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x, row0);
+    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req,
+                       reqs, step, x, row0, u_rows);
   else
-    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req, reqs, step, x, row0);
+    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req,
+                       reqs, step, x, row0, u_rows);
   return hipGetLastError();
 }
 

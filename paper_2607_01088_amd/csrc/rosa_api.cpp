@@ -119,6 +119,23 @@ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+hipError_t upload_weights_kb32(void *dst, const float *src, int L, int K, int N) {
+  const size_t per = (size_t)K * N;
+  std::vector<uint16_t> tmp(per * L);
+  auto work = [&](int l) {
+    const float *s = src + per * l;
+    uint16_t *d = tmp.data() + per * l;
+    for (int k = 0; k < K; ++k)
+      for (int n = 0; n < N; ++n) d[kb32_offset(N, n, k)] = f32_to_bf16_rne(s[(size_t)k * N + n]);
+  };
+  std::vector<std::thread> th;
+  const int nt = std::max(1, std::min(L, 8));
+  for (int t = 0; t < nt; ++t)
+    th.emplace_back([&, t] { for (int l = t; l < L; l += nt) work(l); });
+  for (auto &x : th) x.join();
+  return hipMemcpy(dst, tmp.data(), tmp.size() * 2, hipMemcpyHostToDevice);
+}
+
 hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16) {
   const size_t per = (size_t)K * N;
   std::vector<uint8_t> tmp(per * L * (bf16 ? 2 : 4));
@@ -214,6 +231,9 @@ struct rosa_batch {
   hipStream_t stream = nullptr;
   bool poisoned = false;
   int gemm_cfg = -1;                 // forced projection block configuration, -1: cost model
+  // bf16: u, o and g (the projections' A operands) are kb32 with planes of
+  // kb_rows rows (the handle's row capacity); 0 in fp32 mode (row-major).
+  int kb_rows = 0;
   // Lanes: sub-batches run concurrently; lane 0 uses `stream`, lane l > 0 its own
   // stream (default priority), forked after the time conditioning and joined back.
   int lanes = 1;
@@ -653,7 +673,7 @@ hipError_t run_time_conditioning(rosa_batch *b, const float *d_taus, int n_tau, 
 
 // Attention of one layer for the requests active at step k of lane ln.
 hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int k, int layer, const void *qkv,
-                         void *o, hipStream_t st) {
+                         void *o, hipStream_t st, int o_rows) {
   const Dims &D = b->dims;
   const ReqDesc *reqs = (const ReqDesc *)((uint8_t *)b->d_plan + b->off_reqs);
   const AttnItem *items = (const AttnItem *)((uint8_t *)b->d_plan + b->off_items);
@@ -674,14 +694,14 @@ hipError_t run_attention(rosa_batch *b, const Plan &p, const Plan::Lane &ln, int
     a.n_blocks = ln.list_blocks[v][k];
   }
   a.reqs = reqs; a.layer = layer;
-  a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
+  a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim; a.o_rows = o_rows;
   a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
   a.part_o = b->part_o; a.part_ml = b->part_ml;
   hipError_t e = timed(b, kcAttention, [&] { return launch_attention(a, b->bf16, st); });
   if (e == hipSuccess && gr_hi > gr_lo)
     e = timed(b, kcMerge, [&] {
       return launch_attn_merge(groups + gr_lo, gr_hi - gr_lo, reqs, b->part_o, b->part_ml, o, D.o_dim, D.nq, D.nkv,
-                               D.hd, b->bf16, st);
+                               D.hd, b->bf16, st, o_rows);
     });
   return e;
 }
@@ -826,6 +846,7 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     b->b_out = dalloc<float>(b, D.A, e);
     if (b->bf16) b->wt_out = dalloc<uint8_t>(b, (size_t)d * D.A * 2, e);
     // workspaces
+    b->kb_rows = b->bf16 ? (int)maxM : 0;
     b->x = dalloc<float>(b, maxM * D.A, e);
     b->h = dalloc<float>(b, maxM * d, e);
     b->u = dalloc<uint8_t>(b, maxM * d * b->esz, e);
@@ -900,10 +921,10 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
     if (e == hipSuccess) e = hipMemcpy(b->b_t2, w->b_t2, d * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = upload_act(b, b->w_modall, modall.data(), modall.size());
     if (e == hipSuccess) e = hipMemcpy(b->b_modall, bmodall.data(), bmodall.size() * 4, hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = upload_transposed(b, b->wt_qkv, w->w_qkv, D.L, D.d, D.qkv_dim);
-    if (e == hipSuccess) e = upload_transposed(b, b->wt_o, w->w_o, D.L, D.o_dim, D.d);
-    if (e == hipSuccess) e = upload_transposed(b, b->wt_up, w->w_up, D.L, D.d, D.dff);
-    if (e == hipSuccess) e = upload_transposed(b, b->wt_down, w->w_down, D.L, D.dff, D.d);
+    if (e == hipSuccess) e = upload_gemm_weights(b->wt_qkv, w->w_qkv, D.L, D.d, D.qkv_dim, b->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(b->wt_o, w->w_o, D.L, D.o_dim, D.d, b->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(b->wt_up, w->w_up, D.L, D.d, D.dff, b->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(b->wt_down, w->w_down, D.L, D.dff, D.d, b->bf16);
     if (e == hipSuccess) e = hipMemcpy(b->w_out, w->w_out, d * D.A * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(b->b_out, w->b_out, D.A * 4, hipMemcpyHostToDevice);
     if (e == hipSuccess && b->bf16) e = upload_transposed(b, b->wt_out, w->w_out, 1, D.d, D.A);
@@ -971,47 +992,50 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
         const hipStream_t st = b->lane_stream[li];
         const size_t r0 = (size_t)ln.row_lo;
         // This lane's rows of every per-row buffer.
+        // (kb32 operands: a lane's rows start r0 rows into every 32-wide plane.)
+        const int R = b->kb_rows;
         float *x = b->x + r0 * D.A, *h = b->h + r0 * D.d;
-        uint8_t *u = (uint8_t *)b->u + r0 * D.d * es, *qkv = (uint8_t *)b->qkv + r0 * D.qkv_dim * es;
-        uint8_t *o = (uint8_t *)b->o + r0 * D.o_dim * es, *g = (uint8_t *)b->g + r0 * D.dff * es;
+        uint8_t *u = (uint8_t *)b->u + r0 * (R ? 32 : D.d) * es, *qkv = (uint8_t *)b->qkv + r0 * D.qkv_dim * es;
+        uint8_t *o = (uint8_t *)b->o + r0 * (R ? 32 : D.o_dim) * es, *g = (uint8_t *)b->g + r0 * (R ? 32 : D.dff) * es;
         const int32_t *rowmod = b->rowmod + (size_t)k * p.M0 + r0;
         const int32_t *row_req = b->row_req + r0;
         e = timed(b, kcInProj, [&] { return launch_in_proj(x, M, D.A, b->w_in, b->b_in, D.d, h, st); });
         for (int l = 0; l < D.L && e == hipSuccess; ++l) {
           const int base = (int)(l * d6);
           e = timed(b, kcModNorm, [&] {
-            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16, st);
+            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16, st,
+                                  R);
           });
           if (e != hipSuccess) break;
           GemmArgs gq{};
           if (nl == 1) { gq.part = b->gemm_part; gq.part_floats = b->gemm_part_floats; }
-          gq.a = u; gq.lda = D.d; gq.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * es;
+          gq.a = u; gq.lda = D.d; gq.a_rows = R; gq.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * es;
           gq.M = M; gq.N = D.qkv_dim; gq.K = D.d; gq.epi = kEpiStore; gq.out = qkv; gq.ldo = D.qkv_dim;
           e = timed(b, kcGemmQKV, [&] { return launch_gemm(gq, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
-          e = run_attention(b, p, ln, k, l, b->qkv, b->o, st);
+          e = run_attention(b, p, ln, k, l, b->qkv, b->o, st, b->kb_rows);
           if (e != hipSuccess) break;
           GemmArgs go{};
           if (nl == 1) { go.part = b->gemm_part; go.part_floats = b->gemm_part_floats; }
-          go.a = o; go.lda = D.o_dim; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
+          go.a = o; go.lda = D.o_dim; go.a_rows = R; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
           go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = h; go.ldo = D.d;
           go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
           e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
           e = timed(b, kcModNorm, [&] {
             return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, u,
-                                  b->bf16, st);
+                                  b->bf16, st, R);
           });
           if (e != hipSuccess) break;
           GemmArgs gu{};
           if (nl == 1) { gu.part = b->gemm_part; gu.part_floats = b->gemm_part_floats; }
-          gu.a = u; gu.lda = D.d; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * es;
+          gu.a = u; gu.lda = D.d; gu.a_rows = R; gu.out_rows = R; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * es;
           gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = g; gu.ldo = D.dff;
           e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
           GemmArgs gd{};
           if (nl == 1) { gd.part = b->gemm_part; gd.part_floats = b->gemm_part_floats; }
-          gd.a = g; gd.lda = D.dff; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * es;
+          gd.a = g; gd.lda = D.dff; gd.a_rows = R; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * es;
           gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = h; gd.ldo = D.d;
           gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
           e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, st, b->gemm_cfg); });
@@ -1020,12 +1044,12 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
         const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
         if (e == hipSuccess && b->bf16) {
           e = timed(b, kcFinal, [&] {
-            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, u, true, st);
+            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, u, true, st, R);
           });
           if (e == hipSuccess)
             e = timed(b, kcFinal, [&] {
               return launch_out_proj_euler((const __bf16 *)u, M, D.d, (const __bf16 *)b->wt_out, b->b_out, D.A, row_req,
-                                           d_reqs, k, x, (int)r0, st);
+                                           d_reqs, k, x, (int)r0, st, R);
             });
         } else if (e == hipSuccess) {
           e = timed(b, kcFinal, [&] {
@@ -1199,7 +1223,7 @@ rosa_status rosa_debug_attention(rosa_batch *b, const rosa_request *reqs, int32_
     if (n == 0) return ROSA_OK;
     hipError_t e = hipSetDevice(b->device);
     if (e == hipSuccess) e = upload_plan(b, p, reqs, n);
-    if (e == hipSuccess) e = run_attention(b, p, p.lanes[0], 0, layer, qkv, o, b->stream);
+    if (e == hipSuccess) e = run_attention(b, p, p.lanes[0], 0, layer, qkv, o, b->stream, 0);
     if (e != hipSuccess) return device_fail(b, e, "attention");
     return ROSA_OK;
   } catch (...) {
@@ -1331,6 +1355,14 @@ rosa_status rosa_debug_gemm(rosa_batch *b, int32_t which, int32_t layer, const v
     }
     const int cls = which == 0 ? kcGemmQKV : which == 1 ? kcGemmO : which == 2 ? kcGemmUp : kcGemmDown;
     hipError_t e = hipSetDevice(b->device);
+    if (e == hipSuccess && b->bf16) {
+      // The caller's row-major A, repacked kb32 into the workspace the step
+      // loop uses for this operand; the output stays row-major.
+      void *ws = which == 1 ? b->o : which == 3 ? b->g : b->u;
+      e = launch_kb32_pack(a, M, g.K, g.lda, ws, b->kb_rows, b->stream);
+      g.a = ws;
+      g.a_rows = b->kb_rows;
+    }
     if (e == hipSuccess) e = timed(b, cls, [&] { return launch_gemm(g, b->bf16, b->stream, b->gemm_cfg); });
     if (e != hipSuccess) return device_fail(b, e, "gemm");
     return ROSA_OK;

@@ -105,28 +105,42 @@ hipError_t launch_setup_rows(const ReqDesc *reqs, int n_req, const int32_t *tau_
                              int A, int32_t *row_req, int32_t *rowmod, int M0, float *x, hipStream_t s);
 hipError_t launch_in_proj(const float *x, int M, int A, const float *w_in, const float *b_in, int d,
                           float *h, hipStream_t s);
+// u: bf16 mode with u_rows > 0: kb32 planes of u_rows rows; else row-major [M][d].
 hipError_t launch_modnorm(const float *h, int M, int d, float eps, const float *modtab, int mod_stride,
                           int shift_off, int scale_off, const int32_t *rowmod, void *u, bool bf16,
-                          hipStream_t s);
+                          hipStream_t s, int u_rows = 0);
+// bf16 row-major [M][K] (row stride lda) -> kb32 planes of R rows.
+hipError_t launch_kb32_pack(const void *src, int M, int K, int lda, void *dst, int R, hipStream_t s);
 hipError_t launch_final_euler(const float *h, int M, int d, float eps, const float *modtab,
                               int mod_stride, int shift_off, int scale_off, const int32_t *rowmod,
                               const float *w_out, const float *b_out, int A, const int32_t *row_req,
                               const ReqDesc *reqs, int step, float *x, int row0, hipStream_t s);
 
-// bf16 mode: v = u W_out + b_out on final-normalized rows u (bf16 [M][d]), Euler step
+// bf16 mode: v = u W_out + b_out on final-normalized rows u (bf16 [M][d], or kb32
+// planes of u_rows rows when u_rows > 0), Euler step
 // x += v / K per row's request, actions written on its last step.  wt = W_out^T bf16 [A][d].
 // u, row_req and x point at the first of the M rows, which is stacked row row0.
 hipError_t launch_out_proj_euler(const __bf16 *u, int M, int d, const __bf16 *wt, const float *b_out, int A,
                                  const int32_t *row_req, const ReqDesc *reqs, int step, float *x, int row0,
-                                 hipStream_t s);
+                                 hipStream_t s, int u_rows = 0);
 
-// GEMM: C[M][N] = A[M][K] * W^T where Wt is [N][K] (K contiguous).
+// K-blocked layout of a bf16 GEMM operand ("kb32"): element (m, k) of a
+// matrix with planes of R rows at ((k / 32) * R + m) * 32 + k % 32, i.e. the
+// matrix cut into 32-wide column blocks, each stored as R contiguous 64-byte
+// rows.  A copy of 16 (or 8 twice) consecutive rows of one block is then 1 KB
+// of contiguous memory.  kb32_offset gives the element offset.
+__host__ __device__ inline size_t kb32_offset(size_t R, size_t m, size_t k) { return ((k >> 5) * R + m) * 32 + (k & 31); }
+
+// GEMM: C[M][N] = A[M][K] * W^T.  fp32 mode: A row-major (lda), Wt [N][K]
+// (K contiguous).  bf16 mode: A kb32 with planes of a_rows rows, Wt kb32 with
+// planes of N rows ([K/32][N][32]).
 struct GemmArgs {
-  const void *a; int lda;
+  const void *a; int lda; int a_rows;
   const void *wt;            // [N][K]
   int M, N, K;
   int epi;
   void *out; int ldo;        // kEpiStore / kEpiGelu: activation dtype; kEpiGatedResidual: fp32 h
+  int out_rows;              // bf16 kEpiStore / kEpiGelu: 0 row-major (ldo), else kb32 planes of out_rows rows
   const float *gate; int gate_stride; const int32_t *rowmod;  // gate = gate[rowmod[m]*gate_stride + n]
   // Optional fp32 workspace of part_floats floats.  When a launch would have
   // fewer than kSplitMinTiles tiles (few rows), K is split over up to
@@ -164,6 +178,7 @@ struct AttnArgs {
   int layer;
   const void *qkv; int ldqkv;      // q at column g*hd, k_a at (nq+j)*hd, v_a at (nq+nkv+j)*hd
   void *o; int ldo;                // o at column g*hd
+  int o_rows;                      // bf16: 0 row-major (ldo), else kb32 planes of o_rows rows
   int nq, nkv, hd;
   float *part_o;                   // [slot][kAttnQB][hd] fp32
   float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
@@ -181,12 +196,19 @@ uint16_t f32_to_bf16_rne(float f);
 // Host: upload L stacked [K][N] fp32 matrices as [L][N][K] (K contiguous), in
 // bf16 or fp32; synchronous.
 hipError_t upload_weights_transposed(void *dst, const float *src, int L, int K, int N, bool bf16);
+// Host: the projection weights of the bf16 GEMM: L stacked [K][N] fp32
+// matrices as bf16 kb32 [L][K/32][N][32]; synchronous.
+hipError_t upload_weights_kb32(void *dst, const float *src, int L, int K, int N);
+// The projection weights in the form launch_gemm expects for the mode.
+inline hipError_t upload_gemm_weights(void *dst, const float *src, int L, int K, int N, bool bf16) {
+  return bf16 ? upload_weights_kb32(dst, src, L, K, N) : upload_weights_transposed(dst, src, L, K, N, false);
+}
 // Host: the block lists as item records (an idle block gets an item with
 // nq = 0), each with its `next` link, written to dst.
 void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, const int32_t *next, size_t n,
                       AttnItem *dst);
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
                              const float *part_o, const float *part_ml, void *o, int ldo, int nq,
-                             int nkv, int hd, bool bf16, hipStream_t s);
+                             int nkv, int hd, bool bf16, hipStream_t s, int o_rows = 0);
 
 }  // namespace rosa

@@ -68,7 +68,8 @@ struct rosa_prefill {
   void *wt_ctx = nullptr, *ctx = nullptr;
   float *h = nullptr;
   void *u = nullptr, *qkv = nullptr, *o = nullptr, *g = nullptr;
-  int ldg = 0;                               // row stride of g: d_mlp + 64, off a power of two
+  int ldg = 0;                               // fp32: row stride of g: d_mlp + 64, off a power of two
+  int kb_rows = 0;                           // bf16: u, o, g kb32 with planes of max_tokens rows
   float *zeros = nullptr, *ones = nullptr;   // [d]: zero shift and scale, unit gate
   int32_t *rowmod = nullptr;                 // [max_tokens] zeros
   float *part_o = nullptr, *part_ml = nullptr;
@@ -351,6 +352,7 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     h->qkv = palloc<uint8_t>(h, T * h->qkv_dim * es, e);
     h->o = palloc<uint8_t>(h, T * h->o_dim * es, e);
     h->ldg = h->dff + 64;
+    h->kb_rows = h->bf16 ? (int)T : 0;
     h->g = palloc<uint8_t>(h, T * h->ldg * es, e);
     h->zeros = palloc<float>(h, d, e);
     h->ones = palloc<float>(h, d, e);
@@ -382,10 +384,10 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     }
     if (e != hipSuccess) { rosa_status s2 = pfail(nullptr, ROSA_E_NOMEM, "pinned host allocation failed"); pfree_all(h); delete h; return s2; }
 
-    if (e == hipSuccess) e = upload_weights_transposed(h->wt_qkv, w->w_qkv, h->L, h->d, h->qkv_dim, h->bf16);
-    if (e == hipSuccess) e = upload_weights_transposed(h->wt_o, w->w_o, h->L, h->o_dim, h->d, h->bf16);
-    if (e == hipSuccess) e = upload_weights_transposed(h->wt_up, w->w_up, h->L, h->d, h->dff, h->bf16);
-    if (e == hipSuccess) e = upload_weights_transposed(h->wt_down, w->w_down, h->L, h->dff, h->d, h->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(h->wt_qkv, w->w_qkv, h->L, h->d, h->qkv_dim, h->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(h->wt_o, w->w_o, h->L, h->o_dim, h->d, h->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(h->wt_up, w->w_up, h->L, h->d, h->dff, h->bf16);
+    if (e == hipSuccess) e = upload_gemm_weights(h->wt_down, w->w_down, h->L, h->dff, h->d, h->bf16);
     if (e == hipSuccess && h->context) {
       // [Le][d][2 kv] -> [d][Le * 2 kv], then transposed like every projection
       const size_t kv2 = 2 * (size_t)h->nkv * h->hd;
@@ -393,7 +395,7 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
       for (int l = 0; l < h->head_layers; ++l)
         for (size_t i = 0; i < d; ++i)
           std::memcpy(&cat[i * h->ctx_dim + l * kv2], w->w_ctx + ((size_t)l * d + i) * kv2, kv2 * 4);
-      e = upload_weights_transposed(h->wt_ctx, cat.data(), 1, h->d, h->ctx_dim, h->bf16);
+      e = upload_gemm_weights(h->wt_ctx, cat.data(), 1, h->d, h->ctx_dim, h->bf16);
     }
     if (e == hipSuccess) {
       std::vector<float> one(d, 1.0f);
@@ -440,11 +442,12 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
     e = ptimed(h, pcLoad, [&] { return launch_prefill_load(d_jobs, d_rows, M, h->d, h->bf16, h->h, s); });
     for (int l = 0; l < h->L && e == hipSuccess; ++l) {
       e = ptimed(h, pcNorm, [&] {
-        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s);
+        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s,
+                              h->kb_rows);
       });
       if (e != hipSuccess) break;
       GemmArgs gq{};
-      gq.a = h->u; gq.lda = h->d; gq.wt = (uint8_t *)h->wt_qkv + (size_t)l * h->qkv_dim * h->d * es;
+      gq.a = h->u; gq.lda = h->d; gq.a_rows = h->kb_rows; gq.wt = (uint8_t *)h->wt_qkv + (size_t)l * h->qkv_dim * h->d * es;
       gq.M = M; gq.N = h->qkv_dim; gq.K = h->d; gq.epi = kEpiStore; gq.out = h->qkv; gq.ldo = h->qkv_dim;
       e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gq, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
@@ -460,33 +463,34 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       a.items = d_items; a.n_items = (int)p.items.size();
       a.ordered = d_list; a.n_blocks = p.n_blocks;
       a.reqs = d_reqs; a.layer = 0;
-      a.qkv = h->qkv; a.ldqkv = h->qkv_dim; a.o = h->o; a.ldo = h->o_dim;
+      a.qkv = h->qkv; a.ldqkv = h->qkv_dim; a.o = h->o; a.ldo = h->o_dim; a.o_rows = h->kb_rows;
       a.nq = h->nq; a.nkv = h->nkv; a.hd = h->hd;
       a.part_o = h->part_o; a.part_ml = h->part_ml;
       e = ptimed(h, pcAttention, [&] { return launch_attention(a, h->bf16, s); });
       if (e == hipSuccess && !p.groups.empty())
         e = ptimed(h, pcMerge, [&] {
           return launch_attn_merge(d_groups, (int)p.groups.size(), d_reqs, h->part_o, h->part_ml, h->o, h->o_dim,
-                                   h->nq, h->nkv, h->hd, h->bf16, s);
+                                   h->nq, h->nkv, h->hd, h->bf16, s, h->kb_rows);
         });
       if (e != hipSuccess) break;
       GemmArgs go{};
-      go.a = h->o; go.lda = h->o_dim; go.wt = (uint8_t *)h->wt_o + (size_t)l * h->d * h->o_dim * es;
+      go.a = h->o; go.lda = h->o_dim; go.a_rows = h->kb_rows; go.wt = (uint8_t *)h->wt_o + (size_t)l * h->d * h->o_dim * es;
       go.M = M; go.N = h->d; go.K = h->o_dim; go.epi = kEpiGatedResidual; go.out = h->h; go.ldo = h->d;
       go.gate = h->ones; go.gate_stride = 0; go.rowmod = h->rowmod;
       e = ptimed(h, pcGemmO, [&] { return launch_gemm(go, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
       e = ptimed(h, pcNorm, [&] {
-        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s);
+        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s,
+                              h->kb_rows);
       });
       if (e != hipSuccess) break;
       GemmArgs gu{};
-      gu.a = h->u; gu.lda = h->d; gu.wt = (uint8_t *)h->wt_up + (size_t)l * h->dff * h->d * es;
+      gu.a = h->u; gu.lda = h->d; gu.a_rows = h->kb_rows; gu.out_rows = h->kb_rows; gu.wt = (uint8_t *)h->wt_up + (size_t)l * h->dff * h->d * es;
       gu.M = M; gu.N = h->dff; gu.K = h->d; gu.epi = kEpiGelu; gu.out = h->g; gu.ldo = h->ldg;
       e = ptimed(h, pcGemmUp, [&] { return launch_gemm(gu, h->bf16, s, h->gemm_cfg); });
       if (e != hipSuccess) break;
       GemmArgs gd{};
-      gd.a = h->g; gd.lda = h->ldg; gd.wt = (uint8_t *)h->wt_down + (size_t)l * h->d * h->dff * es;
+      gd.a = h->g; gd.lda = h->ldg; gd.a_rows = h->kb_rows; gd.wt = (uint8_t *)h->wt_down + (size_t)l * h->d * h->dff * es;
       gd.M = M; gd.N = h->d; gd.K = h->dff; gd.epi = kEpiGatedResidual; gd.out = h->h; gd.ldo = h->d;
       gd.gate = h->ones; gd.gate_stride = 0; gd.rowmod = h->rowmod;
       e = ptimed(h, pcGemmDown, [&] { return launch_gemm(gd, h->bf16, s, h->gemm_cfg); });
@@ -495,10 +499,11 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       // Final RMSNorm, one projection for every head layer, then each layer's
       // [K | V] column block into the caches.
       e = ptimed(h, pcNorm, [&] {
-        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s);
+        return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s,
+                              h->kb_rows);
       });
       GemmArgs gc{};
-      gc.a = h->u; gc.lda = h->d; gc.wt = h->wt_ctx;
+      gc.a = h->u; gc.lda = h->d; gc.a_rows = h->kb_rows; gc.wt = h->wt_ctx;
       gc.M = M; gc.N = h->ctx_dim; gc.K = h->d; gc.epi = kEpiStore; gc.out = h->ctx; gc.ldo = h->ctx_dim;
       if (e == hipSuccess) e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gc, h->bf16, s, h->gemm_cfg); });
       const size_t kv2_bytes = 2 * (size_t)h->nkv * h->hd * es;
