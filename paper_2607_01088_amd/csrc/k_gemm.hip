@@ -66,7 +66,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 template <int CPR>
 __device__ __forceinline__ int gswz(int r) { return CPR == 4 ? (r >> 2) & 3 : (r >> 1) & 7; }
 
-template <int MB_, int TN_, int WM_, int WN_, int BK_ = 32>
+template <int MB_, int TN_, int WM_, int WN_, int BK_ = 32, int NST_ = 4>
 struct GemmTile {
   static constexpr int MB = MB_, TN = TN_, WM = WM_, WN = WN_, NW = WM_ * WN_, NT = 64 * NW;
   static constexpr int MBW = MB / WM;                                   // 32-row blocks per wave
@@ -74,8 +74,10 @@ struct GemmTile {
   static constexpr int BK = BK_;                                        // K per stage
   static constexpr int ROWB = BK * 2, CPR = ROWB / 16, RPU = 1024 / ROWB;   // row bytes, chunks per row, rows per 1 KB
   static constexpr int ABYTES = BM * BK * 2, SBYTES = ABYTES + BN * BK * 2;
-  // LDS ring depth (deeper rings measured no faster on these shapes).
-  static constexpr int NST = 4;
+  // LDS ring depth: 4, or 8 for the 64-row tiles of small launches (one
+  // block per CU, latency-bound: more copies in flight per CU).  Deeper rings
+  // measured no faster on the larger tiles.
+  static constexpr int NST = NST_;
   static_assert(NST * SBYTES <= 160 * 1024, "LDS");
   static constexpr int U = (BM + BN) / RPU;                             // 1 KB copies per stage
   static_assert(BK == 32 || BK == 64, "stage K");
@@ -401,7 +403,8 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
 // Block configurations and their measured cost on MI355X (one round of
 // blocks over all CUs, microseconds): a per 1024 of K, plus b by epilogue
 // (store, GELU, gated residual); least-squares fits to the projection shapes
-// of the batch workloads at 1060, 2113, 4241 and 8482 rows.  Past K = 4096 a
+// of the batch workloads at 1060, 2113, 4241 and 8482 rows (the 64-row tiles:
+// at 50, 400, 800 and 1600 rows, where they can win).  Past K = 4096 a
 // round costs a2 more per 1024 of K, from the 16384-deep MLP-down projection
 // of a 26173-row VLM backbone batch (long sustained launches run each tile
 // more slowly, by an amount that differs between tiles).
@@ -418,6 +421,8 @@ static constexpr GemmCfg kCfgs[kGemmConfigs] = {
     {160, 128, 64, 8.1f, 3.4f, {4.5f, 7.1f, 14.7f}},     // 8: 4 waves, 160 x 32 each
     {96, 128, 64, 5.5f, 4.2f, {4.3f, 6.0f, 8.9f}},       // 9: 4 waves, 96 x 32 each
     {256, 64, 64, 6.9f, 7.4f, {4.0f, 4.8f, 8.8f}},       // 10: 8 waves, 64 x 32 each
+    {64, 64, 64, 2.8f, 5.0f, {4.2f, 4.1f, 6.8f}},        // 11: 4 waves, 32 x 32 each, 8 stages
+    {64, 32, 64, 2.3f, 5.0f, {2.5f, 2.3f, 4.9f}},        // 12: 2 waves, 32 x 32 each, 8 stages
 };
 using Cfg0 = GemmTile<12, 2, 4, 2>;
 using Cfg1 = GemmTile<8, 2, 4, 4>;
@@ -430,12 +435,15 @@ using Cfg7 = GemmTile<4, 2, 2, 2, 64>;
 using Cfg8 = GemmTile<5, 1, 1, 4, 64>;
 using Cfg9 = GemmTile<3, 1, 1, 4, 64>;
 using Cfg10 = GemmTile<8, 1, 4, 2, 64>;
+using Cfg11 = GemmTile<2, 1, 2, 2, 64, 8>;
+using Cfg12 = GemmTile<2, 1, 2, 1, 64, 8>;
 template <typename T>
 constexpr bool cfg_matches(const GemmCfg &c) { return T::BM == c.bm && T::BN == c.bn && T::BK == c.bk; }
 static_assert(cfg_matches<Cfg0>(kCfgs[0]) && cfg_matches<Cfg1>(kCfgs[1]) && cfg_matches<Cfg2>(kCfgs[2]) &&
               cfg_matches<Cfg3>(kCfgs[3]) && cfg_matches<Cfg4>(kCfgs[4]) && cfg_matches<Cfg5>(kCfgs[5]) &&
               cfg_matches<Cfg6>(kCfgs[6]) && cfg_matches<Cfg7>(kCfgs[7]) && cfg_matches<Cfg8>(kCfgs[8]) &&
-              cfg_matches<Cfg9>(kCfgs[9]) && cfg_matches<Cfg10>(kCfgs[10]),
+              cfg_matches<Cfg9>(kCfgs[9]) && cfg_matches<Cfg10>(kCfgs[10]) && cfg_matches<Cfg11>(kCfgs[11]) &&
+              cfg_matches<Cfg12>(kCfgs[12]),
               "cost table matches the tiles");
 
 // Sum of the K slices of a split product, in slice order, and the epilogue
@@ -473,6 +481,72 @@ __global__ void __launch_bounds__(256) gemm_split_reduce_kernel(GemmArgs g, int 
   }
 }
 
+// The same sum for a gated-residual product, fused with the modulated
+// RMSNorm of the updated rows (the norm that reads them next): one wave per
+// row sums the KS slices in slice order, applies the gated residual exactly as
+// above, writes the row back to h and normalizes it into u exactly as the norm
+// kernel does, so a split product needs no separate norm launch.
+// N <= kFusedNormMax: each lane holds four 4-column chunks of its row.
+template <int KS>
+__global__ void __launch_bounds__(256) gemm_split_reduce_norm_kernel(GemmArgs g, NormArgs nm) {
+  constexpr int NC = kFusedNormMax / 256;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= g.M) return;
+  const int d = g.N;
+  const size_t slice = (size_t)g.M * g.N;
+  const int mod = g.rowmod[row];
+  const float *gate = g.gate + (size_t)mod * g.gate_stride;
+  const float *mrow = nm.modtab + (size_t)mod * nm.mod_stride;
+  float *hr = reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo;
+  const float *pr = g.part + (size_t)row * g.N;
+  float4 v[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) {
+      f32x4 p[KS];
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2) p[s2] = *reinterpret_cast<const f32x4 *>(pr + s2 * slice + i);
+      const float4 gt = *reinterpret_cast<const float4 *>(gate + i);
+      float4 hv = *reinterpret_cast<const float4 *>(hr + i);
+      f32x4 a = p[0];
+#pragma unroll
+      for (int s2 = 1; s2 < KS; ++s2) { a[0] += p[s2][0]; a[1] += p[s2][1]; a[2] += p[s2][2]; a[3] += p[s2][3]; }
+      hv.x = hv.x + gt.x * a[0];
+      hv.y = hv.y + gt.y * a[1];
+      hv.z = hv.z + gt.z * a[2];
+      hv.w = hv.w + gt.w * a[3];
+      *reinterpret_cast<float4 *>(hr + i) = hv;
+      v[c] = hv;
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)d + nm.eps);
+  bf16 *u = reinterpret_cast<bf16 *>(nm.u);
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int i = c * 256 + lane * 4;
+    if (i < d) {
+      const float4 a = *reinterpret_cast<const float4 *>(mrow + nm.scale_off + i);
+      const float4 b = *reinterpret_cast<const float4 *>(mrow + nm.shift_off + i);
+      bf16x4 o;
+      o[0] = (bf16)(v[c].x * r * (1.0f + a.x) + b.x);
+      o[1] = (bf16)(v[c].y * r * (1.0f + a.y) + b.y);
+      o[2] = (bf16)(v[c].z * r * (1.0f + a.z) + b.z);
+      o[3] = (bf16)(v[c].w * r * (1.0f + a.w) + b.w);
+      const size_t off = nm.u_rows > 0 ? kb32_offset(nm.u_rows, row, i) : (size_t)row * d + i;
+      *reinterpret_cast<bf16x4 *>(u + off) = o;
+    }
+  }
+}
+
 // K slices for a launch of n_tiles tiles of BK-deep stages (1: no split).
 int gemm_split_count(const GemmArgs &g, int n_tiles, int bk) {
   // K = 1024 products are too short for the saving to pay for the second launch.
@@ -483,8 +557,15 @@ int gemm_split_count(const GemmArgs &g, int n_tiles, int bk) {
   return 1;
 }
 
+// Whether a split gated-residual product can take the norm that follows it.
+static bool fusable_norm(const GemmArgs &g, const NormArgs *nm) {
+  return nm && nm->u && g.epi == kEpiGatedResidual && g.N <= kFusedNormMax && g.N % 4 == 0 && g.ldo % 4 == 0 &&
+         (nm->u_rows == 0 || (nm->u_rows >= g.M && g.N % 32 == 0));
+}
+
 template <typename T>
-static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split) {
+static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split, const NormArgs *nm,
+                              bool *normed) {
   const int nrt = (g.M + T::BM - 1) / T::BM, nct = (g.N + T::BN - 1) / T::BN;
   const int ks = allow_split ? gemm_split_count(g, nrt * nct, T::BK) : 1;
   dim3 grid((nrt * nct * ks + 7) / 8 * 8);
@@ -492,6 +573,16 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split
     hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiPartial>), grid, dim3(T::NT), 0, s, g, nrt, nct, ks);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (fusable_norm(g, nm)) {
+      const dim3 ngrid((g.M + 3) / 4);
+      switch (ks) {
+        case 2: hipLaunchKernelGGL(gemm_split_reduce_norm_kernel<2>, ngrid, dim3(256), 0, s, g, *nm); break;
+        case 4: hipLaunchKernelGGL(gemm_split_reduce_norm_kernel<4>, ngrid, dim3(256), 0, s, g, *nm); break;
+        default: hipLaunchKernelGGL(gemm_split_reduce_norm_kernel<kSplitMax>, ngrid, dim3(256), 0, s, g, *nm); break;
+      }
+      if (normed) *normed = true;
+      return hipGetLastError();
+    }
     const int rgrid = (int)std::min<size_t>(((size_t)g.M * g.N / 4 + 255) / 256, 4096);
     switch (g.epi) {
       case kEpiStore: hipLaunchKernelGGL(gemm_split_reduce_kernel<kEpiStore>, dim3(rgrid), dim3(256), 0, s, g, ks); break;
@@ -508,21 +599,24 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split
   return hipGetLastError();
 }
 
-static hipError_t launch_cfg(const GemmArgs &g, int cfg, hipStream_t s, bool allow_split) {
+static hipError_t launch_cfg(const GemmArgs &g, int cfg, hipStream_t s, bool allow_split,
+                             const NormArgs *nm = nullptr, bool *normed = nullptr) {
   if (g.M <= 0) return hipSuccess;
   if (g.K % 128 != 0 || g.N % 8 != 0 || g.a_rows < g.M) return hipErrorInvalidValue;
   switch (cfg) {
-    case 0: return launch_tile<Cfg0>(g, s, allow_split);
-    case 1: return launch_tile<Cfg1>(g, s, allow_split);
-    case 2: return launch_tile<Cfg2>(g, s, allow_split);
-    case 3: return launch_tile<Cfg3>(g, s, allow_split);
-    case 4: return launch_tile<Cfg4>(g, s, allow_split);
-    case 5: return launch_tile<Cfg5>(g, s, allow_split);
-    case 6: return launch_tile<Cfg6>(g, s, allow_split);
-    case 7: return launch_tile<Cfg7>(g, s, allow_split);
-    case 8: return launch_tile<Cfg8>(g, s, allow_split);
-    case 9: return launch_tile<Cfg9>(g, s, allow_split);
-    case 10: return launch_tile<Cfg10>(g, s, allow_split);
+    case 0: return launch_tile<Cfg0>(g, s, allow_split, nm, normed);
+    case 1: return launch_tile<Cfg1>(g, s, allow_split, nm, normed);
+    case 2: return launch_tile<Cfg2>(g, s, allow_split, nm, normed);
+    case 3: return launch_tile<Cfg3>(g, s, allow_split, nm, normed);
+    case 4: return launch_tile<Cfg4>(g, s, allow_split, nm, normed);
+    case 5: return launch_tile<Cfg5>(g, s, allow_split, nm, normed);
+    case 6: return launch_tile<Cfg6>(g, s, allow_split, nm, normed);
+    case 7: return launch_tile<Cfg7>(g, s, allow_split, nm, normed);
+    case 8: return launch_tile<Cfg8>(g, s, allow_split, nm, normed);
+    case 9: return launch_tile<Cfg9>(g, s, allow_split, nm, normed);
+    case 10: return launch_tile<Cfg10>(g, s, allow_split, nm, normed);
+    case 11: return launch_tile<Cfg11>(g, s, allow_split, nm, normed);
+    case 12: return launch_tile<Cfg12>(g, s, allow_split, nm, normed);
     default: return hipErrorInvalidValue;
   }
 }
@@ -614,12 +708,14 @@ static int device_cu_count() {
   return v;
 }
 
-hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int force_cfg) {
+hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int force_cfg, const NormArgs *then_norm,
+                       bool *normed) {
+  if (normed) *normed = false;
   if (g.M <= 0) return hipSuccess;
   if (bf16_mode) {
     const int n_cu = device_cu_count();
     if (force_cfg >= 0) return launch_cfg(g, force_cfg, s, false);
-    return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true);
+    return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true, then_norm, normed);
   }
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   switch (g.epi) {

@@ -1000,12 +1000,18 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
         const int32_t *rowmod = b->rowmod + (size_t)k * p.M0 + r0;
         const int32_t *row_req = b->row_req + r0;
         e = timed(b, kcInProj, [&] { return launch_in_proj(x, M, D.A, b->w_in, b->b_in, D.d, h, st); });
+        const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
+        // u_ready: the norm that reads the rows just updated was fused into
+        // the split product that updated them (small batches only).
+        bool u_ready = false;
         for (int l = 0; l < D.L && e == hipSuccess; ++l) {
           const int base = (int)(l * d6);
-          e = timed(b, kcModNorm, [&] {
-            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16, st,
-                                  R);
-          });
+          if (!u_ready)
+            e = timed(b, kcModNorm, [&] {
+              return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16,
+                                    st, R);
+            });
+          u_ready = false;
           if (e != hipSuccess) break;
           GemmArgs gq{};
           if (nl == 1) { gq.part = b->gemm_part; gq.part_floats = b->gemm_part_floats; }
@@ -1020,12 +1026,15 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           go.a = o; go.lda = D.o_dim; go.a_rows = R; go.wt = (uint8_t *)b->wt_o + (size_t)l * D.d * D.o_dim * es;
           go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = h; go.ldo = D.d;
           go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
-          e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg); });
+          const NormArgs mlp_norm{b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, D.eps, u, R};
+          e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg, &mlp_norm, &u_ready); });
           if (e != hipSuccess) break;
-          e = timed(b, kcModNorm, [&] {
-            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod, u,
-                                  b->bf16, st, R);
-          });
+          if (!u_ready)
+            e = timed(b, kcModNorm, [&] {
+              return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod,
+                                    u, b->bf16, st, R);
+            });
+          u_ready = false;
           if (e != hipSuccess) break;
           GemmArgs gu{};
           if (nl == 1) { gu.part = b->gemm_part; gu.part_floats = b->gemm_part_floats; }
@@ -1038,14 +1047,18 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           gd.a = g; gd.lda = D.dff; gd.a_rows = R; gd.wt = (uint8_t *)b->wt_down + (size_t)l * D.d * D.dff * es;
           gd.M = M; gd.N = D.d; gd.K = D.dff; gd.epi = kEpiGatedResidual; gd.out = h; gd.ldo = D.d;
           gd.gate = b->modtab + base + 5 * D.d; gd.gate_stride = D.mod_stride; gd.rowmod = rowmod;
-          e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, st, b->gemm_cfg); });
+          // The next norm: the next layer's attention norm, or the final norm.
+          const bool last = l + 1 == D.L;
+          const NormArgs next_norm{b->modtab, D.mod_stride, last ? fshift : base + (int)d6,
+                                   last ? fscale : base + (int)d6 + D.d, D.eps, u, R};
+          e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, st, b->gemm_cfg, &next_norm, &u_ready); });
         }
         // Final norm with the final modulation, output projection and Euler step.
-        const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
         if (e == hipSuccess && b->bf16) {
-          e = timed(b, kcFinal, [&] {
-            return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, u, true, st, R);
-          });
+          if (!u_ready)
+            e = timed(b, kcFinal, [&] {
+              return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, fshift, fscale, rowmod, u, true, st, R);
+            });
           if (e == hipSuccess)
             e = timed(b, kcFinal, [&] {
               return launch_out_proj_euler((const __bf16 *)u, M, D.d, (const __bf16 *)b->wt_out, b->b_out, D.A, row_req,

@@ -59,7 +59,7 @@ constexpr int kAttnSplitTarget = 256;
 // Persistent blocks of the bf16 attention kernel per launch: two per compute
 // unit of a 256-CU MI355X.
 constexpr int kAttnBlocks = 512;
-constexpr int kAttnMinSplitKeys = 256;
+constexpr int kAttnMinSplitKeys = 128;
 constexpr int kAttnMaxSlots = 2 * kAttnSplitTarget;
 constexpr int kMaxTau = 128;       // distinct flow times per call
 constexpr int kMaxSteps = 64;
@@ -150,11 +150,25 @@ struct GemmArgs {
 };
 constexpr int kSplitMinTiles = 64;
 constexpr int kSplitMax = 8;
-// force_cfg < 0: block configuration chosen by the cost model.
-hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1);
-// bf16 GEMM with a given block configuration (0: 384x128, 1: 256x256, 2: 128x256,
-// 3: 192x128, 4: 288x128).
-constexpr int kGemmConfigs = 11;
+// The modulated RMSNorm that consumes the rows a gated-residual projection
+// has just updated: u[m] = RMSNorm(h[m]) (1 + scale) + shift, scale and shift
+// at modtab[rowmod[m] * mod_stride + scale_off / shift_off + n] (rowmod: the
+// projection's own).  u is bf16: kb32 planes of u_rows rows, or row-major
+// [M][N] when u_rows = 0.
+struct NormArgs {
+  const float *modtab; int mod_stride; int shift_off; int scale_off; float eps;
+  void *u; int u_rows;
+};
+// force_cfg < 0: block configuration chosen by the cost model.  With
+// then_norm (kEpiGatedResidual, bf16, N <= kFusedNormMax), a product whose K
+// is split has the norm fused into the kernel that sums its slices; *normed
+// tells the caller whether that happened (else it launches the norm itself).
+constexpr int kFusedNormMax = 1024;
+hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1,
+                       const NormArgs *then_norm = nullptr, bool *normed = nullptr);
+// bf16 GEMM with a given block configuration (an index into the launcher's
+// table of kGemmConfigs tiles, from 384 x 128 down to 64 x 32).
+constexpr int kGemmConfigs = 13;
 hipError_t launch_gemm_cfg(const GemmArgs &g, int cfg, hipStream_t s);
 int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 
