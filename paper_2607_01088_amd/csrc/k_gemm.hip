@@ -482,78 +482,68 @@ __global__ void __launch_bounds__(256) gemm_split_reduce_kernel(GemmArgs g, int 
 }
 
 // The same sum for a gated-residual product, fused with the modulated
-// RMSNorm of the updated rows (the norm that reads them next): one wave per
-// row sums the KS slices in slice order, applies the gated residual exactly as
-// above, writes the row back to h and normalizes it into u exactly as the norm
-// kernel does, so a split product needs no separate norm launch.
-// N <= kFusedNormMax: each lane holds four 4-column chunks of its row.
+// RMSNorm of the updated rows (the norm that reads them next).  One block per
+// row, four columns per thread (N <= kFusedNormMax): sum the KS slices in
+// slice order, apply the gated residual exactly as above, write the row back
+// to h, and normalize it into u (row sum of squares: per wave, then the four
+// wave sums in wave order), so a split product needs no separate norm launch.
 template <int KS>
 __global__ void __launch_bounds__(256) gemm_split_reduce_norm_kernel(GemmArgs g, NormArgs nm) {
-  constexpr int NC = kFusedNormMax / 256;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= g.M) return;
+  static_assert(kFusedNormMax == 4 * 256, "four columns per thread");
+  __shared__ float wsum[4];
+  const int row = blockIdx.x, i = threadIdx.x * 4;
   const int d = g.N;
   const size_t slice = (size_t)g.M * g.N;
   const int mod = g.rowmod[row];
-  const float *gate = g.gate + (size_t)mod * g.gate_stride;
-  const float *mrow = nm.modtab + (size_t)mod * nm.mod_stride;
   float *hr = reinterpret_cast<float *>(g.out) + (size_t)row * g.ldo;
-  const float *pr = g.part + (size_t)row * g.N;
-  float4 v[NC];
+  float4 hv = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < d) {
+    const float *pr = g.part + (size_t)row * g.N + i;
+    f32x4 p[KS];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int i = c * 256 + lane * 4;
-    if (i < d) {
-      f32x4 p[KS];
+    for (int s2 = 0; s2 < KS; ++s2) p[s2] = *reinterpret_cast<const f32x4 *>(pr + s2 * slice);
+    const float4 gt = *reinterpret_cast<const float4 *>(g.gate + (size_t)mod * g.gate_stride + i);
+    hv = *reinterpret_cast<const float4 *>(hr + i);
+    f32x4 a = p[0];
 #pragma unroll
-      for (int s2 = 0; s2 < KS; ++s2) p[s2] = *reinterpret_cast<const f32x4 *>(pr + s2 * slice + i);
-      const float4 gt = *reinterpret_cast<const float4 *>(gate + i);
-      float4 hv = *reinterpret_cast<const float4 *>(hr + i);
-      f32x4 a = p[0];
-#pragma unroll
-      for (int s2 = 1; s2 < KS; ++s2) { a[0] += p[s2][0]; a[1] += p[s2][1]; a[2] += p[s2][2]; a[3] += p[s2][3]; }
-      hv.x = hv.x + gt.x * a[0];
-      hv.y = hv.y + gt.y * a[1];
-      hv.z = hv.z + gt.z * a[2];
-      hv.w = hv.w + gt.w * a[3];
-      *reinterpret_cast<float4 *>(hr + i) = hv;
-      v[c] = hv;
-    }
+    for (int s2 = 1; s2 < KS; ++s2) { a[0] += p[s2][0]; a[1] += p[s2][1]; a[2] += p[s2][2]; a[3] += p[s2][3]; }
+    hv.x = hv.x + gt.x * a[0];
+    hv.y = hv.y + gt.y * a[1];
+    hv.z = hv.z + gt.z * a[2];
+    hv.w = hv.w + gt.w * a[3];
+    *reinterpret_cast<float4 *>(hr + i) = hv;
   }
-  float ss = 0.f;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int i = c * 256 + lane * 4;
-    if (i < d) ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
-  }
-  ss = wave_sum(ss);
-  const float r = 1.0f / sqrtf(ss / (float)d + nm.eps);
-  bf16 *u = reinterpret_cast<bf16 *>(nm.u);
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int i = c * 256 + lane * 4;
-    if (i < d) {
-      const float4 a = *reinterpret_cast<const float4 *>(mrow + nm.scale_off + i);
-      const float4 b = *reinterpret_cast<const float4 *>(mrow + nm.shift_off + i);
-      bf16x4 o;
-      o[0] = (bf16)(v[c].x * r * (1.0f + a.x) + b.x);
-      o[1] = (bf16)(v[c].y * r * (1.0f + a.y) + b.y);
-      o[2] = (bf16)(v[c].z * r * (1.0f + a.z) + b.z);
-      o[3] = (bf16)(v[c].w * r * (1.0f + a.w) + b.w);
-      const size_t off = nm.u_rows > 0 ? kb32_offset(nm.u_rows, row, i) : (size_t)row * d + i;
-      *reinterpret_cast<bf16x4 *>(u + off) = o;
-    }
+  const float ss = wave_sum(hv.x * hv.x + hv.y * hv.y + hv.z * hv.z + hv.w * hv.w);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float r = 1.0f / sqrtf((((wsum[0] + wsum[1]) + wsum[2]) + wsum[3]) / (float)d + nm.eps);
+  if (i < d) {
+    const float *mrow = nm.modtab + (size_t)mod * nm.mod_stride;
+    const float4 a = *reinterpret_cast<const float4 *>(mrow + nm.scale_off + i);
+    const float4 b = *reinterpret_cast<const float4 *>(mrow + nm.shift_off + i);
+    bf16x4 o;
+    o[0] = (bf16)(hv.x * r * (1.0f + a.x) + b.x);
+    o[1] = (bf16)(hv.y * r * (1.0f + a.y) + b.y);
+    o[2] = (bf16)(hv.z * r * (1.0f + a.z) + b.z);
+    o[3] = (bf16)(hv.w * r * (1.0f + a.w) + b.w);
+    const size_t off = nm.u_rows > 0 ? kb32_offset(nm.u_rows, row, i) : (size_t)row * d + i;
+    *reinterpret_cast<bf16x4 *>(reinterpret_cast<bf16 *>(nm.u) + off) = o;
   }
 }
 
 // K slices for a launch of n_tiles tiles of BK-deep stages (1: no split).
-int gemm_split_count(const GemmArgs &g, int n_tiles, int bk) {
+// A product whose slice reduction also takes the norm that follows it
+// (fused) costs no extra launch, so it splits up to a whole round of blocks
+// (kSplitMinTilesNorm tiles); others only below kSplitMinTiles.
+int gemm_split_count(const GemmArgs &g, int n_tiles, int bk, bool fused) {
   // K = 1024 products are too short for the saving to pay for the second launch.
-  if (!g.part || n_tiles >= kSplitMinTiles || g.K < 2048 || g.N % 4 || g.ldo % 4) return 1;
+  if (!g.part || n_tiles >= (fused ? kSplitMinTilesNorm : kSplitMinTiles) || g.K < 2048 || g.N % 4 || g.ldo % 4)
+    return 1;
   const int nk = g.K / bk;
+  const int most_blocks = fused ? std::max(256, 2 * kSplitMinTilesNorm) : 256;
   for (int ks = kSplitMax; ks >= 2; ks /= 2)
-    if (n_tiles * ks <= 256 && nk % ks == 0 && nk / ks >= 4 && (size_t)ks * g.M * g.N <= g.part_floats) return ks;
+    if (n_tiles * ks <= most_blocks && nk % ks == 0 && nk / ks >= 4 && (size_t)ks * g.M * g.N <= g.part_floats)
+      return ks;
   return 1;
 }
 
@@ -567,14 +557,14 @@ template <typename T>
 static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split, const NormArgs *nm,
                               bool *normed) {
   const int nrt = (g.M + T::BM - 1) / T::BM, nct = (g.N + T::BN - 1) / T::BN;
-  const int ks = allow_split ? gemm_split_count(g, nrt * nct, T::BK) : 1;
+  const int ks = allow_split ? gemm_split_count(g, nrt * nct, T::BK, fusable_norm(g, nm)) : 1;
   dim3 grid((nrt * nct * ks + 7) / 8 * 8);
   if (ks > 1) {
     hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiPartial>), grid, dim3(T::NT), 0, s, g, nrt, nct, ks);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (fusable_norm(g, nm)) {
-      const dim3 ngrid((g.M + 3) / 4);
+      const dim3 ngrid(g.M);
       switch (ks) {
         case 2: hipLaunchKernelGGL(gemm_split_reduce_norm_kernel<2>, ngrid, dim3(256), 0, s, g, *nm); break;
         case 4: hipLaunchKernelGGL(gemm_split_reduce_norm_kernel<4>, ngrid, dim3(256), 0, s, g, *nm); break;

@@ -149,6 +149,7 @@ struct GemmArgs {
   float *part; size_t part_floats;
 };
 constexpr int kSplitMinTiles = 64;
+constexpr int kSplitMinTilesNorm = 128;
 constexpr int kSplitMax = 8;
 // The modulated RMSNorm that consumes the rows a gated-residual projection
 // has just updated: u[m] = RMSNorm(h[m]) (1 + scale) + shift, scale and shift
