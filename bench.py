@@ -183,7 +183,8 @@ def _classify_dispatches(rows):
     """Dispatch id -> kernel role for a one-lane bf16 generate run.  Per layer
     the expert launches modnorm, the QKV projection, attention (and, for split
     keys, the merge), the output projection, modnorm, MLP up, MLP down; a split
-    product's reduce kernel belongs to the projection before it."""
+    product's reduce kernel belongs to the projection before it, and when that
+    reduce also takes the following norm, no modnorm launch follows."""
     names = {}
     for r in rows:
         names[int(r["Dispatch_Id"])] = r["Kernel_Name"]
@@ -201,6 +202,10 @@ def _classify_dispatches(rows):
                 cur = "gemm_down"
             elif prev == "modnorm":
                 cur = "gemm_up" if last_gemm == "gemm_o" else "gemm_qkv"
+            elif prev == "gemm_o":
+                cur = "gemm_up"
+            elif prev == "gemm_down":
+                cur = "gemm_qkv"
             else:
                 cur = "other"
             last_gemm = cur

@@ -1,0 +1,32 @@
+"""Host-side logic of bench.py's profile summaries (CPU only)."""
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+import bench  # noqa: E402
+
+
+def _rows(names):
+    return [{"Dispatch_Id": str(i), "Kernel_Name": n} for i, n in enumerate(names)]
+
+
+def test_classify_dispatches_plain_layer():
+    seq = ["modnorm_kernel", "gemm_bf16_kernel<A,0>", "attention_bf16_kernel", "gemm_bf16_kernel<B,2>",
+           "modnorm_kernel", "gemm_bf16_kernel<C,1>", "gemm_bf16_kernel<D,2>",
+           "modnorm_kernel", "gemm_bf16_kernel<A,0>"]
+    role = bench._classify_dispatches(_rows(seq))
+    assert [role[i] for i in range(len(seq))] == ["modnorm", "gemm_qkv", "attention", "gemm_o", "modnorm",
+                                                  "gemm_up", "gemm_down", "modnorm", "gemm_qkv"]
+
+
+def test_classify_dispatches_split_products_with_fused_norms():
+    # Small batch: split keys (merge), split output and MLP-down products
+    # whose slice reductions also take the following norm (no modnorm launch).
+    seq = ["modnorm_kernel", "gemm_bf16_kernel<A,0>", "attention_bf16_kernel", "attn_merge_kernel",
+           "gemm_bf16_kernel<B,3>", "gemm_split_reduce_norm_kernel<8>", "gemm_bf16_kernel<C,1>",
+           "gemm_bf16_kernel<D,3>", "gemm_split_reduce_norm_kernel<8>", "gemm_bf16_kernel<A,0>",
+           "attention_bf16_kernel"]
+    role = bench._classify_dispatches(_rows(seq))
+    assert [role[i] for i in range(len(seq))] == ["modnorm", "gemm_qkv", "attention", "attn_merge", "gemm_o",
+                                                  "gemm_o", "gemm_up", "gemm_down", "gemm_down", "gemm_qkv",
+                                                  "attention"]
