@@ -372,6 +372,49 @@ def _summarize_presets(out):
     open(os.path.join(PROFILES, "bench_workloads.md"), "w").write("\n".join(lines) + "\n")
 
 
+def _summarize_b1_trace(out):
+    """Per-kernel durations and launch gaps of one single-robot call from a
+    --kernel-trace run of `bench.py --workload pi0_b1` (tr_b1/)."""
+    import collections
+    rows = _csv_rows(f"{out}/tr_b1/**/*kernel_trace.csv")
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    starts = [i for i, r in enumerate(rows) if "time_embedding" in r["Kernel_Name"]]
+    if len(starts) < 4:
+        raise SystemExit("tr_b1: fewer than 4 generate calls in the trace")
+    call = rows[starts[2]:starts[3]]              # the first timed call (after 1 warm-up)
+    span = (int(call[-1]["End_Timestamp"]) - int(call[0]["Start_Timestamp"])) / 1e3
+    dur = collections.defaultdict(list)
+    gap = collections.defaultdict(list)
+    prev_end = None
+    for r in call:
+        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        t0, t1 = int(r["Start_Timestamp"]), int(r["End_Timestamp"])
+        dur[name].append((t1 - t0) / 1e3)
+        if prev_end is not None:
+            gap[name].append((t0 - prev_end) / 1e3)
+        prev_end = t1
+    busy = sum(sum(v) for v in dur.values())
+    lines = ["# Kernel trace of one single-robot call: pi0_b1 workload (1 request, prefix 816, horizon 50, "
+             "10 Euler steps, bf16)", "",
+             "Command (one MI355X, repository root, library built in-tree):", "", "```",
+             f"export TMPDIR=/tmp; rocprofv3 --kernel-trace --output-format csv -d {out}/tr_b1 -o b1 -- "
+             "python -u bench.py --workload pi0_b1 --steps 3 --warmup 1 --no-cpu-baseline",
+             f"python bench.py --summarize-profiles {out}", "```", "",
+             f"The first timed call: {len(call)} kernels, {busy / 1e3:.2f} ms of kernel time, {span / 1e3:.2f} ms "
+             "from its first kernel's start to its last kernel's end under the tracer (the untraced call takes "
+             "about the kernel time: the tracer widens the gaps between dependent launches).  Per layer-step "
+             "(18 layers x 10 steps) the call launches QKV, attention, the merge of split key ranges, the output "
+             "projection's K slices, their reduction fused with the MLP norm, MLP up, MLP down's K slices and "
+             "their reduction fused with the next norm.", "",
+             "| Kernel | Launches | Avg (us) | Min (us) | Total (ms) | Avg gap before (us) |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for name, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        g = gap.get(name, [])
+        lines.append(f"| `{name}` | {len(v)} | {sum(v) / len(v):.2f} | {min(v):.2f} | {sum(v) / 1e3:.3f} | "
+                     f"{(sum(g) / len(g)) if g else 0.0:.2f} |")
+    open(os.path.join(PROFILES, "kernel_trace_pi0_b1.md"), "w").write("\n".join(lines) + "\n")
+
+
 def summarize_profiles(out):
     """Turn rocprofv3 outputs of this script into the summaries under
     profiles/ (kernel-time table, calibrated HBM traffic of the attention
@@ -384,6 +427,8 @@ def summarize_profiles(out):
         _summarize_prefill(out)
     if glob.glob(f"{out}/pmc_util/**/*counter_collection.csv", recursive=True):
         _summarize_pmc(out)
+    if glob.glob(f"{out}/tr_b1/**/*kernel_trace.csv", recursive=True):
+        _summarize_b1_trace(out)
     _summarize_presets(out)
     if not glob.glob(f"{out}/prof_factory/**/*kernel_stats.csv", recursive=True):
         return
