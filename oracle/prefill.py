@@ -10,9 +10,12 @@ it is used):
 
 * input: the prefix tokens already embedded (image patches and text), [P][d];
 * each layer: RMSNorm (eps 1e-6, no learned gain), fused QKV projection,
-  attention of every prefix token over all prefix tokens of its own request
-  (bidirectional, no positions), output projection and residual; RMSNorm, a
-  plain two-matrix tanh-GELU MLP and residual; no biases;
+  attention of every prefix token over the prefix tokens of its own request
+  (no positions): all of them (bidirectional), or, when the job ends in a
+  causal segment of c tokens, token t over tokens [0, max(P - c, t + 1)) (a
+  prefix-LM mask: image patches and prompt see each other, the segment's
+  tokens see those and the segment up to themselves), output projection and
+  residual; RMSNorm, a plain two-matrix tanh-GELU MLP and residual; no biases;
 * the layer's cache: its K and V projections of the prefix tokens,
   [L][P][n_kv][hd].
 
@@ -26,10 +29,14 @@ every backbone layer, RMS-normalises the final hidden state and projects it
 with each head layer's own context weights into that layer's K and V.
 
 Pins (tests marked ``not gpu``): a scalar brute force on nested lists for a
-tiny backbone (both cache forms); with the residual branches zeroed every
-layer's cache is the closed form RMSNorm(x) W_k, W_v of that layer (context
-form: RMSNorm(x) W_ctx[e]); permuting the prefix tokens permutes the cache
-rows (no causal mask, no positions).
+tiny backbone (both cache forms, with and without a causal segment); with the
+residual branches zeroed every layer's cache is the closed form RMSNorm(x)
+W_k, W_v of that layer (context form: RMSNorm(x) W_ctx[e]); permuting the
+prefix tokens permutes the cache rows (no causal segment, no positions).
+With a causal segment: a token's caches do not change when the tokens it
+cannot see are changed or dropped (the job cut after it, or, for the
+bidirectional part, the segment removed), and a fully causal job's first
+token has the caches of that token alone.
 """
 from __future__ import annotations
 
@@ -37,14 +44,37 @@ from typing import Dict, Tuple
 
 import numpy as np
 
-from .rosa_oracle import attention, gelu_tanh, rms_norm
+from .rosa_oracle import attention, gelu_tanh, rms_norm, softmax_rows
 
 F = np.float64
 
 
-def prefill(x: np.ndarray, w: Dict[str, np.ndarray], shape) -> Tuple[np.ndarray, np.ndarray]:
+def prefix_lm_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, causal_len: int) -> np.ndarray:
+    """Grouped-query attention of one job's tokens over each other when its
+    last causal_len tokens form a causal segment: token t sees tokens
+    [0, max(P - causal_len, t + 1)).  causal_len = 0 is plain bidirectional
+    attention."""
+    if causal_len == 0:
+        return attention(q, k, v)
+    P, n_q, hd = q.shape
+    n_kv = k.shape[1]
+    group = n_q // n_kv
+    b = P - causal_len
+    t = np.arange(P)
+    visible = t[None, :] < np.maximum(b, t + 1)[:, None]          # [query token][key token]
+    o = np.empty_like(q)
+    for g in range(n_q):
+        j = g // group
+        s = q[:, g, :] @ k[:, j, :].T / np.sqrt(hd)
+        o[:, g, :] = softmax_rows(np.where(visible, s, -np.inf)) @ v[:, j, :]
+    return o
+
+
+def prefill(x: np.ndarray, w: Dict[str, np.ndarray], shape, causal_len: int = 0
+            ) -> Tuple[np.ndarray, np.ndarray]:
     """Prefix caches (K, V), each [L][P][n_kv][hd] float64, of one request whose
-    embedded prefix tokens are x [P][d]."""
+    embedded prefix tokens are x [P][d] (the last causal_len of them a causal
+    segment)."""
     L, nq, nkv, hd, eps = shape.n_layers, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.rms_eps
     P = x.shape[0]
     h = np.asarray(x, dtype=F).copy()
@@ -56,14 +86,14 @@ def prefill(x: np.ndarray, w: Dict[str, np.ndarray], shape) -> Tuple[np.ndarray,
         k = qkv[:, nq * hd:(nq + nkv) * hd].reshape(P, nkv, hd)
         v = qkv[:, (nq + nkv) * hd:].reshape(P, nkv, hd)
         K[l], V[l] = k, v
-        o = attention(q, k, v) if P > 0 else np.zeros((0, nq, hd), dtype=F)
+        o = prefix_lm_attention(q, k, v, causal_len) if P > 0 else np.zeros((0, nq, hd), dtype=F)
         h = h + o.reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
         u = rms_norm(h, eps)
         h = h + gelu_tanh(u @ np.asarray(w["w_up"][l], dtype=F)) @ np.asarray(w["w_down"][l], dtype=F)
     return K, V
 
 
-def prefill_context(x: np.ndarray, w: Dict[str, np.ndarray], shape, w_ctx: np.ndarray
+def prefill_context(x: np.ndarray, w: Dict[str, np.ndarray], shape, w_ctx: np.ndarray, causal_len: int = 0
                     ) -> Tuple[np.ndarray, np.ndarray]:
     """Context caches (K, V), each [L_e][P][n_kv][hd] float64, for an action
     head that cross-attends to the backbone's output (the GR00T-style head):
@@ -78,7 +108,7 @@ def prefill_context(x: np.ndarray, w: Dict[str, np.ndarray], shape, w_ctx: np.nd
         q = qkv[:, :nq * hd].reshape(P, nq, hd)
         k = qkv[:, nq * hd:(nq + nkv) * hd].reshape(P, nkv, hd)
         v = qkv[:, (nq + nkv) * hd:].reshape(P, nkv, hd)
-        h = h + attention(q, k, v).reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
+        h = h + prefix_lm_attention(q, k, v, causal_len).reshape(P, nq * hd) @ np.asarray(w["w_o"][l], dtype=F)
         h = h + gelu_tanh(rms_norm(h, eps) @ np.asarray(w["w_up"][l], dtype=F)) @ np.asarray(w["w_down"][l], dtype=F)
     u = rms_norm(h, eps)
     Le = w_ctx.shape[0]

@@ -10,8 +10,10 @@ from synthetic import TINY_VLM, VlmShape, make_context_weights, make_prefix_embe
 SMALL = VlmShape(n_layers=2, d_model=8, n_q_heads=4, n_kv_heads=2, head_dim=4, d_mlp=12)
 
 
-def _brute_prefill(x, w, s):
-    """Scalar brute force on nested Python lists."""
+def _brute_prefill(x, w, s, causal_len=0):
+    """Scalar brute force on nested Python lists.  With a causal segment of the
+    last causal_len tokens, key u is visible to token t when u lies before the
+    segment or u <= t."""
     L, d, nq, nkv, hd, dff = s.n_layers, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_mlp
     G = nq // nkv
     P = len(x)
@@ -37,11 +39,12 @@ def _brute_prefill(x, w, s):
             row = []
             for g in range(nq):
                 j = g // G
-                sc = [sum(q[t][g][e] * k[u][j][e] for e in range(hd)) / math.sqrt(hd) for u in range(P)]
+                keys = [u for u in range(P) if u < P - causal_len or u <= t]
+                sc = [sum(q[t][g][e] * k[u][j][e] for e in range(hd)) / math.sqrt(hd) for u in keys]
                 m = max(sc)
                 ex = [math.exp(z - m) for z in sc]
                 tot = sum(ex)
-                row += [sum(ex[u] * v[u][j][e] for u in range(P)) / tot for e in range(hd)]
+                row += [sum(ex[i] * v[u][j][e] for i, u in enumerate(keys)) / tot for e in range(hd)]
             o.append(row)
         h = [[a + b for a, b in zip(hr, matvec(orow, w["w_o"][l]))] for hr, orow in zip(h, o)]
         new = []
@@ -123,3 +126,66 @@ def test_context_form_zero_residual_closed_form_and_permutation():
     Kp, Vp = prefill_context(x[perm], w, TINY_VLM, wc)
     np.testing.assert_allclose(Kp, K1[:, perm], rtol=1e-12, atol=1e-13)
     np.testing.assert_allclose(Vp, V1[:, perm], rtol=1e-12, atol=1e-13)
+
+
+def test_causal_segment_matches_scalar_bruteforce():
+    rng = np.random.default_rng(2)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL, "fp32").items()}
+    x = rng.standard_normal((5, SMALL.d_model))
+    for c in (1, 3, 5):
+        K, V = prefill(x, w, SMALL, causal_len=c)
+        Kb, Vb, _ = _brute_prefill(x, w, SMALL, causal_len=c)
+        np.testing.assert_allclose(K, Kb, rtol=0, atol=1e-11)
+        np.testing.assert_allclose(V, Vb, rtol=0, atol=1e-11)
+
+
+def test_causal_caches_ignore_the_tokens_they_cannot_see():
+    # P = 12 with a causal segment of 5: tokens 0..6 see each other only, token
+    # t >= 7 sees tokens 0..t.  Cutting the job after token t (t >= 7) keeps
+    # tokens 0..t's caches; dropping the segment keeps tokens 0..6's; changing
+    # the last token changes no other token's caches.
+    w = make_vlm_weights(TINY_VLM, "fp32", seed=11)
+    x = make_prefix_embeddings(TINY_VLM, 12, "fp32", seed=12).astype(np.float64)
+    K, V = prefill(x, w, TINY_VLM, causal_len=5)
+    for t in range(7, 12):
+        Kt, Vt = prefill(x[:t + 1], w, TINY_VLM, causal_len=t + 1 - 7)
+        np.testing.assert_allclose(Kt, K[:, :t + 1], rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(Vt, V[:, :t + 1], rtol=1e-12, atol=1e-13)
+    Kb, Vb = prefill(x[:7], w, TINY_VLM)
+    np.testing.assert_allclose(Kb, K[:, :7], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(Vb, V[:, :7], rtol=1e-12, atol=1e-13)
+    x2 = x.copy()
+    x2[11] = -x2[11]
+    K2, V2 = prefill(x2, w, TINY_VLM, causal_len=5)
+    np.testing.assert_allclose(K2[:, :11], K[:, :11], rtol=1e-12, atol=1e-13)
+    assert np.abs(K2[1:, 11] - K[1:, 11]).max() > 1e-3     # the changed token itself does change
+    # Without the segment every token sees the last one.
+    Kf, _ = prefill(x, w, TINY_VLM)
+    Kf2, _ = prefill(x2, w, TINY_VLM)
+    assert np.abs(Kf2[1:, 0] - Kf[1:, 0]).max() > 1e-6
+
+
+def test_fully_causal_first_token_is_alone():
+    w = make_vlm_weights(TINY_VLM, "fp32", seed=13)
+    x = make_prefix_embeddings(TINY_VLM, 6, "fp32", seed=14).astype(np.float64)
+    K, V = prefill(x, w, TINY_VLM, causal_len=6)
+    K1, V1 = prefill(x[:1], w, TINY_VLM)
+    np.testing.assert_allclose(K[:, :1], K1, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(V[:, :1], V1, rtol=1e-12, atol=1e-13)
+
+
+def test_context_form_causal_matches_scalar_bruteforce():
+    rng = np.random.default_rng(3)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL, "fp32").items()}
+    wc = rng.standard_normal((2, SMALL.d_model, 2 * SMALL.n_kv_heads * SMALL.head_dim)) * 0.5
+    x = rng.standard_normal((5, SMALL.d_model))
+    K, V = prefill_context(x, w, SMALL, wc, causal_len=2)
+    _, _, h = _brute_prefill(x, w, SMALL, causal_len=2)
+    kvw = SMALL.n_kv_heads * SMALL.head_dim
+    for e in range(2):
+        for t in range(5):
+            ms = sum(z * z for z in h[t]) / len(h[t])
+            u = [z / math.sqrt(ms + SMALL.rms_eps) for z in h[t]]
+            kv = [sum(u[i] * wc[e][i][j] for i in range(len(u))) for j in range(2 * kvw)]
+            np.testing.assert_allclose(K[e, t].reshape(-1), kv[:kvw], rtol=0, atol=1e-11)
+            np.testing.assert_allclose(V[e, t].reshape(-1), kv[kvw:], rtol=0, atol=1e-11)
