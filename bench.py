@@ -699,13 +699,22 @@ def step_batching(torch, rosa, expert, db, reqs, preset, args, n_req=1024, seed=
                       "clock": "virtual: advanced by each call's measured duration"}), flush=True)
 
 
-def prefill_work(shape, lens, head_layers: int = 0):
+def visible_keys(P: int, c: int) -> float:
+    """Sum over a job's tokens of the keys each sees: P^2 when bidirectional;
+    with a causal segment of the last c tokens, b^2 + (b+1) + ... + P for
+    b = P - c."""
+    b = P - c
+    return float(b) * b + (float(P) * (P + 1) - float(b) * (b + 1)) / 2.0
+
+
+def prefill_work(shape, lens, head_layers: int = 0, causal=None):
     """Algorithmic flops of one prefix-producer call by kernel class.  Per-layer
     form: every layer's QKV projection; the attention, output projection and
     MLP of all layers but the last (its caches need only its K and V).
     Context form (head_layers > 0): every layer in full, plus the context
     projection for every head layer (counted with the QKV class, the same
-    kernel class).  Attention: 4 * n_q * hd * P^2 per job and layer."""
+    kernel class).  Attention: 4 * n_q * hd * (visible keys summed over the
+    job's tokens: P^2 without a causal segment) per job and layer."""
     L, d, nq, nkv, hd, dff = (shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
                               shape.d_mlp)
     M = float(sum(lens))
@@ -715,11 +724,11 @@ def prefill_work(shape, lens, head_layers: int = 0):
         "gemm_o": 2.0 * M * nq * hd * d * Lb,
         "gemm_up": 2.0 * M * d * dff * Lb,
         "gemm_down": 2.0 * M * dff * d * Lb,
-        "attention": 4.0 * nq * hd * sum(float(P) * P for P in lens) * Lb,
+        "attention": 4.0 * nq * hd * sum(visible_keys(P, c) for P, c in zip(lens, causal or [0] * len(lens))) * Lb,
     }
 
 
-def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float, wctx=None):
+def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float, wctx=None, causal=None):
     """The oracle backbone on a bounded sample: whole jobs of the batch, in
     order, until budget_s seconds have been spent; scaled to the whole batch by
     algorithmic flops (the oracle's cost is additive over jobs)."""
@@ -733,19 +742,22 @@ def prefill_cpu_baseline(shape, weights, xs, lens, budget_s: float, wctx=None):
     per_tok = 2.0 * (shape.d_model * shape.qkv_dim + shape.n_q_heads * shape.head_dim * shape.d_model
                      + 2 * shape.d_model * shape.d_mlp)
     ctx_tok = 0.0 if wctx is None else 2.0 * shape.d_model * wctx.shape[0] * wctx.shape[2]
-    flops = lambda P: shape.n_layers * (per_tok * P + 4.0 * shape.n_q_heads * shape.head_dim * float(P) * P) + ctx_tok * P
+    causal = causal or [0] * len(lens)
+    flops = lambda P, c: (shape.n_layers * (per_tok * P + 4.0 * shape.n_q_heads * shape.head_dim * visible_keys(P, c))
+                          + ctx_tok * P)
     t_used, done = 0.0, 0
-    for x in xs:
+    for x, c in zip(xs, causal):
         t0 = time.perf_counter()
         if wctx is None:
-            prefill(x, weights, shape)
+            prefill(x, weights, shape, causal_len=c)
         else:
-            prefill_context(x, weights, shape, wctx)
+            prefill_context(x, weights, shape, wctx, causal_len=c)
         t_used += time.perf_counter() - t0
         done += 1
         if t_used >= budget_s:
             break
-    batch_s = t_used * sum(flops(P) for P in lens) / sum(flops(P) for P in lens[:done])
+    batch_s = t_used * (sum(flops(P, c) for P, c in zip(lens, causal))
+                        / sum(flops(P, c) for P, c in zip(lens[:done], causal[:done])))
     return {"value": sum(lens) / batch_s, "unit": "prefix tokens/s", "cores": int(blas_threads),
             "host_cores_available": len(os.sched_getaffinity(0)), "kind": "oracle",
             "sample": (f"{done} of {len(lens)} jobs ({sum(lens[:done])} tokens, all {shape.n_layers} layers), "
@@ -772,7 +784,8 @@ def prefill_bench(torch, rosa, args):
     kc = [torch.empty((cache_layers, P, shape.n_kv_heads, shape.head_dim), dtype=torch.bfloat16,
                       device="cuda") for P in lens]
     vc = [torch.empty_like(k) for k in kc]
-    jobs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(emb, kc, vc, lens)]
+    causal = [min(args.prefill_causal, P) for P in lens]
+    jobs = [rosa.prefix_job(e, k, v, P, c) for e, k, v, P, c in zip(emb, kc, vc, lens, causal)]
     pp = rosa.PrefixProducer(shape, "bf16", weights, len(lens), sum(lens), context_weights=wctx)
     stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
@@ -795,7 +808,7 @@ def prefill_bench(torch, rosa, args):
         pp.run(jobs)
     prof = pp.profile()
     pp.set_profiling(False)
-    work = prefill_work(shape, lens, head_layers if context else 0)
+    work = prefill_work(shape, lens, head_layers if context else 0, causal)
     kernels = {}
     for name, (launches, ms) in prof.items():
         if launches == 0:
@@ -820,8 +833,10 @@ def prefill_bench(torch, rosa, args):
         "ms_per_step": round(ms_per_step, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": "vlm_prefill_b32" + ("_context" if context else ""), "jobs": len(lens),
+        "config": {"workload": "vlm_prefill_b32" + ("_context" if context else "")
+                   + (f"_causal{args.prefill_causal}" if args.prefill_causal else ""), "jobs": len(lens),
                    "prefix_tokens": int(sum(lens)), "cache_form": args.prefill_cache,
+                   "causal_segment_tokens": args.prefill_causal,
                    "backbone": "18 layers, width 2048, 8 query heads / 1 KV head of 256, MLP 16384"},
         "jobs_per_s": round(len(lens) * args.steps / elapsed, 2),
         "p50_ms": round(float(np.percentile(lat, 50)), 3),
@@ -835,7 +850,7 @@ def prefill_bench(torch, rosa, args):
     }
     pp.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs, lens, args.cpu_budget, wctx)
+        out["cpu_baseline"] = prefill_cpu_baseline(shape, weights, xs, lens, args.cpu_budget, wctx, causal)
     print(json.dumps(out), flush=True)
 
 
@@ -924,6 +939,8 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="the whole System-1 path: VLM prefill then action generation for 32 robots "
                          "(prints its own JSON line)")
+    ap.add_argument("--prefill-causal", type=int, default=0, metavar="C",
+                    help="with --prefill: each job's last C tokens (at most P) form a causal segment")
     ap.add_argument("--prefill-cache", choices=["per_layer", "context"], default="per_layer",
                     help="with --prefill: per-layer backbone K/V, or the context form (the backbone's "
                          "normalised output projected for every layer of an 18-layer cross-attending head)")

@@ -10,9 +10,13 @@
  *   h = the embedded prefix tokens (image patches and text, [P][d]);
  *   each layer l: u = RMSNorm(h) (eps = rms_eps, no learned gain);
  *     [q | k | v] = u W_qkv[l];  cache_k[l] = k, cache_v[l] = v;
- *     every prefix token attends to all prefix tokens of its own request
- *     (bidirectional, no positions, scale 1/sqrt(head_dim), query head g reads
- *     KV head g / (n_q / n_kv));  h += o W_o[l];
+ *     every prefix token attends to the prefix tokens of its own request
+ *     (no positions, scale 1/sqrt(head_dim), query head g reads KV head
+ *     g / (n_q / n_kv)): all of them (bidirectional), or, for a job with a
+ *     causal segment of its last c tokens, token t sees tokens
+ *     [0, max(P - c, t + 1)) (prefix-LM: the first P - c tokens, image patches
+ *     and prompt, see each other; each later token sees those and the
+ *     segment's tokens up to itself);  h += o W_o[l];
  *     h += gelu_tanh(RMSNorm(h) W_up[l]) W_down[l];
  *   no biases.
  * The backbone's n_layers, n_kv_heads and head_dim must equal the action
@@ -90,7 +94,9 @@ typedef struct rosa_prefix_job {
   void       *prefix_k;
   void       *prefix_v;
   int32_t     prefix_len;  /* P >= 1 */
-  int32_t     reserved;    /* must be 0 */
+  int32_t     causal_len;  /* c, 0 <= c <= P: the last c tokens form a causal
+                              segment (see the layer above); 0 = all
+                              bidirectional */
 } rosa_prefix_job;
 
 /* Create a handle: validate, upload and repack the weights, allocate
@@ -102,7 +108,7 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
 
 /* Run the backbone over n jobs (a ragged batch: each job's tokens attend only
  * to their own prefix) and write every layer's caches.  n == 0 is a no-op.
- * Errors: ROSA_E_INVALID (NULL pointers, P < 1, reserved != 0),
+ * Errors: ROSA_E_INVALID (NULL pointers, P < 1, causal_len outside [0, P]),
  * ROSA_E_CAPACITY (n or the sum of P above the capacity), ROSA_E_DEVICE. */
 rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32_t n);
 

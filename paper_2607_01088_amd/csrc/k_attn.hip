@@ -78,7 +78,10 @@ struct AttnTile {
 // w and w + 4 of the item).  Step t (one 32-key tile): wait for K tile t and
 // V tile t, one barrier, issue the copies of V tile t + 1 and K tile t + 2,
 // S^T = K Q^T, the softmax of the tile, O^T += V^T P^T.
-template <int HD, int NG>
+// CAUSAL: the prefix producer's launches with causal segments; each query
+// row additionally masks the keys at or past its token's limit
+// max(causal_b, t + 1) in the tiles that reach it.
+template <int HD, int NG, bool CAUSAL>
 __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
   using at::TK;
   using T = AttnTile<HD, NG>;
@@ -279,6 +282,37 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
+  // Causal limits: key j is visible to this lane's query row of group g iff
+  // j < lim(g) (rows past the item's queries never mask).  Only the wave's
+  // smallest limit, lim_lo (wave-uniform), is held through the key loop: it
+  // tells the tiles that need the mask, which recomputes the lane's limits.
+  auto causal_lim = [&](int g, int ln) __attribute__((always_inline)) -> int {
+    const int loc = 32 * (wave + 4 * g) + (ln & 31);
+    return loc < it.nq ? max(it.causal_b, (it.q0 + loc) / G + 1) : 0x7fffffff;
+  };
+  int lim_lo = 0x7fffffff;
+  if constexpr (CAUSAL) {
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      int v = causal_lim(g, lane);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+      lim_lo = min(lim_lo, __builtin_amdgcn_readfirstlane(v));
+    }
+  }
+  auto mask_causal = [&](f32x16 (&s)[NG], int kt0) __attribute__((always_inline)) {
+    int ln = lane;
+    asm volatile("" : "+v"(ln));            // recomputed here, not held through the loop
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int lim = causal_lim(g, ln);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt0 + (r >> 2) * 8 + ((ln >> 5) & 1) * 4 + (r & 3);
+        if (key >= lim) s[g][r] = -INFINITY;
+      }
+    }
+  };
   // Keys of the item's first tile below its key range take no weight.
   auto mask_first = [&](f32x16 (&s)[NG]) __attribute__((always_inline)) {
 #pragma unroll
@@ -354,6 +388,9 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
     f32x16 sc[NG];
     scores(KS, sc);
     if (t == 0) mask_first(sc);
+    if constexpr (CAUSAL) {
+      if (k0 + TK * t + TK > lim_lo) mask_causal(sc, k0 + TK * t);
+    }
     if constexpr (MODE == 1) {
 #pragma unroll
       for (int g = 0; g < NG; ++g) m_true[g] = fmaxf(m_true[g], tile_max(sc[g]));
@@ -544,7 +581,8 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnArgs a) {
   }
   const float scale = 1.0f / sqrtf((float)HD);
   float m = -INFINITY, l = 0.f;
-  for (int key = it.kbeg; key < it.kend; ++key) {
+  const int kend = a.causal ? min(it.kend, max(it.causal_b, qt + 1)) : it.kend;
+  for (int key = it.kbeg; key < kend; ++key) {
     const float *kr = key < rq.P ? pk + (size_t)key * prow : ak + (size_t)(key - rq.P) * a.ldqkv;
     const float *vr = key < rq.P ? pv + (size_t)key * prow : av + (size_t)(key - rq.P) * a.ldqkv;
     float dot = 0.f;
@@ -645,10 +683,22 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
     if (a.n_blocks <= 0) return hipSuccess;
     dim3 grid(a.n_blocks);
     switch (a.hd) {
-      case 32: hipLaunchKernelGGL((attention_bf16_kernel<32, attn_groups_per_wave(32)>), grid, dim3(256), 0, s, a); break;
-      case 64: hipLaunchKernelGGL((attention_bf16_kernel<64, attn_groups_per_wave(64)>), grid, dim3(256), 0, s, a); break;
-      case 128: hipLaunchKernelGGL((attention_bf16_kernel<128, attn_groups_per_wave(128)>), grid, dim3(256), 0, s, a); break;
-      case 256: hipLaunchKernelGGL((attention_bf16_kernel<256, attn_groups_per_wave(256)>), grid, dim3(256), 0, s, a); break;
+      case 32:
+        if (a.causal) hipLaunchKernelGGL((attention_bf16_kernel<32, attn_groups_per_wave(32), true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((attention_bf16_kernel<32, attn_groups_per_wave(32), false>), grid, dim3(256), 0, s, a);
+        break;
+      case 64:
+        if (a.causal) hipLaunchKernelGGL((attention_bf16_kernel<64, attn_groups_per_wave(64), true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((attention_bf16_kernel<64, attn_groups_per_wave(64), false>), grid, dim3(256), 0, s, a);
+        break;
+      case 128:
+        if (a.causal) hipLaunchKernelGGL((attention_bf16_kernel<128, attn_groups_per_wave(128), true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((attention_bf16_kernel<128, attn_groups_per_wave(128), false>), grid, dim3(256), 0, s, a);
+        break;
+      case 256:
+        if (a.causal) hipLaunchKernelGGL((attention_bf16_kernel<256, attn_groups_per_wave(256), true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((attention_bf16_kernel<256, attn_groups_per_wave(256), false>), grid, dim3(256), 0, s, a);
+        break;
       default: return hipErrorInvalidValue;
     }
   } else {

@@ -36,7 +36,12 @@ struct AttnItem {
   int32_t req, kvh, q0, nq, kbeg, kend, slot;
   int32_t P, tok_off;
   int32_t next;          // launch lists: the block's next entry, -1 after its last
-  int32_t pad1, pad2;
+  // Causal launches (AttnArgs::causal) only: key j is visible to the query
+  // rows of token t (counted from the request's first token) iff
+  // j < max(causal_b, t + 1), i.e. tokens below causal_b see each other and
+  // every later token sees the keys up to itself.
+  int32_t causal_b;
+  int32_t pad2;
 };
 static_assert(sizeof(AttnItem) == 64, "AttnItem is 64 bytes");
 
@@ -197,6 +202,9 @@ struct AttnArgs {
   int nq, nkv, hd;
   float *part_o;                   // [slot][kAttnQB][hd] fp32
   float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
+  // 1: every item's causal_b masks keys per query token (the prefix
+  // producer's causal segments); such items are never key-split.
+  int causal;
 };
 hipError_t launch_attention(const AttnArgs &a, bool bf16, hipStream_t s);
 // Host: XCD-balanced item lists of persistent blocks for the items of the

@@ -41,6 +41,7 @@ struct PrefillPlan {
   std::vector<int32_t> list, list_next;   // bf16 launch order (block item lists)
   int n_blocks = 0;
   int64_t M = 0;
+  bool causal = false;                    // some job has a causal segment
 };
 
 }  // namespace
@@ -198,8 +199,8 @@ rosa_status build_prefill_plan(const rosa_prefill *h, const rosa_prefix_job *job
   for (int i = 0; i < n; ++i) {
     const rosa_prefix_job &j = jobs[i];
     char buf[160];
-    if (j.prefix_len < 1 || j.reserved != 0) {
-      snprintf(buf, sizeof buf, "job %d: prefix_len=%d reserved=%d out of range", i, j.prefix_len, j.reserved);
+    if (j.prefix_len < 1 || j.causal_len < 0 || j.causal_len > j.prefix_len) {
+      snprintf(buf, sizeof buf, "job %d: prefix_len=%d causal_len=%d out of range", i, j.prefix_len, j.causal_len);
       err = buf; return ROSA_E_INVALID;
     }
     if (!j.embeddings || !j.prefix_k || !j.prefix_v) {
@@ -231,15 +232,22 @@ rosa_status build_prefill_plan(const rosa_prefill *h, const rosa_prefix_job *job
   const int G = h->nq / h->nkv;
   const int gpb = 4 * attn_groups_per_wave(h->hd);
   int64_t total_qb = 0;
-  for (int i = 0; i < n; ++i) total_qb += (int64_t)h->nkv * query_blocks(jobs[i].prefix_len * G, gpb);
+  for (int i = 0; i < n; ++i) {
+    total_qb += (int64_t)h->nkv * query_blocks(jobs[i].prefix_len * G, gpb);
+    if (jobs[i].causal_len > 0) p.causal = true;
+  }
   const bool split = h->bf16 && total_qb > 0 && total_qb < kAttnSplitTarget;
   int slots = 0;
   std::vector<std::pair<int, int>> ranges;
   for (int i = 0; i < n; ++i) {
     const int P = jobs[i].prefix_len;
+    // Tokens below b see each other; later tokens see the keys up to their own.
+    const int b = P - jobs[i].causal_len;
     const int R = P * G, ngrp = (R + 31) / 32, nqb = query_blocks(R, gpb);
     int nsplit = 1, chunk = P;
-    if (split) {
+    // A causal job's keys are not split: a split item could then hold no
+    // visible key for some of its query rows.
+    if (split && b == P) {
       const int want = (int)((kAttnSplitTarget + total_qb - 1) / total_qb);
       const int most = std::max(1, (P + kAttnMinSplitKeys - 1) / kAttnMinSplitKeys);
       nsplit = std::min(want, most);
@@ -260,6 +268,9 @@ rosa_status build_prefill_plan(const rosa_prefill *h, const rosa_prefix_job *job
           it.kbeg = c * chunk;
           it.kend = std::min(P, (c + 1) * chunk);
           it.slot = nsplit > 1 ? slots++ : -1;
+          // Keys past the block's last token's limit are invisible to all its rows.
+          it.causal_b = b;
+          if (b < P) it.kend = std::min(it.kend, std::max(b, (q0 + nq - 1) / G + 1));
           p.items.push_back(it);
         }
       }
@@ -466,6 +477,7 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       a.qkv = h->qkv; a.ldqkv = h->qkv_dim; a.o = h->o; a.ldo = h->o_dim; a.o_rows = h->kb_rows;
       a.nq = h->nq; a.nkv = h->nkv; a.hd = h->hd;
       a.part_o = h->part_o; a.part_ml = h->part_ml;
+      a.causal = p.causal ? 1 : 0;
       e = ptimed(h, pcAttention, [&] { return launch_attention(a, h->bf16, s); });
       if (e == hipSuccess && !p.groups.empty())
         e = ptimed(h, pcMerge, [&] {

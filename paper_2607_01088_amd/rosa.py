@@ -73,7 +73,7 @@ class VlmWeights(C.Structure):
 
 class PrefixJob(C.Structure):
     _fields_ = [("embeddings", C.c_void_p), ("prefix_k", C.c_void_p), ("prefix_v", C.c_void_p),
-                ("prefix_len", C.c_int32), ("reserved", C.c_int32)]
+                ("prefix_len", C.c_int32), ("causal_len", C.c_int32)]
 
 
 class RatePoint(C.Structure):
@@ -473,11 +473,12 @@ def vlm_config(shape, dtype: str, head_layers: int = 0) -> VlmConfig:
                      ROSA_CACHE_CONTEXT if head_layers > 0 else ROSA_CACHE_PER_LAYER, head_layers)
 
 
-def prefix_job(embeddings, prefix_k, prefix_v, P: int) -> PrefixJob:
-    """A prefix-producer job from torch device tensors (or raw integer device pointers)."""
+def prefix_job(embeddings, prefix_k, prefix_v, P: int, causal_len: int = 0) -> PrefixJob:
+    """A prefix-producer job from torch device tensors (or raw integer device
+    pointers); causal_len: the job's trailing causal segment (0: none)."""
     def ptr(t):
         return t if isinstance(t, int) else t.data_ptr()
-    return PrefixJob(ptr(embeddings), ptr(prefix_k), ptr(prefix_v), P, 0)
+    return PrefixJob(ptr(embeddings), ptr(prefix_k), ptr(prefix_v), P, causal_len)
 
 
 class PrefixProducer:

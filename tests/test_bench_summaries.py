@@ -30,3 +30,11 @@ def test_classify_dispatches_split_products_with_fused_norms():
     assert [role[i] for i in range(len(seq))] == ["modnorm", "gemm_qkv", "attention", "attn_merge", "gemm_o",
                                                   "gemm_o", "gemm_up", "gemm_down", "gemm_down", "gemm_qkv",
                                                   "attention"]
+
+
+def test_visible_keys_counts_the_prefix_lm_mask():
+    # brute force over the mask: token t sees key j iff j < max(P - c, t + 1)
+    for P in (1, 5, 17):
+        for c in range(P + 1):
+            brute = sum(1 for t in range(P) for j in range(P) if j < max(P - c, t + 1))
+            assert bench.visible_keys(P, c) == brute

@@ -48,9 +48,10 @@ def _tdtype(dtype):
 class _Jobs:
     """Embeddings on the device and NaN-filled cache buffers."""
 
-    def __init__(self, shape, dtype, lens, seed, cache_layers=None):
+    def __init__(self, shape, dtype, lens, seed, cache_layers=None, causal=None):
         rosa = _rosa()
         self.lens = list(lens)
+        self.causal = list(causal) if causal is not None else [0] * len(lens)
         self.x = [make_prefix_embeddings(shape, P, dtype, seed * 1000 + i) for i, P in enumerate(lens)]
         td = _tdtype(dtype)
         self.emb = [torch.from_numpy(x).to(td).cuda() for x in self.x]
@@ -59,16 +60,17 @@ class _Jobs:
                                      dtype=td, device="cuda")
         self.k = [cache(P) for P in lens]
         self.v = [cache(P) for P in lens]
-        self.structs = [rosa.prefix_job(e, k, v, P) for e, k, v, P in zip(self.emb, self.k, self.v, lens)]
+        self.structs = [rosa.prefix_job(e, k, v, P, c)
+                        for e, k, v, P, c in zip(self.emb, self.k, self.v, lens, self.causal)]
 
     def caches(self, i):
         return self.k[i].float().cpu().numpy(), self.v[i].float().cpu().numpy()
 
 
-def _run(shape, dtype, lens, seed=1, max_jobs=None, max_tokens=None):
+def _run(shape, dtype, lens, seed=1, max_jobs=None, max_tokens=None, causal=None):
     rosa = _rosa()
     w = _weights(shape, dtype)
-    jobs = _Jobs(shape, dtype, lens, seed)
+    jobs = _Jobs(shape, dtype, lens, seed, causal=causal)
     pp = rosa.PrefixProducer(shape, dtype, w, max_jobs or len(lens), max_tokens or sum(lens))
     pp.run(jobs.structs)
     torch.cuda.synchronize()
@@ -78,12 +80,12 @@ def _run(shape, dtype, lens, seed=1, max_jobs=None, max_tokens=None):
 
 def _check_layers(shape, dtype, w, jobs, idx):
     for i in idx:
-        K, V = prefill(jobs.x[i], w, shape)
+        K, V = prefill(jobs.x[i], w, shape, causal_len=jobs.causal[i])
         gk, gv = jobs.caches(i)
         assert np.isfinite(gk).all() and np.isfinite(gv).all(), i
         for l in range(shape.n_layers):
             ek, ev = rel_l2(gk[l], K[l]), rel_l2(gv[l], V[l])
-            print(f"job {i} P={jobs.lens[i]} layer {l}: K {ek:.2e} V {ev:.2e}", flush=True)
+            print(f"job {i} P={jobs.lens[i]} causal {jobs.causal[i]} layer {l}: K {ek:.2e} V {ev:.2e}", flush=True)
             assert ek <= TOL[dtype] and ev <= TOL[dtype], (i, l, ek, ev)
 
 
@@ -94,6 +96,26 @@ def test_tiny_ragged_batch_matches_oracle(dtype):
     lens = [1, 5, 37, 130, 300, 64]
     w, jobs = _run(TINY_VLM, dtype, lens)
     _check_layers(TINY_VLM, dtype, w, jobs, range(len(lens)))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_causal_segments_match_oracle(dtype):
+    # Jobs ending in causal segments (a single causal token, wholly causal
+    # jobs, partial segments over several 32-row groups) next to bidirectional
+    # jobs in the same launch, one of them long enough for its keys to be
+    # split over work items in bf16.
+    lens = [1, 5, 37, 130, 300, 64, 300]
+    causal = [1, 0, 37, 50, 100, 7, 0]
+    w, jobs = _run(TINY_VLM, dtype, lens, seed=5, causal=causal)
+    _check_layers(TINY_VLM, dtype, w, jobs, range(len(lens)))
+
+
+def test_bf16_pi0_width_causal_segments():
+    # head_dim 256 tiles with a 48-token causal text segment after the image
+    # patches, a bidirectional job and a wholly causal one.
+    lens = [816, 300, 17]
+    w, jobs = _run(PI0_VLM_2L, "bf16", lens, seed=6, causal=[48, 0, 17])
+    _check_layers(PI0_VLM_2L, "bf16", w, jobs, range(len(lens)))
 
 
 def test_bf16_many_jobs_no_key_split():
@@ -150,11 +172,11 @@ def test_prefill_feeds_action_expert(dtype):
 
 # ------------------------------------------------------------------ context form (cross-attending head)
 
-def _run_context(shape, dtype, lens, head_layers, seed):
+def _run_context(shape, dtype, lens, head_layers, seed, causal=None):
     rosa = _rosa()
     w = _weights(shape, dtype)
     wc = make_context_weights(shape, head_layers, dtype)
-    jobs = _Jobs(shape, dtype, lens, seed, cache_layers=head_layers)
+    jobs = _Jobs(shape, dtype, lens, seed, cache_layers=head_layers, causal=causal)
     pp = rosa.PrefixProducer(shape, dtype, w, len(lens), sum(lens), context_weights=wc)
     pp.run(jobs.structs)
     torch.cuda.synchronize()
@@ -162,15 +184,16 @@ def _run_context(shape, dtype, lens, head_layers, seed):
     return w, wc, jobs
 
 
-@pytest.mark.parametrize("shape,dtype,lens,head_layers", [
-    (TINY_VLM, "fp32", [1, 37, 300, 64], 2),
-    (TINY_VLM, "bf16", [1, 37, 300, 64], 3),
-    (PI0_VLM_2L, "bf16", [816, 65], 18),
+@pytest.mark.parametrize("shape,dtype,lens,head_layers,causal", [
+    (TINY_VLM, "fp32", [1, 37, 300, 64], 2, None),
+    (TINY_VLM, "bf16", [1, 37, 300, 64], 3, None),
+    (TINY_VLM, "bf16", [1, 37, 300, 64], 2, [1, 0, 120, 9]),
+    (PI0_VLM_2L, "bf16", [816, 65], 18, None),
 ])
-def test_context_form_matches_oracle(shape, dtype, lens, head_layers):
-    w, wc, jobs = _run_context(shape, dtype, lens, head_layers, seed=6)
+def test_context_form_matches_oracle(shape, dtype, lens, head_layers, causal):
+    w, wc, jobs = _run_context(shape, dtype, lens, head_layers, seed=6, causal=causal)
     for i in range(len(lens)):
-        K, V = prefill_context(jobs.x[i], w, shape, wc)
+        K, V = prefill_context(jobs.x[i], w, shape, wc, causal_len=jobs.causal[i])
         gk, gv = jobs.caches(i)
         for l in range(head_layers):
             ek, ev = rel_l2(gk[l], K[l]), rel_l2(gv[l], V[l])
@@ -209,9 +232,9 @@ def test_validation():
     assert pp.run_status([]) == rosa.ROSA_OK
     bad = rosa.prefix_job(jobs.emb[0], jobs.k[0], jobs.v[0], 0)
     assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
-    bad = rosa.prefix_job(jobs.emb[0], jobs.k[0], jobs.v[0], 8)
-    bad.reserved = 1
-    assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
+    for c in (-1, 9):                                   # causal_len outside [0, P]
+        bad = rosa.prefix_job(jobs.emb[0], jobs.k[0], jobs.v[0], 8, c)
+        assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
     bad = rosa.prefix_job(0, jobs.k[0], jobs.v[0], 8)
     assert pp.run_status([bad]) == rosa.ROSA_E_INVALID
     bad = rosa.prefix_job(jobs.emb[0].data_ptr() + 4, jobs.k[0], jobs.v[0], 7)
