@@ -263,6 +263,7 @@ class VlmShape:
     head_dim: int
     d_mlp: int
     rms_eps: float = 1e-6
+    rope_base: float = 0.0      # > 1: rotary position embedding of queries and keys; 0: no positions
 
     @property
     def qkv_dim(self) -> int:

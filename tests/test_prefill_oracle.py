@@ -1,10 +1,13 @@
 """Pins of the prefix-producer oracle (Sec. 2.2.1: the VLM backbone's per-layer
 keys and values are the action head's prefix cache).  No GPU needed."""
+import cmath
+import dataclasses
 import math
 
 import numpy as np
 
 from oracle import prefill, prefill_context
+from oracle.prefill import rotary
 from synthetic import TINY_VLM, VlmShape, make_context_weights, make_prefix_embeddings, make_vlm_weights
 
 SMALL = VlmShape(n_layers=2, d_model=8, n_q_heads=4, n_kv_heads=2, head_dim=4, d_mlp=12)
@@ -13,7 +16,9 @@ SMALL = VlmShape(n_layers=2, d_model=8, n_q_heads=4, n_kv_heads=2, head_dim=4, d
 def _brute_prefill(x, w, s, causal_len=0):
     """Scalar brute force on nested Python lists.  With a causal segment of the
     last causal_len tokens, key u is visible to token t when u lies before the
-    segment or u <= t."""
+    segment or u <= t.  With s.rope_base > 0 each (i, i + hd/2) pair of a query
+    or key head at position t is the complex number x_i + j x_(i+hd/2) times
+    exp(j t rope_base^(-2i/hd))."""
     L, d, nq, nkv, hd, dff = s.n_layers, s.d_model, s.n_q_heads, s.n_kv_heads, s.head_dim, s.d_mlp
     G = nq // nkv
     P = len(x)
@@ -31,6 +36,16 @@ def _brute_prefill(x, w, s, causal_len=0):
         qkv = [matvec(norm(row), w["w_qkv"][l]) for row in h]
         q = [[r[g * hd:(g + 1) * hd] for g in range(nq)] for r in qkv]
         k = [[r[(nq + j) * hd:(nq + j + 1) * hd] for j in range(nkv)] for r in qkv]
+        if s.rope_base > 0:
+            def turn(vec, t):
+                half = hd // 2
+                out = [0.0] * hd
+                for i in range(half):
+                    z = complex(vec[i], vec[i + half]) * cmath.exp(1j * t * s.rope_base ** (-2.0 * i / hd))
+                    out[i], out[i + half] = z.real, z.imag
+                return out
+            q = [[turn(head, t) for head in q[t]] for t in range(P)]
+            k = [[turn(head, t) for head in k[t]] for t in range(P)]
         v = [[r[(nq + nkv + j) * hd:(nq + nkv + j + 1) * hd] for j in range(nkv)] for r in qkv]
         Ks.append(k)
         Vs.append(v)
@@ -186,6 +201,75 @@ def test_context_form_causal_matches_scalar_bruteforce():
         for t in range(5):
             ms = sum(z * z for z in h[t]) / len(h[t])
             u = [z / math.sqrt(ms + SMALL.rms_eps) for z in h[t]]
+            kv = [sum(u[i] * wc[e][i][j] for i in range(len(u))) for j in range(2 * kvw)]
+            np.testing.assert_allclose(K[e, t].reshape(-1), kv[:kvw], rtol=0, atol=1e-11)
+            np.testing.assert_allclose(V[e, t].reshape(-1), kv[kvw:], rtol=0, atol=1e-11)
+
+
+SMALL_ROPE = dataclasses.replace(SMALL, rope_base=10000.0)
+
+
+def test_rotary_identity_at_zero_and_plain_rotation_at_width_two():
+    rng = np.random.default_rng(20)
+    x = rng.standard_normal((7, 3, 8))
+    y = rotary(x, 10000.0)
+    np.testing.assert_array_equal(y[0], x[0])                       # position 0: angle 0
+    # head width 2: the single pair turns by p radians (base^0 = 1)
+    x2 = rng.standard_normal((9, 1, 2))
+    y2 = rotary(x2, 500.0)
+    for p in range(9):
+        c, s = math.cos(p), math.sin(p)
+        a, b = x2[p, 0]
+        np.testing.assert_allclose(y2[p, 0], [a * c - b * s, b * c + a * s], rtol=0, atol=1e-14)
+
+
+def test_rotary_keeps_pair_lengths_and_depends_on_relative_position():
+    rng = np.random.default_rng(21)
+    hd, P = 16, 40
+    x = rng.standard_normal((P, 2, hd))
+    y = rotary(x, 10000.0)
+    half = hd // 2
+    np.testing.assert_allclose(np.hypot(y[..., :half], y[..., half:]), np.hypot(x[..., :half], x[..., half:]),
+                               rtol=1e-13)
+    # the same query and key vectors at every position: q_m . k_n depends on m - n only
+    qv, kv = rng.standard_normal(hd), rng.standard_normal(hd)
+    rq = rotary(np.tile(qv, (P, 1, 1)), 10000.0)[:, 0]
+    rk = rotary(np.tile(kv, (P, 1, 1)), 10000.0)[:, 0]
+    dots = rq @ rk.T
+    for d in (-5, 0, 3, 17):
+        diag = np.array([dots[m, m - d] for m in range(max(0, d), min(P, P + d))])
+        np.testing.assert_allclose(diag, diag[0], rtol=1e-11, atol=1e-11)
+    assert abs(dots[5, 2] - dots[5, 3]) > 1e-6                      # and it does depend on it
+
+
+def test_rotary_prefill_matches_scalar_bruteforce():
+    rng = np.random.default_rng(22)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL_ROPE, "fp32").items()}
+    x = rng.standard_normal((6, SMALL_ROPE.d_model))
+    for c in (0, 2):
+        K, V = prefill(x, w, SMALL_ROPE, causal_len=c)
+        Kb, Vb, _ = _brute_prefill(x, w, SMALL_ROPE, causal_len=c)
+        np.testing.assert_allclose(K, Kb, rtol=0, atol=1e-11)
+        np.testing.assert_allclose(V, Vb, rtol=0, atol=1e-11)
+    # positions take effect: permuting the tokens no longer permutes the cache
+    perm = np.array([1, 0, 2, 3, 4, 5])
+    Kp, _ = prefill(x[perm], w, SMALL_ROPE)
+    K0, _ = prefill(x, w, SMALL_ROPE)
+    assert np.abs(Kp[:, perm] - K0).max() > 1e-6
+
+
+def test_rotary_context_form_matches_scalar_bruteforce():
+    rng = np.random.default_rng(23)
+    w = {k: rng.standard_normal(v.shape) * 0.5 for k, v in make_vlm_weights(SMALL_ROPE, "fp32").items()}
+    wc = rng.standard_normal((2, SMALL_ROPE.d_model, 2 * SMALL_ROPE.n_kv_heads * SMALL_ROPE.head_dim)) * 0.5
+    x = rng.standard_normal((5, SMALL_ROPE.d_model))
+    K, V = prefill_context(x, w, SMALL_ROPE, wc)
+    _, _, h = _brute_prefill(x, w, SMALL_ROPE)
+    kvw = SMALL_ROPE.n_kv_heads * SMALL_ROPE.head_dim
+    for e in range(2):
+        for t in range(5):
+            ms = sum(z * z for z in h[t]) / len(h[t])
+            u = [z / math.sqrt(ms + SMALL_ROPE.rms_eps) for z in h[t]]
             kv = [sum(u[i] * wc[e][i][j] for i in range(len(u))) for j in range(2 * kvw)]
             np.testing.assert_allclose(K[e, t].reshape(-1), kv[:kvw], rtol=0, atol=1e-11)
             np.testing.assert_allclose(V[e, t].reshape(-1), kv[kvw:], rtol=0, atol=1e-11)
