@@ -770,6 +770,9 @@ def prefill_bench(torch, rosa, args):
     batch of robots' embedded prefixes; value = prefix tokens/s."""
     from synthetic import PI0_VLM, make_context_weights, make_prefix_embeddings, make_vlm_weights, prefill_lengths
     shape = PI0_VLM
+    if args.prefill_rope:
+        import dataclasses
+        shape = dataclasses.replace(shape, rope_base=args.prefill_rope)
     lens = prefill_lengths()
     context = args.prefill_cache == "context"
     head_layers = 18
@@ -834,9 +837,10 @@ def prefill_bench(torch, rosa, args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "vlm_prefill_b32" + ("_context" if context else "")
-                   + (f"_causal{args.prefill_causal}" if args.prefill_causal else ""), "jobs": len(lens),
+                   + (f"_causal{args.prefill_causal}" if args.prefill_causal else "")
+                   + ("_rope" if args.prefill_rope else ""), "jobs": len(lens),
                    "prefix_tokens": int(sum(lens)), "cache_form": args.prefill_cache,
-                   "causal_segment_tokens": args.prefill_causal,
+                   "causal_segment_tokens": args.prefill_causal, "rope_base": args.prefill_rope,
                    "backbone": "18 layers, width 2048, 8 query heads / 1 KV head of 256, MLP 16384"},
         "jobs_per_s": round(len(lens) * args.steps / elapsed, 2),
         "p50_ms": round(float(np.percentile(lat, 50)), 3),
@@ -941,6 +945,8 @@ def main():
                          "(prints its own JSON line)")
     ap.add_argument("--prefill-causal", type=int, default=0, metavar="C",
                     help="with --prefill: each job's last C tokens (at most P) form a causal segment")
+    ap.add_argument("--prefill-rope", type=float, default=0.0, metavar="BASE",
+                    help="with --prefill: rotary position embedding of the backbone's queries and keys")
     ap.add_argument("--prefill-cache", choices=["per_layer", "context"], default="per_layer",
                     help="with --prefill: per-layer backbone K/V, or the context form (the backbone's "
                          "normalised output projected for every layer of an 18-layer cross-attending head)")

@@ -9,9 +9,12 @@
  * The paper does not write out the backbone; the library takes this reading:
  *   h = the embedded prefix tokens (image patches and text, [P][d]);
  *   each layer l: u = RMSNorm(h) (eps = rms_eps, no learned gain);
- *     [q | k | v] = u W_qkv[l];  cache_k[l] = k, cache_v[l] = v;
+ *     [q | k | v] = u W_qkv[l]; with rope_base > 0, q and k are rotated
+ *       (rotary position embedding at the token's index p within its job:
+ *       elements i and i + hd/2 of each head turn by p * rope_base^(-2i/hd));
+ *     cache_k[l] = k, cache_v[l] = v;
  *     every prefix token attends to the prefix tokens of its own request
- *     (no positions, scale 1/sqrt(head_dim), query head g reads KV head
+ *     (scale 1/sqrt(head_dim), query head g reads KV head
  *     g / (n_q / n_kv)): all of them (bidirectional), or, for a job with a
  *     causal segment of its last c tokens, token t sees tokens
  *     [0, max(P - c, t + 1)) (prefix-LM: the first P - c tokens, image patches
@@ -69,6 +72,9 @@ typedef struct rosa_vlm_config {
   int32_t dtype;           /* rosa_dtype */
   int32_t cache_form;      /* rosa_cache_form */
   int32_t head_layers;     /* ROSA_CACHE_CONTEXT: layers of the action head (L_e) */
+  float   rope_base;       /* > 1: rotary position embedding of the backbone's
+                              queries and keys with this base (10000 in Gemma);
+                              0: no positions; else ROSA_E_INVALID */
 } rosa_vlm_config;
 
 /* Weights: HOST float32, row-major [in][out] (y = x W), L = n_layers, d = d_model,

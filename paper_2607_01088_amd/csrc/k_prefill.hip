@@ -1,11 +1,13 @@
 // Row kernels of the prefix producer: the embedded prefix tokens of every job
-// into the stacked fp32 residual stream, and each layer's K and V projections
-// out of the stacked QKV rows into the jobs' caches.  Both are pure copies
-// (HBM bound, 16-byte vectors); the backbone's arithmetic runs in the shared
-// normalisation, GEMM and attention kernels.
+// into the stacked fp32 residual stream, each layer's K and V projections out
+// of the stacked QKV rows into the jobs' caches (both pure copies, HBM bound,
+// 16-byte vectors), and the optional rotary position embedding of each
+// layer's queries and keys.  The rest of the backbone's arithmetic runs in the
+// shared normalisation, GEMM and attention kernels.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "rosa_device.h"
 #include "rosa_internal.h"
@@ -61,6 +63,73 @@ __global__ void __launch_bounds__(256) prefill_kv_scatter_kernel(const PrefillJo
   }
 }
 
+// Rotary position table: tab[p][i] = (cos, sin) of p * base^(-i / half) for
+// positions p < n_pos and pairs i < half (half = head_dim / 2), computed in
+// double and rounded once.
+__global__ void __launch_bounds__(256) rope_table_kernel(float2 *__restrict__ tab, int n_pos, int half,
+                                                         double log2_base) {
+  const int64_t n = (int64_t)n_pos * half;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < n; idx += (int64_t)gridDim.x * blockDim.x) {
+    const int pos = (int)(idx / half), i = (int)(idx - (int64_t)pos * half);
+    const double inv = exp2(-(double)i / (double)half * log2_base);
+    double sn, cs;
+    sincos((double)pos * inv, &sn, &cs);
+    tab[idx] = make_float2((float)cs, (float)sn);
+  }
+}
+
+// In place on the first nheads heads of every qkv row (the query heads, then
+// the key heads): element pair (i, i + half) of a head at the row's position p
+// (its index within its job) becomes (x1 c - x2 s, x2 c + x1 s) with
+// (c, s) = tab[p][i].  Four pairs per thread.
+template <typename T>
+__global__ void __launch_bounds__(256) rope_apply_kernel(const PrefillJob *__restrict__ jobs,
+                                                         const int32_t *__restrict__ row_job, int64_t M,
+                                                         T *__restrict__ qkv, int64_t ldqkv, int nheads, int half,
+                                                         const float2 *__restrict__ tab) {
+  const int quads = half / 4;
+  const int64_t per_row = (int64_t)nheads * quads;
+  const int64_t total = M * per_row;
+  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = idx / per_row;
+    const int r = (int)(idx - row * per_row);
+    const int head = r / quads, i = (r - head * quads) * 4;
+    const int64_t pos = row - jobs[row_job[row]].tok_off;
+    T *x = qkv + row * ldqkv + (int64_t)head * 2 * half + i;
+    float a[4], b[4];
+    if constexpr (sizeof(T) == 4) {
+      const float4 va = *reinterpret_cast<const float4 *>(x), vb = *reinterpret_cast<const float4 *>(x + half);
+      a[0] = va.x; a[1] = va.y; a[2] = va.z; a[3] = va.w;
+      b[0] = vb.x; b[1] = vb.y; b[2] = vb.z; b[3] = vb.w;
+    } else {
+      const uint2 ra = *reinterpret_cast<const uint2 *>(x), rb = *reinterpret_cast<const uint2 *>(x + half);
+      a[0] = __uint_as_float(ra.x << 16); a[1] = __uint_as_float(ra.x & 0xffff0000u);
+      a[2] = __uint_as_float(ra.y << 16); a[3] = __uint_as_float(ra.y & 0xffff0000u);
+      b[0] = __uint_as_float(rb.x << 16); b[1] = __uint_as_float(rb.x & 0xffff0000u);
+      b[2] = __uint_as_float(rb.y << 16); b[3] = __uint_as_float(rb.y & 0xffff0000u);
+    }
+    const float2 *t = tab + pos * half + i;
+    float ya[4], yb[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float2 cs = t[j];
+      ya[j] = a[j] * cs.x - b[j] * cs.y;
+      yb[j] = b[j] * cs.x + a[j] * cs.y;
+    }
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4 *>(x) = make_float4(ya[0], ya[1], ya[2], ya[3]);
+      *reinterpret_cast<float4 *>(x + half) = make_float4(yb[0], yb[1], yb[2], yb[3]);
+    } else {
+      bf16x4 oa, ob;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { oa[j] = (bf16)ya[j]; ob[j] = (bf16)yb[j]; }
+      *reinterpret_cast<bf16x4 *>(x) = oa;
+      *reinterpret_cast<bf16x4 *>(x + half) = ob;
+    }
+  }
+}
+
 int grid_for(int64_t threads) {
   const int64_t blocks = (threads + 255) / 256;
   return (int)std::min<int64_t>(std::max<int64_t>(blocks, 1), 8192);
@@ -89,6 +158,31 @@ hipError_t launch_prefill_kv_scatter(const PrefillJob *jobs, const int32_t *row_
   hipLaunchKernelGGL(prefill_kv_scatter_kernel, dim3(grid), dim3(256), 0, s, jobs, row_job, M,
                      (const uint8_t *)qkv, (int64_t)ldqkv * (int64_t)esz, (int64_t)nq * hd * (int64_t)esz, kv_bytes,
                      layer);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_rope_table(float *tab, int n_pos, int head_dim, double base, hipStream_t s) {
+  if (n_pos <= 0) return hipSuccess;
+  if (head_dim % 8 || !(base > 1.0)) return hipErrorInvalidValue;
+  const int half = head_dim / 2;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(grid_for((int64_t)n_pos * half)), dim3(256), 0, s,
+                     reinterpret_cast<float2 *>(tab), n_pos, half, std::log2(base));
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_rope(const PrefillJob *jobs, const int32_t *row_job, int64_t M, void *qkv, int ldqkv,
+                               int nheads, int head_dim, bool bf16_mode, const float *tab, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (head_dim % 8 || ldqkv % 4) return hipErrorInvalidValue;
+  const int half = head_dim / 2;
+  const int grid = grid_for(M * nheads * (half / 4));
+  const float2 *t = reinterpret_cast<const float2 *>(tab);
+  if (bf16_mode)
+    hipLaunchKernelGGL(rope_apply_kernel<bf16>, dim3(grid), dim3(256), 0, s, jobs, row_job, M, (bf16 *)qkv,
+                       (int64_t)ldqkv, nheads, half, t);
+  else
+    hipLaunchKernelGGL(rope_apply_kernel<float>, dim3(grid), dim3(256), 0, s, jobs, row_job, M, (float *)qkv,
+                       (int64_t)ldqkv, nheads, half, t);
   return hipGetLastError();
 }
 

@@ -182,6 +182,13 @@ int gemm_pick_config(int M, int N, int K, int epi, int n_cu);
 // h[row] = the job's embedding row (bf16 or fp32 in, fp32 out), d % 4 == 0.
 hipError_t launch_prefill_load(const PrefillJob *jobs, const int32_t *row_job, int64_t M, int d, bool bf16_in,
                                float *h, hipStream_t s);
+// Rotary position table [n_pos][head_dim / 2] of (cos, sin) pairs (fp32
+// values computed in double): angle p * base^(-2 i / head_dim).
+hipError_t launch_prefill_rope_table(float *tab, int n_pos, int head_dim, double base, hipStream_t s);
+// Rotary position embedding, in place, of the first nheads heads of every
+// stacked QKV row (queries, then keys) at the row's position within its job.
+hipError_t launch_prefill_rope(const PrefillJob *jobs, const int32_t *row_job, int64_t M, void *qkv, int ldqkv,
+                               int nheads, int head_dim, bool bf16_mode, const float *tab, hipStream_t s);
 // Layer `layer`'s K and V column blocks of the stacked QKV rows into each job's
 // caches; esz: bytes per element.
 hipError_t launch_prefill_kv_scatter(const PrefillJob *jobs, const int32_t *row_job, int64_t M, const void *qkv,

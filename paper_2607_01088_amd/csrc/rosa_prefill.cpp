@@ -25,10 +25,10 @@ using namespace rosa;
 namespace {
 
 enum PrefillClass {
-  pcLoad = 0, pcNorm, pcGemmQKV, pcScatter, pcAttention, pcMerge, pcGemmO, pcGemmUp, pcGemmDown, pcCount
+  pcLoad = 0, pcNorm, pcGemmQKV, pcScatter, pcAttention, pcMerge, pcGemmO, pcGemmUp, pcGemmDown, pcRope, pcCount
 };
 const char *kPrefillClassNames[pcCount] = {"load",      "norm",       "gemm_qkv", "kv_scatter", "attention",
-                                           "attn_merge", "gemm_o",    "gemm_up",  "gemm_down"};
+                                           "attn_merge", "gemm_o",    "gemm_up",  "gemm_down",  "rope"};
 
 thread_local std::string g_prefill_create_error;
 
@@ -74,6 +74,10 @@ struct rosa_prefill {
   float *zeros = nullptr, *ones = nullptr;   // [d]: zero shift and scale, unit gate
   int32_t *rowmod = nullptr;                 // [max_tokens] zeros
   float *part_o = nullptr, *part_ml = nullptr;
+  // Rotary position embedding of the queries and keys (rope_base > 0): the
+  // (cos, sin) table for positions below max_tokens, refreshed per call.
+  double rope_base = 0.0;
+  float *rope_tab = nullptr;
 
   // plan region on the device + two pinned staging copies
   void *d_plan = nullptr;
@@ -180,6 +184,7 @@ rosa_status check_vlm_config(const rosa_vlm_config *c) {
     return ROSA_E_UNSUPPORTED;
   if (c->cache_form != ROSA_CACHE_PER_LAYER && c->cache_form != ROSA_CACHE_CONTEXT) return ROSA_E_INVALID;
   if (c->cache_form == ROSA_CACHE_CONTEXT && (c->head_layers < 1 || c->head_layers > 1024)) return ROSA_E_INVALID;
+  if (!(c->rope_base == 0.f || (c->rope_base > 1.f && c->rope_base < 1e30f))) return ROSA_E_INVALID;
   return ROSA_OK;
 }
 
@@ -368,6 +373,8 @@ rosa_status rosa_prefill_create(const rosa_vlm_config *cfg, const rosa_vlm_weigh
     h->zeros = palloc<float>(h, d, e);
     h->ones = palloc<float>(h, d, e);
     h->rowmod = palloc<int32_t>(h, T, e);
+    h->rope_base = cfg->rope_base;
+    if (h->rope_base > 0.0) h->rope_tab = palloc<float>(h, T * h->hd, e);   // T positions x hd/2 (cos, sin)
     h->part_o = palloc<float>(h, (size_t)kAttnMaxSlots * kAttnQB * h->hd, e);
     h->part_ml = palloc<float>(h, (size_t)kAttnMaxSlots * kAttnQB * 2, e);
 
@@ -451,6 +458,11 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
     const hipStream_t s = h->stream;
 
     e = ptimed(h, pcLoad, [&] { return launch_prefill_load(d_jobs, d_rows, M, h->d, h->bf16, h->h, s); });
+    if (e == hipSuccess && h->rope_tab) {
+      int max_p = 0;
+      for (int i = 0; i < n; ++i) max_p = std::max(max_p, jobs[i].prefix_len);
+      e = ptimed(h, pcRope, [&] { return launch_prefill_rope_table(h->rope_tab, max_p, h->hd, h->rope_base, s); });
+    }
     for (int l = 0; l < h->L && e == hipSuccess; ++l) {
       e = ptimed(h, pcNorm, [&] {
         return launch_modnorm(h->h, M, h->d, h->cfg.rms_eps, h->zeros, 0, 0, 0, h->rowmod, h->u, h->bf16, s,
@@ -461,6 +473,11 @@ rosa_status rosa_prefill_run(rosa_prefill *h, const rosa_prefix_job *jobs, int32
       gq.a = h->u; gq.lda = h->d; gq.a_rows = h->kb_rows; gq.wt = (uint8_t *)h->wt_qkv + (size_t)l * h->qkv_dim * h->d * es;
       gq.M = M; gq.N = h->qkv_dim; gq.K = h->d; gq.epi = kEpiStore; gq.out = h->qkv; gq.ldo = h->qkv_dim;
       e = ptimed(h, pcGemmQKV, [&] { return launch_gemm(gq, h->bf16, s, h->gemm_cfg); });
+      if (e == hipSuccess && h->rope_tab)
+        e = ptimed(h, pcRope, [&] {
+          return launch_prefill_rope(d_jobs, d_rows, M, h->qkv, h->qkv_dim, h->nq + h->nkv, h->hd, h->bf16,
+                                     h->rope_tab, s);
+        });
       if (e != hipSuccess) break;
       if (!h->context) {
         e = ptimed(h, pcScatter, [&] {

@@ -60,7 +60,7 @@ class VlmConfig(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_q_heads", C.c_int32),
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("d_mlp", C.c_int32),
                 ("rms_eps", C.c_float), ("dtype", C.c_int32), ("cache_form", C.c_int32),
-                ("head_layers", C.c_int32)]
+                ("head_layers", C.c_int32), ("rope_base", C.c_float)]
 
 
 _VLM_WEIGHT_FIELDS = ["w_qkv", "w_o", "w_up", "w_down", "w_ctx"]
@@ -470,7 +470,8 @@ def vlm_config(shape, dtype: str, head_layers: int = 0) -> VlmConfig:
     """head_layers > 0: the context cache form for a head of that many layers."""
     return VlmConfig(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
                      shape.d_mlp, shape.rms_eps, ROSA_BF16 if dtype == "bf16" else ROSA_FP32,
-                     ROSA_CACHE_CONTEXT if head_layers > 0 else ROSA_CACHE_PER_LAYER, head_layers)
+                     ROSA_CACHE_CONTEXT if head_layers > 0 else ROSA_CACHE_PER_LAYER, head_layers,
+                     float(getattr(shape, "rope_base", 0.0)))
 
 
 def prefix_job(embeddings, prefix_k, prefix_v, P: int, causal_len: int = 0) -> PrefixJob:

@@ -255,6 +255,10 @@ def test_prefill_create_validates_before_touching_the_gpu():
     bad_layers = rosa.vlm_config(TINY_VLM, "fp32", head_layers=2)
     bad_layers.head_layers = 0
     cases.append(bad_layers)
+    for base in (0.5, 1.0, -1.0, float("inf"), float("nan")):   # rotary base: 0 (none) or > 1
+        bad_rope = rosa.vlm_config(TINY_VLM, "fp32")
+        bad_rope.rope_base = base
+        cases.append(bad_rope)
     for cfg in cases:
         assert lib.rosa_prefill_create(C.byref(cfg), C.byref(w), 1, 8, None, C.byref(h)) == rosa.ROSA_E_INVALID
         assert not h.value and lib.rosa_prefill_last_error(None)

@@ -3,6 +3,8 @@ backbone (Sec. 2.2.1: the VLM's per-layer keys and values are the action
 head's prefix cache): every layer's K and V caches of a ragged batch of jobs,
 element by element, in fp32 and bf16; the caches feeding the action expert
 end to end; the full-size backbone on a sampled job; argument validation."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -23,6 +25,9 @@ TOL = {"fp32": 1e-5, "bf16": 1e-2}
 # Same backbone width and heads as PI0_VLM with two layers: the hd-256 tiles
 # and the 16384-wide MLP at a size the oracle finishes in seconds.
 PI0_VLM_2L = VlmShape(n_layers=2, d_model=2048, n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384)
+# The same backbones with rotary position embedding of queries and keys.
+TINY_VLM_ROPE = dataclasses.replace(TINY_VLM, rope_base=10000.0)
+PI0_VLM_2L_ROPE = dataclasses.replace(PI0_VLM_2L, rope_base=10000.0)
 
 
 def _rosa():
@@ -118,6 +123,22 @@ def test_bf16_pi0_width_causal_segments():
     _check_layers(PI0_VLM_2L, "bf16", w, jobs, range(len(lens)))
 
 
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("causal", [None, [1, 0, 10, 0, 100, 64]])
+def test_rotary_positions_match_oracle(dtype, causal):
+    # positions up to 299 (angles up to 299 rad at the fastest pair), long
+    # jobs key-split in bf16 when no job is causal
+    lens = [1, 5, 37, 130, 300, 64]
+    w, jobs = _run(TINY_VLM_ROPE, dtype, lens, seed=7, causal=causal)
+    _check_layers(TINY_VLM_ROPE, dtype, w, jobs, range(len(lens)))
+
+
+def test_bf16_pi0_width_rotary_positions():
+    lens = [816, 300, 17]
+    w, jobs = _run(PI0_VLM_2L_ROPE, "bf16", lens, seed=8, causal=[48, 0, 0])
+    _check_layers(PI0_VLM_2L_ROPE, "bf16", w, jobs, range(len(lens)))
+
+
 def test_bf16_many_jobs_no_key_split():
     # Enough query blocks that no job's keys are split (one item per block).
     rng = np.random.default_rng(7)
@@ -188,6 +209,7 @@ def _run_context(shape, dtype, lens, head_layers, seed, causal=None):
     (TINY_VLM, "fp32", [1, 37, 300, 64], 2, None),
     (TINY_VLM, "bf16", [1, 37, 300, 64], 3, None),
     (TINY_VLM, "bf16", [1, 37, 300, 64], 2, [1, 0, 120, 9]),
+    (TINY_VLM_ROPE, "fp32", [1, 37, 300, 64], 2, None),
     (PI0_VLM_2L, "bf16", [816, 65], 18, None),
 ])
 def test_context_form_matches_oracle(shape, dtype, lens, head_layers, causal):
