@@ -478,7 +478,7 @@ def summarize_profiles(out):
           f"WRITE_SIZE by {wf:.4f}.", "",
           "| Kernel | Dispatches | FETCH_SIZE (KiB, avg) | WRITE_SIZE (KiB, avg) | HBM read (MB) | HBM write (MB) |",
           "|---|---:|---:|---:|---:|---:|",
-          f"| `rosa::attention_bf16_kernel<256, 1>` | {nf} | {fetch:.1f} | {write:.1f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} |",
+          f"| `rosa::attention_bf16_kernel<256, 1, false>` | {nf} | {fetch:.1f} | {write:.1f} | {rd / 1e6:.1f} | {wr / 1e6:.1f} |",
           *_traffic_rows(out, ff, wf),
           "", f"Per launch: {(rd + wr) / 1e6:.1f} MB of HBM traffic.  Algorithmic bytes per launch (each active "
           "request's prefix K and V of the layer read once) are 174 MB averaged over the 180 launches of one call; "
