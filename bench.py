@@ -329,8 +329,9 @@ def _traffic_rows(out, ff, wf):
 
 
 def _summarize_presets(out):
-    """One line per workload from `bench.py --workload W --no-cpu-baseline`
-    runs whose JSON lines were saved as bench_W.log under `out`."""
+    """One line per workload from `bench.py --workload W` runs whose JSON
+    lines were saved as bench_W.log under `out` (with the oracle's timing on
+    the host cores when the run measured it)."""
     rows = []
     for w in ("factory_b256", "factory_b256_alternating", "pi0_b1", "pi0_b32", "stress_b512"):
         f = f"{out}/bench_{w}.log"
@@ -347,15 +348,17 @@ def _summarize_presets(out):
     lines = ["# Whole-call results per workload (one MI355X, bf16)", "",
              "Commands (repository root, library built in-tree), one per workload:", "", "```",
              "export TMPDIR=/tmp",
-             *[f"timeout -k 10 300 python -u bench.py --workload {w.replace('_alternating', '')} --no-cpu-baseline"
+             *[f"timeout -k 10 400 python -u bench.py --workload {w.replace('_alternating', '')}"
+               + ("" if "cpu_baseline" in j else " --no-cpu-baseline")
                + (" --attention-layout alternating" if w.endswith("_alternating") else "") + f" > {out}/bench_{w}.log"
-               for w, _ in rows],
+               for w, j in rows],
              f"python bench.py --summarize-profiles {out}", "```", "",
              "Each line: 3 warm-up + 20 timed calls; chunks/s = requests x calls / wall time; per-call kernel time "
              "from the library's per-launch events (one extra pass).", "",
              "| Workload | Requests | Action tokens | Prefix tokens | chunks/s | ms per call | p50 ms | p99 ms | "
-             "attention ms/call | GEMMs ms/call | attention GB/s (frac of 8 TB/s) | GEMM TFLOP/s (frac of 2.5 PF) |",
-             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+             "attention ms/call | GEMMs ms/call | attention GB/s (frac of 8 TB/s) | GEMM TFLOP/s (frac of 2.5 PF) | "
+             "oracle chunks/s (host threads) |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     for w, j in rows:
         k = j.get("kernels", {})
         att = k.get("attention", {})
@@ -364,7 +367,13 @@ def _summarize_presets(out):
                      f"{j['config']['prefix_tokens']} | {j['value']} | {j['ms_per_step']} | {j['p50_ms']} | "
                      f"{j['p99_ms']} | {att.get('ms_per_call', 0):.2f} | {gm:.2f} | "
                      f"{att.get('achieved', 0):.0f} ({att.get('frac', 0):.3f}) | "
-                     f"{j['gemm_all']['achieved']} ({j['gemm_all']['frac']:.3f}) |")
+                     f"{j['gemm_all']['achieved']} ({j['gemm_all']['frac']:.3f}) | "
+                     + (f"{j['cpu_baseline']['value']:.3g} ({j['cpu_baseline']['cores']}) |" if "cpu_baseline" in j
+                        else "- |"))
+    samples = [(w, j["cpu_baseline"]["sample"]) for w, j in rows if "cpu_baseline" in j]
+    if samples:
+        lines += ["", "Oracle samples (float64 NumPy on the GPU box's host cores, scaled to the whole batch):"]
+        lines += [f"- {w}: {smp}" for w, smp in samples]
     srcs = {f: hashlib.sha256(open(os.path.join(ROOT, "paper_2607_01088_amd", "csrc", f), "rb").read()).hexdigest()[:16]
             for f in ("k_attn.hip", "k_gemm.hip")}
     lines += ["", "Kernel source sha256 (first 16 hex digits) when measured: " +
