@@ -139,6 +139,21 @@ def test_bf16_pi0_width_rotary_positions():
     _check_layers(PI0_VLM_2L_ROPE, "bf16", w, jobs, range(len(lens)))
 
 
+# Backbones at head_dim 64 (two query heads per KV head, two KV heads) and
+# 128 (three KV heads, one query head each): the other attention tile shapes
+# with causal segments and rotary positions together.
+VLM_HD64 = VlmShape(n_layers=2, d_model=256, n_q_heads=4, n_kv_heads=2, head_dim=64, d_mlp=512, rope_base=10000.0)
+VLM_HD128 = VlmShape(n_layers=2, d_model=384, n_q_heads=3, n_kv_heads=3, head_dim=128, d_mlp=768, rope_base=500.0)
+
+
+@pytest.mark.parametrize("shape", [VLM_HD64, VLM_HD128], ids=["hd64", "hd128"])
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_other_head_dims_causal_and_rotary(shape, dtype):
+    lens = [3, 70, 257, 33]
+    w, jobs = _run(shape, dtype, lens, seed=9, causal=[3, 20, 100, 0])
+    _check_layers(shape, dtype, w, jobs, range(len(lens)))
+
+
 def test_bf16_many_jobs_no_key_split():
     # Enough query blocks that no job's keys are split (one item per block).
     rng = np.random.default_rng(7)
