@@ -381,15 +381,25 @@ def _summarize_presets(out):
     open(os.path.join(PROFILES, "bench_workloads.md"), "w").write("\n".join(lines) + "\n")
 
 
-def _summarize_b1_trace(out):
-    """Per-kernel durations and launch gaps of one single-robot call from a
-    --kernel-trace run of `bench.py --workload pi0_b1` (tr_b1/)."""
+_CALL_TRACES = {
+    # directory under `out`: (file under profiles/, title, bench arguments)
+    "tr_b1": ("kernel_trace_pi0_b1.md", "one single-robot call: pi0_b1 workload (1 request, prefix 816, "
+              "horizon 50, 10 Euler steps, bf16)", "--workload pi0_b1"),
+    "tr_b16": ("kernel_trace_factory_first16.md", "one 16-robot call: the first 16 requests of the factory_b256 "
+               "batch (horizons 16/50, 5/10 Euler steps, bf16)", "--workload factory_b256 --first 16"),
+}
+
+
+def _summarize_call_trace(out, sub):
+    """Per-kernel durations and launch gaps of one timed generate call from a
+    --kernel-trace run of bench.py (`out`/`sub`/)."""
     import collections
-    rows = _csv_rows(f"{out}/tr_b1/**/*kernel_trace.csv")
+    fname, title, bench_args = _CALL_TRACES[sub]
+    rows = _csv_rows(f"{out}/{sub}/**/*kernel_trace.csv")
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     starts = [i for i, r in enumerate(rows) if "time_embedding" in r["Kernel_Name"]]
     if len(starts) < 4:
-        raise SystemExit("tr_b1: fewer than 4 generate calls in the trace")
+        raise SystemExit(f"{sub}: fewer than 4 generate calls in the trace")
     call = rows[starts[2]:starts[3]]              # the first timed call (after 1 warm-up)
     span = (int(call[-1]["End_Timestamp"]) - int(call[0]["Start_Timestamp"])) / 1e3
     dur = collections.defaultdict(list)
@@ -403,25 +413,24 @@ def _summarize_b1_trace(out):
             gap[name].append((t0 - prev_end) / 1e3)
         prev_end = t1
     busy = sum(sum(v) for v in dur.values())
-    lines = ["# Kernel trace of one single-robot call: pi0_b1 workload (1 request, prefix 816, horizon 50, "
-             "10 Euler steps, bf16)", "",
+    lines = [f"# Kernel trace of {title}", "",
              "Command (one MI355X, repository root, library built in-tree):", "", "```",
-             f"export TMPDIR=/tmp; rocprofv3 --kernel-trace --output-format csv -d {out}/tr_b1 -o b1 -- "
-             "python -u bench.py --workload pi0_b1 --steps 3 --warmup 1 --no-cpu-baseline",
+             f"export TMPDIR=/tmp; rocprofv3 --kernel-trace --output-format csv -d {out}/{sub} -o t -- "
+             f"python -u bench.py {bench_args} --steps 3 --warmup 1 --no-cpu-baseline",
              f"python bench.py --summarize-profiles {out}", "```", "",
              f"The first timed call: {len(call)} kernels, {busy / 1e3:.2f} ms of kernel time, {span / 1e3:.2f} ms "
              "from its first kernel's start to its last kernel's end under the tracer (the untraced call takes "
              "about the kernel time: the tracer widens the gaps between dependent launches).  Per layer-step "
-             "(18 layers x 10 steps) the call launches QKV, attention, the merge of split key ranges, the output "
-             "projection's K slices, their reduction fused with the MLP norm, MLP up, MLP down's K slices and "
-             "their reduction fused with the next norm.", "",
+             "the call launches QKV, attention (and, for split key ranges, their merge), the output "
+             "projection, MLP up and MLP down, with the two modulated norms either as launches of their own "
+             "or, after a K-split output or MLP-down projection, fused into its slice reduction.", "",
              "| Kernel | Launches | Avg (us) | Min (us) | Total (ms) | Avg gap before (us) |",
              "|---|---:|---:|---:|---:|---:|"]
     for name, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
         g = gap.get(name, [])
         lines.append(f"| `{name}` | {len(v)} | {sum(v) / len(v):.2f} | {min(v):.2f} | {sum(v) / 1e3:.3f} | "
                      f"{(sum(g) / len(g)) if g else 0.0:.2f} |")
-    open(os.path.join(PROFILES, "kernel_trace_pi0_b1.md"), "w").write("\n".join(lines) + "\n")
+    open(os.path.join(PROFILES, fname), "w").write("\n".join(lines) + "\n")
 
 
 def summarize_profiles(out):
@@ -436,8 +445,9 @@ def summarize_profiles(out):
         _summarize_prefill(out)
     if glob.glob(f"{out}/pmc_util/**/*counter_collection.csv", recursive=True):
         _summarize_pmc(out)
-    if glob.glob(f"{out}/tr_b1/**/*kernel_trace.csv", recursive=True):
-        _summarize_b1_trace(out)
+    for sub in _CALL_TRACES:
+        if glob.glob(f"{out}/{sub}/**/*kernel_trace.csv", recursive=True):
+            _summarize_call_trace(out, sub)
     _summarize_presets(out)
     if not glob.glob(f"{out}/prof_factory/**/*kernel_stats.csv", recursive=True):
         return
@@ -930,6 +940,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="factory_b256")
+    ap.add_argument("--first", type=int, default=0, metavar="N",
+                    help="only the first N requests of the workload (a smaller batch of the same mix)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lanes", type=int, default=0,
@@ -995,6 +1007,9 @@ def main():
     weights = make_weights(preset.shape, preset.dtype)
     meta = make_metadata(preset)
     reqs = make_requests(preset, threads=16)
+    if args.first > 0:
+        reqs, meta = reqs[:args.first], meta[:args.first]
+        workload += f"_first{args.first}"
     print(f"[bench] generated inputs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
     cap = rosa.capacity(len(reqs), max(r.horizon for r in reqs), sum(r.horizon for r in reqs),
                         max(r.steps for r in reqs), sum(r.prefix_len for r in reqs))
