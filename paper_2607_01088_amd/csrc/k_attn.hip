@@ -532,13 +532,15 @@ __global__ void __launch_bounds__(256, 2) attention_bf16_kernel(AttnArgs a) {
     const int loc = 32 * (wave + 4 * g) + (lane & 31);
     if (loc >= it.nq) continue;
     if (it.slot >= 0) {
-      float *po = a.part_o + ((size_t)it.slot * kAttnQB + loc) * HD;
+      bf16 *po = reinterpret_cast<bf16 *>(a.part_o) + ((size_t)it.slot * kAttnQB + loc) * HD;
 #pragma unroll
       for (int n = 0; n < NT; ++n)
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const float4 v = make_float4(o[g][n][rg * 4 + 0], o[g][n][rg * 4 + 1], o[g][n][rg * 4 + 2], o[g][n][rg * 4 + 3]);
-          *reinterpret_cast<float4 *>(po + n * 32 + rg * 8 + half * 4) = v;
+          bf16x4 v;
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) v[e2] = (bf16)o[g][n][rg * 4 + e2];
+          *reinterpret_cast<bf16x4 *>(po + n * 32 + rg * 8 + half * 4) = v;
         }
       if (half == 0) {
         float *pm = a.part_ml + ((size_t)it.slot * kAttnQB + loc) * 2;
@@ -617,7 +619,7 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnArgs a) {
 template <typename OutT>
 __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__restrict__ groups,
                                                          const ReqDesc *__restrict__ reqs,
-                                                         const float *__restrict__ part_o,
+                                                         const bf16 *__restrict__ part_o,
                                                          const float *__restrict__ part_ml, OutT *o,
                                                          int ldo, int nq, int nkv, int hd, int o_rows) {
   const AttnGroup gr = groups[blockIdx.y];
@@ -630,8 +632,10 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
   const int qt = qrow / G, qg = gr.kvh * G + qrow % G;
   // Partials are read CH slots at a time, every load of a batch in flight
   // together; they are combined in slot order, as one slot at a time would.
+  // Lane holds head-dim elements 4 lane .. 4 lane + 3 (head_dim <= 256).
   constexpr int CH = 8;
-  constexpr int kMaxE = 256 / 64;             // head-dim elements per lane (head_dim <= 256)
+  const int e0 = lane * 4;
+  const bool on = e0 < hd;
   const float2 *ml = reinterpret_cast<const float2 *>(part_ml);
   float mx = -INFINITY;
   for (int c0 = 0; c0 < gr.n; c0 += CH) {
@@ -643,19 +647,16 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
     for (int c = 0; c < CH; ++c) mx = fmaxf(mx, m[c]);
   }
   float L = 0.f;
-  float acc[kMaxE];
-#pragma unroll
-  for (int j = 0; j < kMaxE; ++j) acc[j] = 0.f;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < gr.n; c0 += CH) {
     float2 p[CH];
-    float ov[CH][kMaxE];
+    bf16x4 ov[CH];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
       const size_t base = (size_t)(gr.first_slot + c0 + c) * kAttnQB + qloc;
       const bool live = c0 + c < gr.n;
       p[c] = live ? ml[base] : make_float2(0.f, 0.f);
-#pragma unroll
-      for (int j = 0; j < kMaxE; ++j) ov[c][j] = live && lane + 64 * j < hd ? part_o[base * hd + lane + 64 * j] : 0.f;
+      ov[c] = live && on ? *reinterpret_cast<const bf16x4 *>(part_o + base * hd + e0) : bf16x4{};
     }
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
@@ -663,18 +664,17 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
       const float wgt = exp2f(p[c].x - mx);
       L += wgt * p[c].y;
 #pragma unroll
-      for (int j = 0; j < kMaxE; ++j) acc[j] += wgt * ov[c][j];
+      for (int j = 0; j < 4; ++j) acc[j] += wgt * (float)ov[c][j];
     }
   }
+  if (!on) return;
   const float inv = 1.0f / L;
-  const size_t orow = (size_t)(tok_off + qt);
+  const size_t orow = (size_t)(tok_off + qt), col = (size_t)qg * hd + e0;
+  OutT *dst = o + (o_rows > 0 ? kb32_offset(o_rows, orow, col) : orow * ldo + col);
 #pragma unroll
-  for (int j = 0; j < kMaxE; ++j)
-    if (lane + 64 * j < hd) {
-      const size_t col = (size_t)qg * hd + lane + 64 * j;
-      o[o_rows > 0 ? kb32_offset(o_rows, orow, col) : orow * ldo + col] = from_f32<OutT>(acc[j] * inv);
-    }
+  for (int j = 0; j < 4; ++j) dst[j] = from_f32<OutT>(acc[j] * inv);
 }
+
 
 hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
   if (a.n_items <= 0) return hipSuccess;
@@ -715,17 +715,17 @@ hipError_t launch_attention(const AttnArgs &a, bool bf16_mode, hipStream_t s) {
 }
 
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
-                             const float *part_o, const float *part_ml, void *o, int ldo, int nq,
+                             const void *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16_mode, hipStream_t s, int o_rows) {
   if (n_groups <= 0) return hipSuccess;
   if (hd > 256) return hipErrorInvalidValue;   // a lane holds at most 4 head-dim elements
   if (o_rows > 0 && !bf16_mode) return hipErrorInvalidValue;
   dim3 grid(kAttnQB / 4, n_groups);
   if (bf16_mode)
-    hipLaunchKernelGGL(attn_merge_kernel<bf16>, grid, dim3(256), 0, s, groups, reqs, part_o, part_ml,
+    hipLaunchKernelGGL(attn_merge_kernel<bf16>, grid, dim3(256), 0, s, groups, reqs, (const bf16 *)part_o, part_ml,
                        (bf16 *)o, ldo, nq, nkv, hd, o_rows);
   else
-    hipLaunchKernelGGL(attn_merge_kernel<float>, grid, dim3(256), 0, s, groups, reqs, part_o, part_ml,
+    hipLaunchKernelGGL(attn_merge_kernel<float>, grid, dim3(256), 0, s, groups, reqs, (const bf16 *)part_o, part_ml,
                        (float *)o, ldo, nq, nkv, hd, 0);
   return hipGetLastError();
 }

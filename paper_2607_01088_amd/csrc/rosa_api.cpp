@@ -1328,7 +1328,7 @@ rosa_status rosa_attention_noalloc(const rosa_model_config *cfg, const rosa_requ
     a.layer = layer;
     a.qkv = qkv; a.ldqkv = D.qkv_dim; a.o = o; a.ldo = D.o_dim;
     a.nq = D.nq; a.nkv = D.nkv; a.hd = D.hd;
-    a.part_o = reinterpret_cast<float *>(sp + kNaOffO);
+    a.part_o = sp + kNaOffO;
     a.part_ml = reinterpret_cast<float *>(sp + kNaOffMl);
     e = launch_attention(a, bf16, stream);
     if (e == hipSuccess && !S.groups.empty())

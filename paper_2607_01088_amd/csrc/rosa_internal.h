@@ -207,7 +207,7 @@ struct AttnArgs {
   void *o; int ldo;                // o at column g*hd
   int o_rows;                      // bf16: 0 row-major (ldo), else kb32 planes of o_rows rows
   int nq, nkv, hd;
-  float *part_o;                   // [slot][kAttnQB][hd] fp32
+  void *part_o;                    // [slot][kAttnQB][hd] bf16 (unnormalised O of split items)
   float *part_ml;                  // [slot][kAttnQB][2] fp32 (running max in log2 units, sum)
   // 1: every item's causal_b masks keys per query token (the prefix
   // producer's causal segments); such items are never key-split.
@@ -238,7 +238,7 @@ inline hipError_t upload_gemm_weights(void *dst, const float *src, int L, int K,
 void attn_order_items(const std::vector<AttnItem> &items, const int32_t *order, const int32_t *next, size_t n,
                       AttnItem *dst);
 hipError_t launch_attn_merge(const AttnGroup *groups, int n_groups, const ReqDesc *reqs,
-                             const float *part_o, const float *part_ml, void *o, int ldo, int nq,
+                             const void *part_o, const float *part_ml, void *o, int ldo, int nq,
                              int nkv, int hd, bool bf16, hipStream_t s, int o_rows = 0);
 
 }  // namespace rosa
