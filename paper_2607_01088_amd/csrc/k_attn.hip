@@ -615,7 +615,8 @@ __global__ void __launch_bounds__(256) attention_f32_kernel(AttnArgs a) {
 
 // ------------------------------------------------------------------ merge of split-key partials
 // One wave per query row of a split group: combine the group's partials in
-// slot order: m = max_c m_c, w_c = 2^(m_c - m), o = sum_c w_c O_c / sum_c w_c l_c.
+// slot order: m = max_c m_c, w_c = 2^(m_c - m), o = sum_c w_c O_c / sum_c w_c l_c
+// (O_c in bf16, m_c and l_c in fp32).
 template <typename OutT>
 __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__restrict__ groups,
                                                          const ReqDesc *__restrict__ reqs,
@@ -630,23 +631,16 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
   const int tok_off = reqs[gr.req].tok_off;   // issued now, used for the store
   const int qrow = gr.q0 + qloc;
   const int qt = qrow / G, qg = gr.kvh * G + qrow % G;
-  // Partials are read CH slots at a time, every load of a batch in flight
-  // together; they are combined in slot order, as one slot at a time would.
+  // Partials are read CH slots at a time (their max and sum with their O),
+  // every load of a batch in flight together, so a group of at most CH
+  // slots costs one round trip; batches combine in slot order against a
+  // running max (the sums so far rescaled when a later batch raises it).
   // Lane holds head-dim elements 4 lane .. 4 lane + 3 (head_dim <= 256).
   constexpr int CH = 8;
   const int e0 = lane * 4;
   const bool on = e0 < hd;
   const float2 *ml = reinterpret_cast<const float2 *>(part_ml);
-  float mx = -INFINITY;
-  for (int c0 = 0; c0 < gr.n; c0 += CH) {
-    float m[CH];
-#pragma unroll
-    for (int c = 0; c < CH; ++c)
-      m[c] = c0 + c < gr.n ? ml[(size_t)(gr.first_slot + c0 + c) * kAttnQB + qloc].x : -INFINITY;
-#pragma unroll
-    for (int c = 0; c < CH; ++c) mx = fmaxf(mx, m[c]);
-  }
-  float L = 0.f;
+  float mx = -INFINITY, L = 0.f;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < gr.n; c0 += CH) {
     float2 p[CH];
@@ -655,17 +649,25 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const AttnGroup *__rest
     for (int c = 0; c < CH; ++c) {
       const size_t base = (size_t)(gr.first_slot + c0 + c) * kAttnQB + qloc;
       const bool live = c0 + c < gr.n;
-      p[c] = live ? ml[base] : make_float2(0.f, 0.f);
+      p[c] = live ? ml[base] : make_float2(-INFINITY, 0.f);
       ov[c] = live && on ? *reinterpret_cast<const bf16x4 *>(part_o + base * hd + e0) : bf16x4{};
     }
+    float nm = mx;
+#pragma unroll
+    for (int c = 0; c < CH; ++c) nm = fmaxf(nm, p[c].x);
+    const float sc = exp2f(mx - nm);          // 0 on the first batch (mx = -inf)
+    L *= sc;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] *= sc;
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
       if (c0 + c >= gr.n) break;
-      const float wgt = exp2f(p[c].x - mx);
+      const float wgt = exp2f(p[c].x - nm);
       L += wgt * p[c].y;
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[j] += wgt * (float)ov[c][j];
     }
+    mx = nm;
   }
   if (!on) return;
   const float inv = 1.0f / L;
