@@ -184,7 +184,8 @@ def _classify_dispatches(rows):
     the expert launches modnorm, the QKV projection, attention (and, for split
     keys, the merge), the output projection, modnorm, MLP up, MLP down; a split
     product's reduce kernel belongs to the projection before it, and when that
-    reduce also takes the following norm, no modnorm launch follows."""
+    reduce also takes the following norm, or an unsplit output projection or
+    MLP-down defers it to the next product, no modnorm launch follows."""
     names = {}
     for r in rows:
         names[int(r["Dispatch_Id"])] = r["Kernel_Name"]

@@ -238,8 +238,10 @@ __device__ __forceinline__ void gemm_mainloop(const GemmArgs &g, int m0, int n0,
 }
 
 // Epilogue of the tile at (m0, n0) from acc; stages through the ring's LDS,
-// which must be free (gemm_mainloop ends that way).
-template <typename T, int EPI>
+// which must be free (gemm_mainloop ends that way).  DN: the deferred norm's
+// part of the epilogue (outputs t and the row sums of squares after a gated
+// residual; the norm's completion before a bf16 store).
+template <typename T, int EPI, bool DN = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0, uint8_t *L,
                                               f32x16 (&acc)[T::MBW][T::TN]) {
   constexpr int MBW = T::MBW, TN = T::TN;
@@ -281,8 +283,12 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
     // just before use).
     constexpr int Q = MBW * TN;
     constexpr bool kTwoBlocks = T::NST * T::SBYTES <= 80 * 1024;
-    constexpr int NB = (EPI == kEpiGatedResidual && T::NW < 16 && !kTwoBlocks) ? 2 : 1;
+    constexpr int NB = (EPI == kEpiGatedResidual && T::NW < 16 && !kTwoBlocks && !DN) ? 2 : 1;
     float4 hv[NB][4], gt[NB][4];
+    // The deferred norm's scale rows load with the tile's other rows, except in
+    // 16-wave tiles (no registers to spare), which load them at use.
+    constexpr bool kScvAhead = DN && T::NW < 16;
+    float4 scv[kScvAhead ? NB : 1][4];
     const int col0 = (lane & 7) * 4;
     auto load_rows = [&](int q, int buf) __attribute__((always_inline)) {
       const int i = q / TN, j = q % TN;
@@ -294,6 +300,10 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
           hv[buf][p] = *reinterpret_cast<const float4 *>(H + (size_t)row * g.ldo + col);
           if constexpr (kHoist) gt[buf][p] = *reinterpret_cast<const float4 *>(g.gate + goff[i][p] + col);
           else gt[buf][p] = *reinterpret_cast<const float4 *>(g.gate + (size_t)g.rowmod[row] * g.gate_stride + col);
+          if constexpr (kScvAhead) {
+            if constexpr (kHoist) scv[buf][p] = *reinterpret_cast<const float4 *>(g.dscale + goff[i][p] + col);
+            else scv[buf][p] = *reinterpret_cast<const float4 *>(g.dscale + (size_t)g.rowmod[row] * g.gate_stride + col);
+          }
         }
       }
     };
@@ -321,6 +331,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         const int row = rb + 8 * p + (lane >> 3);
+        float q2 = 0.f;
         if (row < g.M && col < g.N) {
           if constexpr (EPI == kEpiPartial) {
             *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = v[p];
@@ -331,7 +342,27 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
             h.z = h.z + gt[buf][p].z * v[p].z;
             h.w = h.w + gt[buf][p].w * v[p].w;
             *reinterpret_cast<float4 *>(H + (size_t)row * g.ldo + col) = h;
+            if constexpr (DN) {
+              float4 sc;
+              if constexpr (kScvAhead) sc = scv[buf][p];
+              else sc = *reinterpret_cast<const float4 *>(g.dscale + (size_t)g.rowmod[row] * g.gate_stride + col);
+              bf16x4 tv;
+              tv[0] = (bf16)(h.x * (1.0f + sc.x));
+              tv[1] = (bf16)(h.y * (1.0f + sc.y));
+              tv[2] = (bf16)(h.z * (1.0f + sc.z));
+              tv[3] = (bf16)(h.w * (1.0f + sc.w));
+              *reinterpret_cast<bf16x4 *>(reinterpret_cast<bf16 *>(g.dt) + kb32_offset(g.dt_rows, row, col)) = tv;
+              q2 = fmaf(h.w, h.w, fmaf(h.z, h.z, fmaf(h.y, h.y, h.x * h.x)));
+            }
           }
+        }
+        if constexpr (DN) {
+          // The row's 32 columns of this tile sit on the 8 lanes lane / 8
+          // shares; their sum (fixed butterfly order) goes to the row's entry.
+          q2 += __shfl_xor(q2, 1, 64);
+          q2 += __shfl_xor(q2, 2, 64);
+          q2 += __shfl_xor(q2, 4, 64);
+          if ((lane & 7) == 0 && row < g.M && col < g.N) g.dss[(size_t)row * (g.N >> 5) + (col >> 5)] = q2;
         }
       }
     }
@@ -339,16 +370,70 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
     // Each wave stages one 32 x 32 tile at a time in its own 4 KB slot, then
     // reads it back row-contiguous.
     uint8_t *stg = L + wave * 4096;
+    // Deferred norm: 1 / rms of this lane's row in each row block, its sum of
+    // squares taken over the two lane halves (each half sums its share of the
+    // row's block sums in order; the halves' totals are then added).
+    // The shift rows of every column this lane stores are loaded here too, all
+    // before the first store (the stores could alias them for the compiler);
+    // 16-wave tiles (no registers to spare) load each 32 x 32 tile's before it.
+    constexpr bool kShAll = DN && T::NW < 16;
+    float rinv[DN ? MBW : 1];
+    int mrow[DN ? MBW : 1];
+    f32x4 shv[kShAll ? MBW : 1][kShAll ? TN : 1][4];
+    auto load_shift = [&](int i, int j, f32x4 (&dst)[4]) __attribute__((always_inline)) {
+      const float *shrow = g.cshift + (size_t)mrow[i] * g.cshift_stride;
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int c4 = n0 + (wn * TN + j) * 32 + 8 * gq + 4 * half;
+        dst[gq] = c4 < g.N ? *reinterpret_cast<const f32x4 *>(shrow + c4) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+    if constexpr (DN) {
+      // Every load is issued before the first sum (cparts = 8 nv, nv <= 4).
+      const int nv = g.cparts >> 3;
+      f32x4 pv[MBW][4];
+#pragma unroll
+      for (int i = 0; i < MBW; ++i) {
+        const int row = min(m0 + (wm * MBW + i) * 32 + r32, g.M - 1);
+        const f32x4 *sp = reinterpret_cast<const f32x4 *>(g.css + (size_t)row * g.cparts) + half * nv;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (v < nv) pv[i][v] = sp[v];
+        mrow[i] = g.rowmod[row];
+        if constexpr (kShAll) {
+#pragma unroll
+          for (int j = 0; j < TN; ++j) load_shift(i, j, shv[i][j]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < MBW; ++i) {
+        float ss = 0.f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (v < nv) ss = (((ss + pv[i][v][0]) + pv[i][v][1]) + pv[i][v][2]) + pv[i][v][3];
+        ss += __shfl_xor(ss, 32, 64);
+        rinv[i] = 1.0f / sqrtf(ss / (float)g.cd + g.ceps);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < MBW; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int rb = m0 + (wm * MBW + i) * 32, cb = n0 + (wn * TN + j) * 32;
+        f32x4 sh1[4];
+        if constexpr (DN && !kShAll) load_shift(i, j, sh1);
         // bf16 slot: 32 rows x 4 chunks of 16 B (8 bf16), chunk c of row r at
         // c ^ ((r / 4) % 4); this lane's 4 values are half `half` of chunk gq.
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
           float a0 = acc[i][j][4 * gq], a1 = acc[i][j][4 * gq + 1], a2 = acc[i][j][4 * gq + 2], a3 = acc[i][j][4 * gq + 3];
+          if constexpr (DN) {
+            const f32x4 sh = kShAll ? shv[kShAll ? i : 0][kShAll ? j : 0][gq] : sh1[gq];
+            a0 = fmaf(a0, rinv[i], sh[0]);
+            a1 = fmaf(a1, rinv[i], sh[1]);
+            a2 = fmaf(a2, rinv[i], sh[2]);
+            a3 = fmaf(a3, rinv[i], sh[3]);
+          }
           if constexpr (EPI == kEpiGelu) {
             a0 = gelu_tanh_f(a0); a1 = gelu_tanh_f(a1); a2 = gelu_tanh_f(a2); a3 = gelu_tanh_f(a3);
           }
@@ -372,7 +457,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs &g, int m0, int n0,
   }
 }
 
-template <typename T, int EPI>
+template <typename T, int EPI, bool DN = false>
 __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, int nct, int ksplit) {
   constexpr int SBYTES = T::SBYTES;
   __shared__ __attribute__((aligned(1024))) uint8_t L[T::NST * SBYTES];
@@ -396,7 +481,7 @@ __global__ void __launch_bounds__(T::NT) gemm_bf16_kernel(GemmArgs g, int nrt, i
     gp.ldo = g.N;
     gemm_epilogue<T, EPI>(gp, m0, n0, L, acc);
   } else {
-    gemm_epilogue<T, EPI>(g, m0, n0, L, acc);
+    gemm_epilogue<T, EPI, DN>(g, m0, n0, L, acc);
   }
 }
 
@@ -555,9 +640,11 @@ static bool fusable_norm(const GemmArgs &g, const NormArgs *nm) {
 
 template <typename T>
 static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split, const NormArgs *nm,
-                              bool *normed) {
+                              bool *normed, bool *deferred) {
   const int nrt = (g.M + T::BM - 1) / T::BM, nct = (g.N + T::BN - 1) / T::BN;
-  const int ks = allow_split ? gemm_split_count(g, nrt * nct, T::BK, fusable_norm(g, nm)) : 1;
+  // A launch that completes a deferred norm is never split.
+  const bool completes = g.css && (g.epi == kEpiStore || g.epi == kEpiGelu);
+  const int ks = allow_split && !completes ? gemm_split_count(g, nrt * nct, T::BK, fusable_norm(g, nm)) : 1;
   dim3 grid((nrt * nct * ks + 7) / 8 * 8);
   if (ks > 1) {
     hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiPartial>), grid, dim3(T::NT), 0, s, g, nrt, nct, ks);
@@ -581,6 +668,16 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split
     }
     return hipGetLastError();
   }
+  if (g.dt && g.epi == kEpiGatedResidual) {
+    hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGatedResidual, true>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1);
+    if (deferred) *deferred = true;
+    return hipGetLastError();
+  }
+  if (completes) {
+    if (g.epi == kEpiGelu) hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu, true>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1);
+    else hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore, true>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1);
+    return hipGetLastError();
+  }
   switch (g.epi) {
     case kEpiStore: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiStore>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1); break;
     case kEpiGelu: hipLaunchKernelGGL((gemm_bf16_kernel<T, kEpiGelu>), grid, dim3(T::NT), 0, s, g, nrt, nct, 1); break;
@@ -590,25 +687,109 @@ static hipError_t launch_tile(const GemmArgs &g, hipStream_t s, bool allow_split
 }
 
 static hipError_t launch_cfg(const GemmArgs &g, int cfg, hipStream_t s, bool allow_split,
-                             const NormArgs *nm = nullptr, bool *normed = nullptr) {
+                             const NormArgs *nm = nullptr, bool *normed = nullptr, bool *deferred = nullptr) {
   if (g.M <= 0) return hipSuccess;
   if (g.K % 128 != 0 || g.N % 8 != 0 || g.a_rows < g.M) return hipErrorInvalidValue;
   switch (cfg) {
-    case 0: return launch_tile<Cfg0>(g, s, allow_split, nm, normed);
-    case 1: return launch_tile<Cfg1>(g, s, allow_split, nm, normed);
-    case 2: return launch_tile<Cfg2>(g, s, allow_split, nm, normed);
-    case 3: return launch_tile<Cfg3>(g, s, allow_split, nm, normed);
-    case 4: return launch_tile<Cfg4>(g, s, allow_split, nm, normed);
-    case 5: return launch_tile<Cfg5>(g, s, allow_split, nm, normed);
-    case 6: return launch_tile<Cfg6>(g, s, allow_split, nm, normed);
-    case 7: return launch_tile<Cfg7>(g, s, allow_split, nm, normed);
-    case 8: return launch_tile<Cfg8>(g, s, allow_split, nm, normed);
-    case 9: return launch_tile<Cfg9>(g, s, allow_split, nm, normed);
-    case 10: return launch_tile<Cfg10>(g, s, allow_split, nm, normed);
-    case 11: return launch_tile<Cfg11>(g, s, allow_split, nm, normed);
-    case 12: return launch_tile<Cfg12>(g, s, allow_split, nm, normed);
+    case 0: return launch_tile<Cfg0>(g, s, allow_split, nm, normed, deferred);
+    case 1: return launch_tile<Cfg1>(g, s, allow_split, nm, normed, deferred);
+    case 2: return launch_tile<Cfg2>(g, s, allow_split, nm, normed, deferred);
+    case 3: return launch_tile<Cfg3>(g, s, allow_split, nm, normed, deferred);
+    case 4: return launch_tile<Cfg4>(g, s, allow_split, nm, normed, deferred);
+    case 5: return launch_tile<Cfg5>(g, s, allow_split, nm, normed, deferred);
+    case 6: return launch_tile<Cfg6>(g, s, allow_split, nm, normed, deferred);
+    case 7: return launch_tile<Cfg7>(g, s, allow_split, nm, normed, deferred);
+    case 8: return launch_tile<Cfg8>(g, s, allow_split, nm, normed, deferred);
+    case 9: return launch_tile<Cfg9>(g, s, allow_split, nm, normed, deferred);
+    case 10: return launch_tile<Cfg10>(g, s, allow_split, nm, normed, deferred);
+    case 11: return launch_tile<Cfg11>(g, s, allow_split, nm, normed, deferred);
+    case 12: return launch_tile<Cfg12>(g, s, allow_split, nm, normed, deferred);
     default: return hipErrorInvalidValue;
   }
+}
+
+static int device_cu_count();
+
+// Whether launch_gemm(g, true, s, force_cfg, then_norm) with g.dt set takes
+// the deferred norm (an unsplit gated-residual launch) for these sizes.
+bool gemm_defers(const GemmArgs &g, int force_cfg, const NormArgs *then_norm) {
+  if (g.M <= 0 || g.epi != kEpiGatedResidual) return false;
+  if (force_cfg >= 0) return true;
+  const int c = gemm_pick_config(g.M, g.N, g.K, g.epi, device_cu_count());
+  const int n_tiles = ((g.M + kCfgs[c].bm - 1) / kCfgs[c].bm) * ((g.N + kCfgs[c].bn - 1) / kCfgs[c].bn);
+  return gemm_split_count(g, n_tiles, kCfgs[c].bk, fusable_norm(g, then_norm)) == 1;
+}
+
+// Shift halves of deferred norms: one thread per output column of one layer's
+// product, for up to kShiftRows modulation rows at a time; the rows' shift
+// vectors pass through LDS kShiftK values of K at a time (K-major, so one
+// 16-byte read serves four rows).  Column n of a kb32 weight holds its K
+// values in 64-byte runs, one per 32 of K.
+constexpr int kShiftRows = 16, kShiftK = 256;
+__global__ void __launch_bounds__(256) shift_proj_kernel(const float *__restrict__ modtab, int mod_stride, int n_mod,
+                                                         int layer_stride, int q_off, int u_off, int d,
+                                                         const bf16 *__restrict__ wq, int Nq,
+                                                         const bf16 *__restrict__ wu, int Nu, int nbq,
+                                                         float *__restrict__ S) {
+  __shared__ __attribute__((aligned(16))) float sh[kShiftK][kShiftRows];
+  const int l = blockIdx.y, r0 = blockIdx.z * kShiftRows, nr = min(kShiftRows, n_mod - r0);
+  const bool isq = (int)blockIdx.x < nbq;
+  const int col = (isq ? (int)blockIdx.x : (int)blockIdx.x - nbq) * 256 + threadIdx.x;
+  const int N = isq ? Nq : Nu, off = isq ? q_off : u_off;
+  const bf16 *W = (isq ? wq : wu) + (size_t)l * N * d;
+  float acc[kShiftRows];
+#pragma unroll
+  for (int r = 0; r < kShiftRows; ++r) acc[r] = 0.f;
+  for (int k0 = 0; k0 < d; k0 += kShiftK) {
+    const int kn = min(kShiftK, d - k0);
+    __syncthreads();                        // the previous chunk's reads are done
+    for (int i = threadIdx.x; i < kShiftK * kShiftRows; i += 256) {
+      const int k = i / kShiftRows, r = i % kShiftRows;
+      sh[k][r] = (r < nr && k < kn) ? modtab[(size_t)(r0 + r) * mod_stride + (size_t)l * layer_stride + off + k0 + k]
+                                    : 0.f;
+    }
+    __syncthreads();
+    if (col < N) {
+      for (int kb = 0; kb < kn; kb += 32) {
+        const bf16 *wp = W + ((size_t)((k0 + kb) >> 5) * N + col) * 32;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const bf16x8 w8 = *reinterpret_cast<const bf16x8 *>(wp + 8 * c);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float w = (float)w8[e];
+            const float4 *sv = reinterpret_cast<const float4 *>(&sh[kb + 8 * c + e][0]);
+#pragma unroll
+            for (int r4 = 0; r4 < kShiftRows / 4; ++r4) {
+              const float4 v = sv[r4];
+              acc[4 * r4] = fmaf(v.x, w, acc[4 * r4]);
+              acc[4 * r4 + 1] = fmaf(v.y, w, acc[4 * r4 + 1]);
+              acc[4 * r4 + 2] = fmaf(v.z, w, acc[4 * r4 + 2]);
+              acc[4 * r4 + 3] = fmaf(v.w, w, acc[4 * r4 + 3]);
+            }
+          }
+        }
+      }
+    }
+  }
+  if (col < N) {
+    const int Nt = Nq + Nu;
+#pragma unroll
+    for (int r = 0; r < kShiftRows; ++r)
+      if (r < nr) S[((size_t)l * n_mod + r0 + r) * Nt + (isq ? 0 : Nq) + col] = acc[r];
+  }
+}
+
+hipError_t launch_shift_proj(const float *modtab, int mod_stride, int n_mod, int L, int layer_stride, int q_off,
+                             int u_off, int d, const void *wq, int Nq, const void *wu, int Nu, float *S,
+                             hipStream_t s) {
+  if (n_mod <= 0 || L <= 0) return hipSuccess;
+  if (d % 32 != 0 || Nq <= 0 || Nu <= 0) return hipErrorInvalidValue;
+  const int nbq = (Nq + 255) / 256, nbu = (Nu + 255) / 256;
+  const dim3 grid(nbq + nbu, L, (n_mod + kShiftRows - 1) / kShiftRows);
+  hipLaunchKernelGGL(shift_proj_kernel, grid, dim3(256), 0, s, modtab, mod_stride, n_mod, layer_stride, q_off, u_off,
+                     d, reinterpret_cast<const bf16 *>(wq), Nq, reinterpret_cast<const bf16 *>(wu), Nu, nbq, S);
+  return hipGetLastError();
 }
 
 // A forced configuration never splits K: every configuration then computes
@@ -699,14 +880,18 @@ static int device_cu_count() {
 }
 
 hipError_t launch_gemm(const GemmArgs &g, bool bf16_mode, hipStream_t s, int force_cfg, const NormArgs *then_norm,
-                       bool *normed) {
+                       bool *normed, bool *deferred) {
   if (normed) *normed = false;
+  if (deferred) *deferred = false;
   if (g.M <= 0) return hipSuccess;
   if (bf16_mode) {
     const int n_cu = device_cu_count();
-    if (force_cfg >= 0) return launch_cfg(g, force_cfg, s, false);
-    return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true, then_norm, normed);
+    if ((g.dt || g.css) && (g.N % 32 != 0 || (g.css && (g.cparts <= 0 || g.cparts % 8 || g.cparts > 32 || g.cd <= 0))))
+      return hipErrorInvalidValue;
+    if (force_cfg >= 0) return launch_cfg(g, force_cfg, s, false, nullptr, nullptr, deferred);
+    return launch_cfg(g, gemm_pick_config(g.M, g.N, g.K, g.epi, n_cu), s, true, then_norm, normed, deferred);
   }
+  if (g.dt || g.css) return hipErrorInvalidValue;   // bf16 only
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64);
   switch (g.epi) {
     case kEpiStore: hipLaunchKernelGGL(gemm_f32_kernel<kEpiStore>, grid, dim3(256), 0, s, g); break;

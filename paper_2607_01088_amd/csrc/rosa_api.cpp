@@ -18,6 +18,11 @@
 
 using namespace rosa;
 
+// Most rows a lane-step may have for its unsplit output projection and
+// MLP-down to defer their norms to the next product.  Above it a separate
+// norm launch costs less than the completing products' longer epilogues.
+constexpr int kDeferMaxRows = 1024;
+
 // Attention launch order.  The kernel's blocks are persistent: block b runs
 // the items of its own list one after another, and blocks reach the 8 XCDs
 // round-robin (block b on XCD b % 8).  Two levels of longest-processing-time
@@ -256,6 +261,10 @@ struct rosa_batch {
   float *part_o = nullptr, *part_ml = nullptr;
   float *gemm_part = nullptr;        // K-slice products of split projections (one lane only)
   size_t gemm_part_floats = 0;
+  // bf16 deferred norms (unsplit output projection and MLP-down): per row the
+  // sums of squares of h over its 32-column blocks, and the norms' shift
+  // vectors multiplied by W_qkv and W_up, [L][modulation row][qkv_dim + dff].
+  float *dn_ss = nullptr, *dn_shift = nullptr;
   int max_items = 0;                 // attention work items per call, both sets
   int max_slots = 0;                 // partial-result slots per call, both sets
 
@@ -867,6 +876,10 @@ rosa_status rosa_batch_create(const rosa_model_config *cfg, const rosa_weights *
                                                      (size_t)16 << 20)
                                   : 0;
     if (b->gemm_part_floats) b->gemm_part = dalloc<float>(b, b->gemm_part_floats, e);
+    if (b->bf16) {
+      b->dn_ss = dalloc<float>(b, maxM * (D.d / 32), e);
+      b->dn_shift = dalloc<float>(b, (size_t)D.L * kMaxTau * (D.qkv_dim + D.dff), e);
+    }
     b->part_o = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * D.hd, e);
     b->part_ml = dalloc<float>(b, (size_t)b->max_slots * kAttnQB * 2, e);
 
@@ -974,9 +987,35 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
       e = timed(b, kcSetup, [&] {
         return launch_setup_rows(d_reqs, n, d_tau_idx, p.Kmax, D.A, b->row_req, b->rowmod, p.M0, b->x, b->stream);
       });
+    const int nl = (int)p.lanes.size();
+    // Deferred norms: every unsplit output projection and MLP-down leaves t
+    // and the row sums of squares for the next product, which completes the
+    // norm; the shift halves are computed once per call, when some launch of
+    // the call takes that path.
+    const int n_tau = (int)p.taus.size();
+    bool defer_on = false;
+    if (b->bf16 && b->dn_ss && b->kb_rows > 0 && D.d % 256 == 0 && D.d <= 1024) {
+      for (const Plan::Lane &ln : p.lanes)
+        for (int k = 0; k < p.Kmax && !defer_on; ++k) {
+          if (ln.m[k] == 0 || ln.m[k] > kDeferMaxRows) continue;
+          GemmArgs t{};
+          if (nl == 1) { t.part = b->gemm_part; t.part_floats = b->gemm_part_floats; }
+          t.M = ln.m[k]; t.N = D.d; t.ldo = D.d; t.epi = kEpiGatedResidual;
+          const NormArgs nm{b->modtab, D.mod_stride, 0, 0, D.eps, b->u, b->kb_rows};
+          for (int K2 : {D.o_dim, D.dff}) {
+            t.K = K2;
+            if (gemm_defers(t, b->gemm_cfg, &nm)) defer_on = true;
+          }
+        }
+    }
+    const int n_dn = D.qkv_dim + D.dff;
+    if (e == hipSuccess && defer_on)
+      e = timed(b, kcTime, [&] {
+        return launch_shift_proj(b->modtab, D.mod_stride, n_tau, D.L, 6 * D.d, 0, 3 * D.d, D.d, b->wt_qkv, D.qkv_dim,
+                                 b->wt_up, D.dff, b->dn_shift, b->stream);
+      });
     // Fork: every other lane's stream waits for the plan, the modulation table
     // and the row setup.
-    const int nl = (int)p.lanes.size();
     if (e == hipSuccess && nl > 1) {
       e = hipEventRecord(b->ev_fork, b->stream);
       for (int li = 1; li < nl && e == hipSuccess; ++li) e = hipStreamWaitEvent(b->lane_stream[li], b->ev_fork, 0);
@@ -1001,22 +1040,35 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
         const int32_t *row_req = b->row_req + r0;
         e = timed(b, kcInProj, [&] { return launch_in_proj(x, M, D.A, b->w_in, b->b_in, D.d, h, st); });
         const int fshift = D.L * (int)d6, fscale = D.L * (int)d6 + D.d;
+        float *dss = defer_on && M <= kDeferMaxRows ? b->dn_ss + r0 * (D.d / 32) : nullptr;
+        // The deferred norm's producer outputs (t into u) and its completion
+        // in the product that reads u, from this layer's shift table.
+        auto defer_out = [&](GemmArgs &gx, int scale_off) {
+          if (!dss) return;
+          gx.dt = u; gx.dt_rows = R; gx.dss = dss; gx.dscale = b->modtab + scale_off;
+        };
+        auto defer_in = [&](GemmArgs &gx, int l2, int col0) {
+          gx.css = dss; gx.cparts = D.d / 32; gx.cd = D.d; gx.ceps = D.eps; gx.rowmod = rowmod;
+          gx.cshift = b->dn_shift + (size_t)l2 * n_tau * n_dn + col0; gx.cshift_stride = n_dn;
+        };
         // u_ready: the norm that reads the rows just updated was fused into
-        // the split product that updated them (small batches only).
-        bool u_ready = false;
+        // the split product that updated them (small batches only); t_ready:
+        // u holds that norm's deferred form (t, and the row sums in dss).
+        bool u_ready = false, t_ready = false;
         for (int l = 0; l < D.L && e == hipSuccess; ++l) {
           const int base = (int)(l * d6);
-          if (!u_ready)
+          if (!u_ready && !t_ready)
             e = timed(b, kcModNorm, [&] {
               return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base, base + D.d, rowmod, u, b->bf16,
                                     st, R);
             });
-          u_ready = false;
           if (e != hipSuccess) break;
           GemmArgs gq{};
           if (nl == 1) { gq.part = b->gemm_part; gq.part_floats = b->gemm_part_floats; }
           gq.a = u; gq.lda = D.d; gq.a_rows = R; gq.wt = (uint8_t *)b->wt_qkv + (size_t)l * D.qkv_dim * D.d * es;
           gq.M = M; gq.N = D.qkv_dim; gq.K = D.d; gq.epi = kEpiStore; gq.out = qkv; gq.ldo = D.qkv_dim;
+          if (t_ready) defer_in(gq, l, 0);
+          u_ready = t_ready = false;
           e = timed(b, kcGemmQKV, [&] { return launch_gemm(gq, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
           e = run_attention(b, p, ln, k, l, b->qkv, b->o, st, b->kb_rows);
@@ -1027,19 +1079,21 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           go.M = M; go.N = D.d; go.K = D.o_dim; go.epi = kEpiGatedResidual; go.out = h; go.ldo = D.d;
           go.gate = b->modtab + base + 2 * D.d; go.gate_stride = D.mod_stride; go.rowmod = rowmod;
           const NormArgs mlp_norm{b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, D.eps, u, R};
-          e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg, &mlp_norm, &u_ready); });
+          defer_out(go, base + 4 * D.d);
+          e = timed(b, kcGemmO, [&] { return launch_gemm(go, b->bf16, st, b->gemm_cfg, &mlp_norm, &u_ready, &t_ready); });
           if (e != hipSuccess) break;
-          if (!u_ready)
+          if (!u_ready && !t_ready)
             e = timed(b, kcModNorm, [&] {
               return launch_modnorm(h, M, D.d, D.eps, b->modtab, D.mod_stride, base + 3 * D.d, base + 4 * D.d, rowmod,
                                     u, b->bf16, st, R);
             });
-          u_ready = false;
           if (e != hipSuccess) break;
           GemmArgs gu{};
           if (nl == 1) { gu.part = b->gemm_part; gu.part_floats = b->gemm_part_floats; }
           gu.a = u; gu.lda = D.d; gu.a_rows = R; gu.out_rows = R; gu.wt = (uint8_t *)b->wt_up + (size_t)l * D.dff * D.d * es;
           gu.M = M; gu.N = D.dff; gu.K = D.d; gu.epi = kEpiGelu; gu.out = g; gu.ldo = D.dff;
+          if (t_ready) defer_in(gu, l, D.qkv_dim);
+          u_ready = t_ready = false;
           e = timed(b, kcGemmUp, [&] { return launch_gemm(gu, b->bf16, st, b->gemm_cfg); });
           if (e != hipSuccess) break;
           GemmArgs gd{};
@@ -1051,7 +1105,10 @@ rosa_status rosa_generate_steps(rosa_batch *b, const rosa_request *reqs, int32_t
           const bool last = l + 1 == D.L;
           const NormArgs next_norm{b->modtab, D.mod_stride, last ? fshift : base + (int)d6,
                                    last ? fscale : base + (int)d6 + D.d, D.eps, u, R};
-          e = timed(b, kcGemmDown, [&] { return launch_gemm(gd, b->bf16, st, b->gemm_cfg, &next_norm, &u_ready); });
+          if (!last) defer_out(gd, base + (int)d6 + D.d);
+          e = timed(b, kcGemmDown, [&] {
+            return launch_gemm(gd, b->bf16, st, b->gemm_cfg, &next_norm, &u_ready, &t_ready);
+          });
         }
         // Final norm with the final modulation, output projection and Euler step.
         if (e == hipSuccess && b->bf16) {

@@ -152,6 +152,18 @@ struct GemmArgs {
   // kSplitMax blocks per tile: each writes its slice's product here, and a
   // second kernel sums the slices in order and applies the epilogue.
   float *part; size_t part_floats;
+  // Deferred modulated RMSNorm (bf16, unsplit launches only).  A
+  // kEpiGatedResidual launch with dt set also leaves, for the rows it
+  // updates, t = bf16(h (1 + scale)) (scale at dscale[rowmod[m] * gate_stride
+  // + n]; kb32 planes of dt_rows rows) and the sum of squares of each row of h
+  // over every 32-column block, dss[m * (N / 32) + n / 32].  A kEpiStore or
+  // kEpiGelu launch with css set takes such a t as A and completes the norm
+  // in its epilogue: acc / sqrt(ss_m / cd + ceps) + cshift[rowmod[m] *
+  // cshift_stride + n], ss_m the sum of css[m * cparts .. + cparts) (cparts a
+  // multiple of 8, at most 32) and
+  // cshift the norm's shift multiplied by this launch's W, per modulation row.
+  void *dt; int dt_rows; float *dss; const float *dscale;
+  const float *css; int cparts, cd; float ceps; const float *cshift; int cshift_stride;
 };
 constexpr int kSplitMinTiles = 64;
 constexpr int kSplitMinTilesNorm = 128;
@@ -170,8 +182,19 @@ struct NormArgs {
 // is split has the norm fused into the kernel that sums its slices; *normed
 // tells the caller whether that happened (else it launches the norm itself).
 constexpr int kFusedNormMax = 1024;
+// A gated-residual launch with dt set that is not split this way runs
+// unsplit with the deferred norm's outputs (*deferred = true).
 hipError_t launch_gemm(const GemmArgs &g, bool bf16, hipStream_t s, int force_cfg = -1,
-                       const NormArgs *then_norm = nullptr, bool *normed = nullptr);
+                       const NormArgs *then_norm = nullptr, bool *normed = nullptr, bool *deferred = nullptr);
+bool gemm_defers(const GemmArgs &g, int force_cfg, const NormArgs *then_norm);
+// The shift halves of a deferred norm's products: for layer l < L, modulation
+// row r < n_mod and column n, S[(l * n_mod + r) * (Nq + Nu) + n] = sum_k
+// modtab[r * mod_stride + l * layer_stride + q_off + k] * Wq_l[k][n] for n < Nq,
+// and the same with u_off and Wu_l for the Nu columns after them (Wq, Wu:
+// bf16 kb32 [K/32][N][32] per layer, K = d).
+hipError_t launch_shift_proj(const float *modtab, int mod_stride, int n_mod, int L, int layer_stride, int q_off,
+                             int u_off, int d, const void *wq, int Nq, const void *wu, int Nu, float *S,
+                             hipStream_t s);
 // bf16 GEMM with a given block configuration (an index into the launcher's
 // table of kGemmConfigs tiles, from 384 x 128 down to 64 x 32).
 constexpr int kGemmConfigs = 13;

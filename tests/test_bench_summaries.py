@@ -32,6 +32,23 @@ def test_classify_dispatches_split_products_with_fused_norms():
                                                   "attention"]
 
 
+def test_classify_dispatches_deferred_norms():
+    # Large batch: unsplit output and MLP-down products leave the norm to the
+    # product after them (no modnorm launch between layers), and the call's
+    # shift-table kernel and the final norm sit outside the projections.
+    seq = ["shift_proj_kernel", "in_proj_kernel", "modnorm_kernel", "gemm_bf16_kernel<A,0,false>",
+           "attention_bf16_kernel", "gemm_bf16_kernel<B,2,true>", "gemm_bf16_kernel<C,1,true>",
+           "gemm_bf16_kernel<D,2,true>", "gemm_bf16_kernel<A,0,true>", "attention_bf16_kernel",
+           "gemm_bf16_kernel<B,2,true>", "gemm_bf16_kernel<C,1,true>", "gemm_bf16_kernel<D,2,false>",
+           "modnorm_kernel", "out_proj_euler_kernel", "in_proj_kernel", "modnorm_kernel",
+           "gemm_bf16_kernel<A,0,false>"]
+    role = bench._classify_dispatches(_rows(seq))
+    assert [role[i] for i in range(len(seq))] == ["other", "other", "modnorm", "gemm_qkv", "attention", "gemm_o",
+                                                  "gemm_up", "gemm_down", "gemm_qkv", "attention", "gemm_o",
+                                                  "gemm_up", "gemm_down", "modnorm", "other", "other", "modnorm",
+                                                  "gemm_qkv"]
+
+
 def test_visible_keys_counts_the_prefix_lm_mask():
     # brute force over the mask: token t sees key j iff j < max(P - c, t + 1)
     for P in (1, 5, 17):

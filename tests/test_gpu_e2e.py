@@ -141,6 +141,34 @@ def test_pi0_b32_preset_sampled(pi0_expert):
     _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "pi0_b32")
 
 
+def test_factory_first16_deferred_norms(pi0_expert):
+    """Sixteen robots (528 rows): every output projection and MLP-down either
+    folds the next norm into its K-slice reduction or defers it to the next
+    product, so the only norm launches left are each step's first; four
+    requests (one per horizon x steps class) against the oracle."""
+    e, w = pi0_expert
+    p = PRESETS["factory_b256"]
+    reqs = make_requests(p, indices=list(range(16)))
+    meta = make_metadata(p)[:16]
+    db = _rosa().DeviceBatch(reqs, "bf16")
+    e.set_profiling(True)
+    try:
+        e.generate(db.structs)
+        torch.cuda.synchronize()
+        prof = e.profile()
+    finally:
+        e.set_profiling(False)
+    k_max = max(m.steps for m in meta)
+    assert prof["modnorm"][0] == k_max, prof["modnorm"]
+    # the time MLP's four launches and the shift table of the deferred norms
+    assert prof["time_conditioning"][0] == 5, prof["time_conditioning"]
+    got = db.results()
+    pick = []
+    for cls in sorted({(m.horizon, m.steps) for m in meta}):
+        pick.append(next(i for i, m in enumerate(meta) if (m.horizon, m.steps) == cls))
+    _check([got[i] for i in pick], [reqs[i] for i in pick], w, PI0_SHAPE, 1e-2, "factory first 16")
+
+
 @pytest.mark.timeout(900)
 def test_factory_b256_attention_isolating_both_lanes():
     """The benchmark's whole batch with the MLP removed and the attention gate
