@@ -424,7 +424,8 @@ def _summarize_call_trace(out, sub):
              "about the kernel time: the tracer widens the gaps between dependent launches).  Per layer-step "
              "the call launches QKV, attention (and, for split key ranges, their merge), the output "
              "projection, MLP up and MLP down, with the two modulated norms either as launches of their own "
-             "or, after a K-split output or MLP-down projection, fused into its slice reduction.", "",
+             "or, after a K-split output or MLP-down projection, fused into its slice reduction, or, "
+             "after an unsplit one of at most 1,024 rows, completed in the next product's epilogue.", "",
              "| Kernel | Launches | Avg (us) | Min (us) | Total (ms) | Avg gap before (us) |",
              "|---|---:|---:|---:|---:|---:|"]
     for name, v in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
