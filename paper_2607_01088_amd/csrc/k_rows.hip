@@ -302,86 +302,86 @@ hipError_t launch_final_euler(const float *h, int M, int d, float eps, const flo
 
 // ------------------------------------------------------------------ output projection + Euler (bf16)
 // v = u W_out + b_out on the final-normalized rows u (bf16, from modnorm), then
-// x += v / K and, on the request's last step of this call, x is written to its actions.
-// W_out^T (bf16 [A][d], rows past A read as zero) is staged in LDS in chunks of
-// KC columns, each row's 16-byte chunks XOR-swizzled by row % 16 so that the 32
-// rows one MFMA operand read touches fall in distinct bank groups.  Each wave
-// takes 32-row blocks of u: A operand straight from global memory (16 bytes per
-// lane), B operand from LDS, v_mfma_f32_32x32x16_bf16, NB blocks of 32 outputs.
+// x += v / K and, on the request's last step of this call, x is written to its
+// actions.  One block per 32-row block of u; its four waves take a quarter of
+// K (= d) each, loading their quarter of the rows' u (A operand) and of W_out^T
+// (B operand, bf16 [A][d], rows past A read as zero) straight into registers,
+// kOutKS k-steps at a time with every load issued before the first MFMA
+// (v_mfma_f32_32x32x16_bf16, NB blocks of 32 outputs).  The four partial
+// products meet in LDS and are summed in wave order.  The Euler update's
+// inputs (each output's request and state) are loaded before the products.
+constexpr int kOutKS = 16;
 template <int NB>
-__global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restrict__ u, int M, int d, int KC,
+__global__ void __launch_bounds__(256) out_proj_euler_kernel(const bf16 *__restrict__ u, int M, int d,
                                                              const bf16 *__restrict__ wt, const float *__restrict__ b_out,
                                                              int A, const int32_t *__restrict__ row_req,
                                                              const ReqDesc *__restrict__ reqs, int step,
                                                              float *__restrict__ x, int row0, int u_rows) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds_out[];
+  __shared__ float part[4][NB][32 * 32];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, l32 = lane & 31;
-  const int cpr = KC / 8;                       // 16-byte chunks per LDS row
-  const int nrb = (M + 31) / 32;
-  const int nchunk = d / KC;
-  for (int base = blockIdx.x * 4; base < nrb; base += gridDim.x * 4) {   // block-uniform
-    const int rb = base + wave;
-    const int arow = min(rb * 32 + l32, M - 1);
-    f32x16 acc[NB];
+  const int rb = blockIdx.x;
+  const int arow = min(rb * 32 + l32, M - 1);
+  const int kq = d / 4, kbeg = wave * kq, kend = kbeg + kq;
+  // Outputs e = tid + 256 i of the block's 32 x 32 NB: their requests' step
+  // count, steps of this call and first row, and the current state.
+  constexpr int NE = NB * 4;
+  float xv[NE], invk[NE];
+  int last[NE], arow0[NE];
+  float *act[NE];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
-    for (int c = 0; c < nchunk; ++c) {
-      if (nchunk > 1 || base == (int)blockIdx.x * 4) {
-        __syncthreads();                        // previous chunk consumed
-        for (int i = tid; i < NB * 32 * cpr; i += 256) {
-          const int r = i / cpr, ch = i % cpr;
-          uint4 v = make_uint4(0, 0, 0, 0);
-          if (r < A) v = *reinterpret_cast<const uint4 *>(wt + (size_t)r * d + c * KC + ch * 8);
-          *reinterpret_cast<uint4 *>(lds_out + ((size_t)r * cpr + (ch ^ (r & 15))) * 16) = v;
-        }
-        __syncthreads();
-      }
-      for (int k0 = 0; k0 < KC / 16; k0 += 8) {
-        bf16x8 af[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int k = c * KC + (k0 + j) * 16 + half * 8;   // 8 values inside one 32-wide block
-          af[j] = *reinterpret_cast<const bf16x8 *>(u + (u_rows > 0 ? kb32_offset(u_rows, arow, k) : (size_t)arow * d + k));
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int ch = 2 * (k0 + j) + half;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
-            const int r = nb * 32 + l32;
-            const bf16x8 bfr = *reinterpret_cast<const bf16x8 *>(lds_out + ((size_t)r * cpr + (ch ^ (r & 15))) * 16);
-            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[j], bfr, acc[nb], 0, 0, 0);
-          }
-        }
-      }
-    }
-    if (rb >= nrb) continue;
-    // Lane holds output column nb 32 + lane % 32 of rows (r/4) 8 + 4 half + r%4.
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int col = nb * 32 + l32;
-      if (col >= A) continue;
-      const float bias = b_out[col];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = rb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-        if (row >= M) continue;
-        const ReqDesc q = reqs[row_req[row]];
-        const float v = acc[nb][r] + bias;
-        const float xn = x[(size_t)row * A + col] + (1.0f / (float)q.K) * v;
-        x[(size_t)row * A + col] = xn;
-        if (step == q.S - 1) q.actions[(size_t)(row0 + row - q.tok_off) * A + col] = xn;
-      }
+  for (int i = 0; i < NE; ++i) {
+    const int e = tid + 256 * i, row = rb * 32 + ((e & 1023) >> 5), col = (e >> 10) * 32 + (e & 31);
+    xv[i] = 0.f; invk[i] = 0.f; last[i] = 0; arow0[i] = 0; act[i] = nullptr;
+    if (col < A && row < M) {
+      const ReqDesc *q = reqs + row_req[row];
+      xv[i] = x[(size_t)row * A + col];
+      invk[i] = 1.0f / (float)q->K;
+      last[i] = step == q->S - 1;
+      arow0[i] = row0 + row - q->tok_off;
+      act[i] = q->actions;
     }
   }
-}
-
-size_t out_proj_lds_bytes(int d, int A) {
-  const int nb = A <= 32 ? 1 : 2;
-  const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
-  return (size_t)nb * 32 * kc * 2;
+  f32x16 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+  for (int k0 = kbeg; k0 < kend; k0 += 16 * kOutKS) {
+    bf16x8 af[kOutKS], bfr[NB][kOutKS];
+#pragma unroll
+    for (int j = 0; j < kOutKS; ++j) {
+      const int k = k0 + 16 * j + 8 * half;                 // 8 values inside one 32-wide block
+      const bool in = k0 + 16 * j < kend;
+      af[j] = in ? *reinterpret_cast<const bf16x8 *>(u + (u_rows > 0 ? kb32_offset(u_rows, arow, k) : (size_t)arow * d + k))
+                 : bf16x8{};
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int col = nb * 32 + l32;
+        bfr[nb][j] = in && col < A ? *reinterpret_cast<const bf16x8 *>(wt + (size_t)col * d + k) : bf16x8{};
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kOutKS; ++j)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[j], bfr[nb][j], acc[nb], 0, 0, 0);
+  }
+  // Lane holds output column nb 32 + lane % 32 of rows (r/4) 8 + 4 half + r%4.
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) part[wave][nb][((r >> 2) * 8 + half * 4 + (r & 3)) * 32 + l32] = acc[nb][r];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NE; ++i) {
+    const int e = tid + 256 * i, row = rb * 32 + ((e & 1023) >> 5), col = (e >> 10) * 32 + (e & 31);
+    if (col >= A || row >= M) continue;
+    const float *pp = &part[0][0][0] + e;
+    const float sum = ((pp[0] + pp[NB * 1024]) + pp[2 * NB * 1024]) + pp[3 * NB * 1024];
+    const float v = sum + b_out[col];
+    const float xn = xv[i] + invk[i] * v;
+    x[(size_t)row * A + col] = xn;
+    if (last[i]) act[i][(size_t)arow0[i] * A + col] = xn;
+  }
 }
 
 hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, const float *b_out, int A,
@@ -389,24 +389,13 @@ hipError_t launch_out_proj_euler(const bf16 *u, int M, int d, const bf16 *wt, co
                                  hipStream_t s, int u_rows) {
   if (M <= 0) return hipSuccess;
   if (d % 128 || A < 1 || A > 64 || (u_rows > 0 && u_rows < M)) return hipErrorInvalidValue;
-  const int nb = A <= 32 ? 1 : 2;
-  const int kc = (size_t)nb * 32 * d * 2 <= kLdsMax - 4096 ? d : 128;
-  const size_t lds = (size_t)nb * 32 * kc * 2;
-  static std::atomic<bool> lds_raised[2];   // zero-initialized (static storage)
-  if (!lds_raised[nb - 1].load(std::memory_order_acquire)) {
-    const hipError_t e = hipFuncSetAttribute(nb == 1 ? (const void *)out_proj_euler_kernel<1> : (const void *)out_proj_euler_kernel<2>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-    if (e != hipSuccess) return e;
-    lds_raised[nb - 1].store(true, std::memory_order_release);
-  }
   const int nrb = (M + 31) / 32;
-  const int blocks = std::min((nrb + 3) / 4, 256);
-  if (nb == 1)
-    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req,
-                       reqs, step, x, row0, u_rows);
+  if (A <= 32)
+    hipLaunchKernelGGL(out_proj_euler_kernel<1>, dim3(nrb), dim3(256), 0, s, u, M, d, wt, b_out, A, row_req, reqs,
+                       step, x, row0, u_rows);
   else
-    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(blocks), dim3(256), lds, s, u, M, d, kc, wt, b_out, A, row_req,
-                       reqs, step, x, row0, u_rows);
+    hipLaunchKernelGGL(out_proj_euler_kernel<2>, dim3(nrb), dim3(256), 0, s, u, M, d, wt, b_out, A, row_req, reqs,
+                       step, x, row0, u_rows);
   return hipGetLastError();
 }
 
