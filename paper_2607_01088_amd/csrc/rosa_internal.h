@@ -64,7 +64,7 @@ constexpr int kAttnSplitTarget = 256;
 // Persistent blocks of the bf16 attention kernel per launch: two per compute
 // unit of a 256-CU MI355X.
 constexpr int kAttnBlocks = 512;
-constexpr int kAttnMinSplitKeys = 128;
+constexpr int kAttnMinSplitKeys = 64;
 constexpr int kAttnMaxSlots = 2 * kAttnSplitTarget;
 constexpr int kMaxTau = 128;       // distinct flow times per call
 constexpr int kMaxSteps = 64;

@@ -64,7 +64,7 @@ def test_plan_sorts_by_steps_and_prefixes_active_tokens():
     n_tau, n_items, n_qb, n_split = counts
     assert n_tau == 10                                   # {k/5} is a subset of {k/10}
     assert n_qb == 1 + 4 + 1 + 4                         # ceil(8H/128) per request
-    # a small batch splits long key ranges (>= 128 keys per item); short ones stay whole
+    # a small batch splits long key ranges (>= 64 keys per item); short ones stay whole
     assert n_items > n_qb and n_split > 0
 
 
@@ -223,7 +223,7 @@ def test_plan_alternating_layout():
     st, *_ = _plan([req(5, 8, 5), req(0, 8, 5, k=None, v=None)], shape=PI0_ALT_SHAPE)
     assert st == rosa.ROSA_E_INVALID
     # small batch: the prefix keys split over items (partial slots), the
-    # 50 self-attention keys (fewer than the 128 a split item needs) do not
+    # 50 self-attention keys (fewer than the 64 a split item needs) do not
     st, _, _, _, counts = _plan([req(1200, 50, 10)], shape=PI0_ALT_SHAPE)
     assert st == rosa.ROSA_OK
     assert counts[3] == counts[2] and counts[1] > 2 * counts[2]
