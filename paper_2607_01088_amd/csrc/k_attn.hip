@@ -7,18 +7,17 @@
 //
 // bf16 kernel (gfx950 MFMA).  A work item is (request, KV head, up to 128 NG
 // query rows, key range).  Its four waves stream the key range through LDS in
-// 32-key tiles: a K ring and a V ring of four stages each, filled by
-// global_load_lds_dwordx4 with two copy groups in flight.  Each wave owns NG
-// groups of 32 query rows (groups w and w + 4 of the item), so every K and V
-// fragment it reads from LDS feeds the MFMAs of all its groups; NG is 2 where
-// Q^T and O^T of two groups fit the register file (head_dim <= 128) and 1
-// otherwise.  Step t computes S^T = K Q^T of tile t with
-// v_mfma_f32_32x32x16_bf16 (K from LDS, Q^T held in registers for the whole
-// item; each lane owns one query column, so softmax statistics are in-lane)
-// and O^T += V^T P^T of tile t - 1 (P^T from registers, V^T from the
-// row-major V tile through the LDS transpose read ds_read_b64_tr_b16), with
-// the softmax of tile t interleaved between the PV MFMAs.  Every MFMA's LDS
-// operand is read two fragments ahead.  The softmax uses a fixed reference
+// 32-key tiles: a K ring of three stages and a V ring of two, filled by
+// global_load_lds_dwordx4 (step t issues V tile t + 1 and K tile t + 2).
+// Each wave owns NG groups of 32 query rows (groups w and w + 4 of the item),
+// so every K and V fragment it reads from LDS feeds the MFMAs of all its
+// groups; NG is 2 where Q^T and O^T of two groups fit the register file
+// (head_dim <= 64) and 1 otherwise.  Step t computes S^T = K Q^T of tile t
+// with v_mfma_f32_32x32x16_bf16 (K from LDS, Q^T held in registers for the
+// whole item; each lane owns one query column, so softmax statistics are
+// in-lane), its softmax, and O^T += V^T P^T (P^T from registers, V^T from
+// the row-major V tile through the LDS transpose read ds_read_b64_tr_b16).
+// Every MFMA's LDS operand is read two fragments ahead.  The softmax uses a fixed reference
 // max per query (its first tile's), so the output accumulators are never
 // rescaled; a block whose later scores overshoot that reference runs again
 // with the true max.  Work items that cover part of a request's keys write
